@@ -1,0 +1,183 @@
+#!/usr/bin/env python3
+"""Benchmark of the batched kernel-latency evaluator on one MI355X.
+
+One benchmark step = one ks_eval_steps call: every stage of the path (record
+stream, exact counts, waves, roofline, features, efficiency head on MFMA,
+launch floor, per-step sums, all-reduce and step assembly) for every
+(spec vector, record) pair of the workload.  Inputs are resident in HBM
+before the timed region; only the library call is timed (HIP events on the
+stream it launches on).
+
+Default workload: the capacity-planning grid — the Llama-7B trace (1000
+steps) plus the first 345 steps of the six-shape S2 trace, 390,050 kernel
+records x 256 hypothetical spec vectors = 99.9 M latency predictions per
+step, bf16 16->128->128->1 heads.
+
+Prints one JSON line (see the keys below)."""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import subprocess
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "kernel latency predictions/sec and step evals/sec at 1 GPU; % of HBM/MFMA peak"
+PEAK = {"bf16": 2.5e15, "f32": 157.3e12, "hbm": 8.0e12}
+
+
+def _workload(name: str):
+    from workload import gen
+    if name == "c4":
+        return gen.config4(), "c4-capacity-grid: llama-7b c1 trace + S2 trace prefix, 256 specs"
+    if name == "c1":
+        return gen.config1(), "c1-llama7b: 1000 steps, 2 datasheet specs, fp32 heads"
+    if name == "c5-batch":
+        wl = gen.config5(0, 2000)
+        return wl, "c5-70b-prefix: first 2000 steps, 2 datasheet specs, bf16 32-256-256 heads"
+    raise SystemExit(f"unknown workload {name}")
+
+
+def head_flops_per_pair(in_dim: int, hidden: int) -> int:
+    """Algorithmic MLP FLOPs of one prediction: 2 (in h + h h + h)."""
+    return 2 * (in_dim * hidden + hidden * hidden + hidden)
+
+
+def cpu_baseline(wl, n_spec_sample: int, threads: int):
+    """The oracle as it stands, on all records x the first n_spec_sample
+    spec vectors (a bounded sample of the same workload)."""
+    from threadpoolctl import threadpool_limits
+    from oracle import ks_oracle as o
+    spec_ids = list(range(min(n_spec_sample, wl.n_specs)))
+    with threadpool_limits(limits=threads):
+        t = time.perf_counter()
+        k = o.eval_kernels(wl.desc, wl.specs, wl.heads, spec_ids=spec_ids)
+        o.eval_steps(wl.desc, wl.steps, wl.specs, wl.host, wl.heads, spec_ids=spec_ids, kern=k)
+        dt = time.perf_counter() - t
+    pairs = wl.desc.n_rows * len(spec_ids)
+    return {"value": pairs / dt, "unit": "predictions/s", "cores": threads, "kind": "oracle",
+            "sample": f"all {wl.desc.n_rows} records x {len(spec_ids)} of {wl.n_specs} spec vectors "
+                      f"({pairs} predictions, {dt:.1f} s, fp64 numpy, {threads} BLAS threads)"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c4", choices=["c4", "c1", "c5-batch"])
+    ap.add_argument("--eta-one", action="store_true", help="eta = 1 (pure roofline) mode")
+    ap.add_argument("--per-pair", action="store_true", help="also write per-pair t_roof/eta/t_kernel")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-specs", type=int, default=2)
+    ap.add_argument("--cpu-threads", type=int, default=0)
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build evaluates on one GPU only (the path shards by step ranges "
+              "or spec vectors with no exchange; see the design notes); run with --gpus 1",
+              file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_2606_28565_amd import abi
+
+    if not os.path.exists(abi.LIB_PATH):
+        from paper_2606_28565_amd import build as b
+        b.build()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+
+    print(f"[bench] generating workload {args.workload}", file=sys.stderr, flush=True)
+    wl, wdesc = _workload(args.workload)
+    di = abi.DeviceInputs(wl)
+    heads = di.make_heads(wl.heads.precision, wl.heads.in_dim, wl.heads.hidden,
+                          abi.KS_ETA_ONE if args.eta_one else abi.KS_ETA_MLP)
+    so_t, so = abi.step_outputs(wl.desc.n_steps, di.n_specs)
+    if args.per_pair:
+        ko_t, ko = abi.kernel_outputs(wl.desc.n_rows, di.n_specs, counts=False)
+    else:
+        ko = None
+    stream = abi.current_stream()
+
+    def step():
+        abi.ks_eval_steps(di.desc, di.steps, di.specs_ptr, di.n_specs, heads, di.host, so, ko,
+                          di.ws_ptr, di.ws_bytes, stream)
+
+    print(f"[bench] {wl.desc.n_rows} records x {di.n_specs} specs; warmup {args.warmup}",
+          file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    abi.ks_device_status(di.ws_ptr, di.ws_bytes, stream)
+    cs = torch.cuda.current_stream()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(cs)
+    for _ in range(args.steps):
+        step()
+    ev1.record(cs)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    print(f"[bench] {args.steps} steps: {ms:.3f} ms/step", file=sys.stderr, flush=True)
+
+    pairs = wl.desc.n_rows * di.n_specs
+    value = pairs / (ms * 1e-3)
+    step_evals = wl.desc.n_steps * di.n_specs / (ms * 1e-3)
+    if args.eta_one:
+        # record stream: 6 u32 fields in, and for every pair nothing but the
+        # step partial; traffic is the records (24 B) read once
+        alg = wl.desc.n_rows * 24.0
+        bound, unit, peak = "hbm", "GB/s", PEAK["hbm"] / 1e9
+        achieved = alg / (ms * 1e-3) / 1e9
+        dtype = "f32"
+    else:
+        per_pair = head_flops_per_pair(wl.heads.in_dim, wl.heads.hidden)
+        alg = float(pairs) * per_pair
+        bf16 = wl.heads.precision == "bf16"
+        bound, unit = "mfma", "TFLOP/s"
+        peak = (PEAK["bf16"] if bf16 else PEAK["f32"]) / 1e12
+        achieved = alg / (ms * 1e-3) / 1e12
+        dtype = "bf16" if bf16 else "f32"
+
+    out = {
+        "metric": METRIC, "value": value, "unit": "predictions/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": dtype, "data": "synthetic",
+        "config": {"workload": wdesc, "records": wl.desc.n_rows, "spec_vectors": di.n_specs,
+                   "serving_steps": wl.desc.n_steps, "predictions_per_step": pairs,
+                   "head": ("eta=1" if args.eta_one else
+                            f"{wl.heads.precision} {wl.heads.in_dim}-{wl.heads.hidden}-{wl.heads.hidden}-1"),
+                   "per_pair_outputs": bool(args.per_pair)},
+        "step_evals_per_s": step_evals,
+        "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
+                     "frac": achieved / peak, "traffic": None,
+                     "note": "achieved = algorithmic work of the evaluation kernel per call / "
+                             "HIP-event time of the whole call (all five kernels)"},
+    }
+    if not args.no_cpu_baseline:
+        threads = args.cpu_threads or min(16, os.cpu_count() or 1)
+        print(f"[bench] cpu baseline: oracle, {args.cpu_specs} specs, {threads} threads",
+              file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_specs, threads)
+        try:
+            model = subprocess.run(["lscpu"], capture_output=True, text=True).stdout
+            model = [l.split(":", 1)[1].strip() for l in model.splitlines() if l.startswith("Model name")]
+            out["cpu_baseline"]["cpu_model"] = model[0] if model else platform.processor()
+        except OSError:
+            pass
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

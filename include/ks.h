@@ -1,0 +1,200 @@
+/*
+ * ks.h — C ABI of the MI355X (gfx950) batched kernel-latency evaluator.
+ *
+ * The library evaluates the per-kernel latency model of KernelSight-LM
+ * (arXiv 2606.28565) for every (hardware spec vector, dispatched-kernel
+ * record) pair and aggregates the kernels into per-step latencies:
+ *
+ *   t      = max(t_roof * eta, t0),                    Eq. 2 (Sec. 5.3)
+ *   t_roof = max(F * u / P_peak, Bt / BW_peak),        Eq. 2
+ *   u      = ceil(B / N_cu) * N_cu / B,                Sec. 2.2
+ *   eta    = 1 / sigma(z) = 1 + exp(-z), z from a per-family MLP head on
+ *            dimensionless features,                   Sec. 5.3
+ *   t_ar   = alpha0(P) + 2 (P - 1) / P * S / beta,     Eq. 3 (Sec. 5.6)
+ *   t_step = max(t_gpu + n c_disp, l) + max(0, c_ovl - t_gpu) + c_tail,
+ *                                                      Eq. 4 (Sec. 5.7)
+ *
+ * Conventions (all entry points):
+ *  - Pointers named "device" are device memory owned by the caller; the
+ *    library never allocates, frees or keeps them after the call returns.
+ *    Structs themselves are read on the host during the call only.
+ *  - Work is enqueued asynchronously on the caller's HIP stream; outputs are
+ *    valid once that stream has completed the call's work.  Concurrent calls
+ *    that share a workspace race.
+ *  - Errors are returned as ks_status (never thrown, never abort); the
+ *    thread-local message of the last failing call is ks_last_error().
+ *  - Host-side checks run before any launch.  Conditions that depend on
+ *    device data (ranges, sortedness, offsets) are checked synchronously by
+ *    ks_validate(); the evaluation kernels themselves never read or write out
+ *    of bounds on bad data: they skip the offending record and raise a flag
+ *    that ks_device_status() reports.
+ *  - Units: seconds, FLOP/s, bytes, bytes/s.
+ */
+#ifndef KS_H
+#define KS_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  KS_OK = 0,
+  KS_EINVAL = 1,      /* bad argument: null pointer, bad size, unsorted data */
+  KS_ERANGE = 2,      /* a shape or count outside the documented limits      */
+  KS_EHIP = 3,        /* a HIP runtime call failed                           */
+  KS_EWORKSPACE = 4   /* workspace missing or smaller than required          */
+} ks_status;
+
+/* Kernel families (Sec. 5.3 learns eta per family). */
+enum {
+  KS_GEMM = 0, KS_LM_HEAD, KS_GROUPED_GEMM, KS_ATTN_PREFILL, KS_ATTN_DECODE,
+  KS_RMSNORM, KS_ROPE, KS_SILU_MUL, KS_KV_WRITE, KS_EMBED, KS_NFAM
+};
+
+/*
+ * Dispatched-kernel records (the predictor's per-kernel input, Sec. 4.1),
+ * structure of arrays, family-major: records [fam_off[f], fam_off[f+1]) all
+ * belong to family f, and within a family their step indices never
+ * decrease.  Field meaning per family (unused fields are ignored):
+ *
+ *   GEMM, LM_HEAD   m = M, n = N, k = K
+ *   GROUPED_GEMM    n = N, k = K, a = E experts, b = offset of the E
+ *                   per-expert row counts M_e in expert_rows
+ *   ATTN_PREFILL,   n = H query heads, k = head dim d, a = Hkv KV heads;
+ *   ATTN_DECODE     the queries are the requests of the record's step
+ *                   (Sec. 5.8: each decode over its context, a prefill chunk
+ *                   over its history plus its causal triangle)
+ *   RMSNORM         m = T tokens, n = D
+ *   ROPE            m = T, n = rotated heads, k = d
+ *   SILU_MUL        m = T rows, n = I output width
+ *   KV_WRITE        m = T, n = Hkv, k = d
+ *   EMBED           m = T, n = D
+ *
+ * The batch descriptor of each step (Sec. 4.1) is its request list:
+ * requests [req_off[j], req_off[j+1]) with q_r query tokens and h_r cached
+ * history tokens.  Limits (KS_ERANGE): n_rows < 2^32; m < 2^24; n, k < 2^18;
+ * attention n, k, a < 2^12; q_r, h_r < 2^24; per-step causal pairs < 2^40;
+ * sum of a grouped record's M_e < 2^24; E <= 1024; elem_bytes in 1..8.
+ */
+typedef struct ks_desc {
+  int64_t n_rows;
+  int64_t fam_off[KS_NFAM + 1];          /* host array, fam_off[0] = 0       */
+  const uint32_t *step;                  /* device [n_rows]                  */
+  const uint32_t *m, *n, *k, *a, *b;     /* device [n_rows]                  */
+  int64_t n_steps;
+  const uint32_t *req_off;               /* device [n_steps + 1], req_off[0] = 0 */
+  const uint32_t *req_q, *req_h;         /* device [n_req]                   */
+  int64_t n_req;
+  const uint32_t *expert_rows;           /* device [n_expert_rows] or NULL   */
+  int64_t n_expert_rows;
+  uint32_t elem_bytes;                   /* dt, bytes per element (2 = bf16) */
+  uint32_t reserved;
+} ks_desc;
+
+/*
+ * One hardware spec vector (Tier A datasheet, Sec. 5.4) and its interconnect
+ * (Sec. 5.6).  Passed as a DEVICE array of n_specs records (64 bytes each).
+ * alpha0(P) = ar_alpha0 + ar_alpha_log2p * log2(P).
+ */
+typedef struct ks_spec {
+  double peak_flops;       /* P_peak, FLOP/s, > 0                     */
+  double hbm_bw;           /* BW_peak, bytes/s, > 0                   */
+  double t0;               /* launch floor, s, >= 0                   */
+  double l2_bytes;         /* L2 capacity, bytes, >= 0                */
+  double ar_alpha0;        /* all-reduce startup, s                   */
+  double ar_alpha_log2p;   /* startup growth per doubling of P, s     */
+  double ar_beta;          /* effective interconnect bandwidth, B/s   */
+  uint32_t n_cu;           /* N_SM, 1 .. 65535                        */
+  uint32_t reserved;
+} ks_spec;
+
+enum { KS_F32 = 0, KS_BF16 = 1 };
+enum { KS_ETA_MLP = 0, KS_ETA_ONE = 1 };
+
+/*
+ * Per-family efficiency heads (Sec. 5.3), device arrays, row-major [out][in]:
+ *   w1 [KS_NFAM][hidden][in_dim]   (no first-layer bias: feature 15 is 1)
+ *   w2 [KS_NFAM][hidden][hidden], b2 [KS_NFAM][hidden]
+ *   w3 [KS_NFAM][hidden],         b3 [KS_NFAM]
+ * Element type float for KS_F32, bfloat16 bits (uint16) for KS_BF16.
+ * z = w3 . relu(W2 relu(W1 x) + b2) + b3;  eta = 1 + exp(-z).
+ * Supported: in_dim 16 or 32; hidden 64 or 128 (KS_F32), 64, 128 or 256
+ * (KS_BF16).  mode KS_ETA_ONE ignores every other field (eta = 1).
+ */
+typedef struct ks_heads {
+  int32_t in_dim, hidden, precision, mode;
+  const void *w1, *w2, *b2, *w3, *b3;
+} ks_heads;
+
+/* Per-step model record, device arrays [n_steps]. */
+typedef struct ks_steps {
+  int64_t n_steps;                 /* must equal ks_desc.n_steps               */
+  const uint32_t *layers;          /* L                                        */
+  const uint32_t *hidden;          /* D (all-reduce message S = T * D * dt)    */
+  const uint32_t *tp;              /* P (1: no all-reduce)                     */
+  const uint32_t *n_launch;        /* n of Eq. 4: host launches priced c_disp  */
+} ks_steps;
+
+/* Host constants of Eq. 4 (host memory, read during the call). */
+typedef struct ks_host {
+  double c_disp, ell, c_ovl, c_tail, body_scale;
+} ks_host;
+
+/* Per-record and per-pair outputs (device; any pointer may be NULL = skip).
+ * flops, bytes, blocks: [n_rows]; t_roof, eta, t_kernel: [n_specs][n_rows]. */
+typedef struct ks_kernel_out {
+  uint64_t *flops, *bytes, *blocks;
+  float *t_roof, *eta, *t_kernel;
+} ks_kernel_out;
+
+/* Per-step outputs (device, [n_specs][n_steps], none may be NULL). */
+typedef struct ks_step_out {
+  double *t_body, *t_gpu, *t_step;
+} ks_step_out;
+
+/* Bytes of device workspace ks_eval_kernels / ks_eval_steps / ks_validate
+ * need for this record set and spec count (256-byte aligned).  0 on bad
+ * arguments. */
+size_t ks_workspace_bytes(const ks_desc* desc, int32_t n_specs);
+
+/* Per-pair latencies (Eq. 2) for every spec vector and record.  ws: device
+ * workspace of at least ks_workspace_bytes() bytes. */
+ks_status ks_eval_kernels(const ks_desc* desc, const ks_spec* specs, int32_t n_specs,
+                          const ks_heads* heads, const ks_kernel_out* out,
+                          void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Per-step latencies (Sec. 5.6–5.7, Eq. 3–4) for every spec vector, plus
+ * optional per-pair outputs (kout may be NULL).  Every record of a step must
+ * be in desc. */
+ks_status ks_eval_steps(const ks_desc* desc, const ks_steps* steps,
+                        const ks_spec* specs, int32_t n_specs,
+                        const ks_heads* heads, const ks_host* host,
+                        const ks_step_out* out, const ks_kernel_out* kout,
+                        void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Synchronous device-side check of the inputs: step order within families,
+ * field limits, request and expert offsets, spec sanity.  Synchronizes the
+ * stream.  Returns KS_OK, KS_EINVAL or KS_ERANGE with a message. */
+ks_status ks_validate(const ks_desc* desc, const ks_steps* steps,
+                      const ks_spec* specs, int32_t n_specs,
+                      void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Synchronizes the stream and reports the flag the evaluation kernels raise
+ * when they skipped a record on bad data since the workspace's last
+ * evaluation call started (KS_OK if none). */
+ks_status ks_device_status(const void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Message of the last non-OK status returned on this thread. */
+const char* ks_last_error(void);
+
+/* Library version string. */
+const char* ks_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* KS_H */

@@ -1,0 +1,278 @@
+"""ctypes binding of the C ABI in include/ks.h (libks.so).
+
+Argument marshalling only: every stage of the evaluation runs in the HIP
+kernels of libks.so.  torch owns the device memory and supplies the stream.
+There is no fallback: if the library is missing or fails to load, the
+import of the entry points raises."""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libks.so")
+
+NFAM = 10
+KS_OK, KS_EINVAL, KS_ERANGE, KS_EHIP, KS_EWORKSPACE = range(5)
+KS_F32, KS_BF16 = 0, 1
+KS_ETA_MLP, KS_ETA_ONE = 0, 1
+STATUS_NAMES = {0: "KS_OK", 1: "KS_EINVAL", 2: "KS_ERANGE", 3: "KS_EHIP", 4: "KS_EWORKSPACE"}
+
+P = C.c_void_p
+
+
+class ks_desc(C.Structure):
+    _fields_ = [("n_rows", C.c_int64), ("fam_off", C.c_int64 * (NFAM + 1)),
+                ("step", P), ("m", P), ("n", P), ("k", P), ("a", P), ("b", P),
+                ("n_steps", C.c_int64), ("req_off", P), ("req_q", P), ("req_h", P),
+                ("n_req", C.c_int64), ("expert_rows", P), ("n_expert_rows", C.c_int64),
+                ("elem_bytes", C.c_uint32), ("reserved", C.c_uint32)]
+
+
+class ks_spec(C.Structure):
+    _fields_ = [("peak_flops", C.c_double), ("hbm_bw", C.c_double), ("t0", C.c_double),
+                ("l2_bytes", C.c_double), ("ar_alpha0", C.c_double),
+                ("ar_alpha_log2p", C.c_double), ("ar_beta", C.c_double),
+                ("n_cu", C.c_uint32), ("reserved", C.c_uint32)]
+
+
+class ks_heads(C.Structure):
+    _fields_ = [("in_dim", C.c_int32), ("hidden", C.c_int32), ("precision", C.c_int32),
+                ("mode", C.c_int32), ("w1", P), ("w2", P), ("b2", P), ("w3", P), ("b3", P)]
+
+
+class ks_steps(C.Structure):
+    _fields_ = [("n_steps", C.c_int64), ("layers", P), ("hidden", P), ("tp", P), ("n_launch", P)]
+
+
+class ks_host(C.Structure):
+    _fields_ = [("c_disp", C.c_double), ("ell", C.c_double), ("c_ovl", C.c_double),
+                ("c_tail", C.c_double), ("body_scale", C.c_double)]
+
+
+class ks_kernel_out(C.Structure):
+    _fields_ = [("flops", P), ("bytes", P), ("blocks", P),
+                ("t_roof", P), ("eta", P), ("t_kernel", P)]
+
+
+class ks_step_out(C.Structure):
+    _fields_ = [("t_body", P), ("t_gpu", P), ("t_step", P)]
+
+
+assert C.sizeof(ks_spec) == 64
+
+
+class KsError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> C.CDLL:
+    """Load libks.so (built by ``paper_2606_28565_amd.build``)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with "
+                           "`python -m paper_2606_28565_amd.build` (there is no fallback)")
+    lib = C.CDLL(path)
+    pd, pst, psp, ph, phost, pko, pso = (C.POINTER(ks_desc), C.POINTER(ks_steps),
+                                          P, C.POINTER(ks_heads), C.POINTER(ks_host),
+                                          C.POINTER(ks_kernel_out), C.POINTER(ks_step_out))
+    lib.ks_workspace_bytes.argtypes = [pd, C.c_int32]
+    lib.ks_workspace_bytes.restype = C.c_size_t
+    lib.ks_eval_kernels.argtypes = [pd, psp, C.c_int32, ph, pko, P, C.c_size_t, P]
+    lib.ks_eval_kernels.restype = C.c_int
+    lib.ks_eval_steps.argtypes = [pd, pst, psp, C.c_int32, ph, phost, pso, pko, P, C.c_size_t, P]
+    lib.ks_eval_steps.restype = C.c_int
+    lib.ks_validate.argtypes = [pd, pst, psp, C.c_int32, P, C.c_size_t, P]
+    lib.ks_validate.restype = C.c_int
+    lib.ks_device_status.argtypes = [P, C.c_size_t, P]
+    lib.ks_device_status.restype = C.c_int
+    lib.ks_last_error.argtypes = []
+    lib.ks_last_error.restype = C.c_char_p
+    lib.ks_version.argtypes = []
+    lib.ks_version.restype = C.c_char_p
+    _lib = lib
+    return lib
+
+
+def _check(st: int) -> int:
+    if st != KS_OK:
+        raise KsError(st, load().ks_last_error().decode())
+    return st
+
+
+# --------------------------------------------------------------------------
+# the entry points, same names as the C ABI; arguments are ctypes structs
+# and raw device addresses
+# --------------------------------------------------------------------------
+def ks_workspace_bytes(desc: ks_desc, n_specs: int) -> int:
+    return load().ks_workspace_bytes(C.byref(desc), n_specs)
+
+
+def ks_eval_kernels(desc, specs_ptr, n_specs, heads, out, ws_ptr, ws_bytes, stream, check=True):
+    st = load().ks_eval_kernels(C.byref(desc), specs_ptr, n_specs, C.byref(heads), C.byref(out),
+                                ws_ptr, ws_bytes, stream)
+    return _check(st) if check else st
+
+
+def ks_eval_steps(desc, steps, specs_ptr, n_specs, heads, host, out, kout, ws_ptr, ws_bytes,
+                  stream, check=True):
+    st = load().ks_eval_steps(C.byref(desc), C.byref(steps), specs_ptr, n_specs, C.byref(heads),
+                              C.byref(host), C.byref(out),
+                              C.byref(kout) if kout is not None else None,
+                              ws_ptr, ws_bytes, stream)
+    return _check(st) if check else st
+
+
+def ks_validate(desc, steps, specs_ptr, n_specs, ws_ptr, ws_bytes, stream, check=True):
+    st = load().ks_validate(C.byref(desc), C.byref(steps) if steps is not None else None,
+                            specs_ptr, n_specs, ws_ptr, ws_bytes, stream)
+    return _check(st) if check else st
+
+
+def ks_device_status(ws_ptr, ws_bytes, stream, check=True):
+    st = load().ks_device_status(ws_ptr, ws_bytes, stream)
+    return _check(st) if check else st
+
+
+def ks_last_error() -> str:
+    return load().ks_last_error().decode()
+
+
+def ks_version() -> str:
+    return load().ks_version().decode()
+
+
+# --------------------------------------------------------------------------
+# marshalling helpers: host arrays -> torch device tensors -> ctypes structs
+# --------------------------------------------------------------------------
+SPEC_DTYPE = np.dtype([("peak_flops", "<f8"), ("hbm_bw", "<f8"), ("t0", "<f8"),
+                       ("l2_bytes", "<f8"), ("ar_alpha0", "<f8"), ("ar_alpha_log2p", "<f8"),
+                       ("ar_beta", "<f8"), ("n_cu", "<u4"), ("reserved", "<u4")])
+assert SPEC_DTYPE.itemsize == 64
+
+
+def pack_specs(specs: dict) -> np.ndarray:
+    """Spec vectors (dict of equal-length arrays) -> ks_spec records."""
+    n = len(specs["peak_flops"])
+    rec = np.zeros(n, SPEC_DTYPE)
+    for name in SPEC_DTYPE.names:
+        if name != "reserved":
+            rec[name] = specs[name]
+    return rec
+
+
+def _ptr(t) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+class DeviceInputs:
+    """The inputs of one evaluation, resident in device memory (torch
+    tensors), and the ctypes structs that point at them."""
+
+    def __init__(self, wl, device="cuda", n_specs: int | None = None):
+        import torch
+        dev = torch.device(device)
+
+        def u32(x):
+            return torch.from_numpy(np.ascontiguousarray(x, np.uint32).view(np.int32)).to(dev)
+
+        d = wl.desc
+        self.t = {name: u32(getattr(d, name)) for name in
+                  ("step", "m", "n", "k", "a", "b", "req_off", "req_q", "req_h", "expert_rows")}
+        sr = wl.steps
+        for name in ("layers", "hidden", "tp", "n_launch"):
+            self.t["s_" + name] = u32(getattr(sr, name))
+        rec = pack_specs(wl.specs)
+        if n_specs is not None:
+            rec = rec[:n_specs]
+        self.n_specs = len(rec)
+        self.t["specs"] = torch.from_numpy(rec.view(np.uint8).copy()).to(dev)
+        h = wl.heads
+        self.heads_t = {}
+        for name in ("w1", "w2", "b2", "w3", "b3"):
+            arr = np.ascontiguousarray(h.storage[name])
+            if arr.dtype == np.uint16:
+                arr = arr.view(np.int16)
+            self.heads_t[name] = torch.from_numpy(arr.reshape(-1).copy()).to(dev)
+
+        self.desc = ks_desc()
+        self.desc.n_rows = d.n_rows
+        for f in range(NFAM + 1):
+            self.desc.fam_off[f] = int(d.fam_off[f])
+        for name in ("step", "m", "n", "k", "a", "b", "req_off", "req_q", "req_h"):
+            setattr(self.desc, name, _ptr(self.t[name]) if self.t[name].numel() else None)
+        self.desc.n_steps = d.n_steps
+        self.desc.n_req = len(d.req_q)
+        self.desc.expert_rows = _ptr(self.t["expert_rows"]) if len(d.expert_rows) else None
+        self.desc.n_expert_rows = len(d.expert_rows)
+        self.desc.elem_bytes = d.elem_bytes
+
+        self.steps = ks_steps()
+        self.steps.n_steps = d.n_steps
+        for name in ("layers", "hidden", "tp", "n_launch"):
+            t = self.t["s_" + name]
+            setattr(self.steps, name, _ptr(t) if t.numel() else None)
+
+        self.heads = self.make_heads(h.precision, h.in_dim, h.hidden, KS_ETA_MLP)
+        hc = wl.host
+        self.host = ks_host(hc.c_disp, hc.ell, hc.c_ovl, hc.c_tail, hc.body_scale)
+        self.ws_bytes = ks_workspace_bytes(self.desc, self.n_specs)
+        if self.ws_bytes == 0:
+            raise KsError(KS_EINVAL, ks_last_error() or "bad descriptor")
+        self.ws = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=dev)
+        off = (-self.ws.data_ptr()) % 256
+        self.ws_ptr = self.ws.data_ptr() + off
+
+    def make_heads(self, precision, in_dim, hidden, mode) -> ks_heads:
+        hd = ks_heads()
+        hd.in_dim, hd.hidden = in_dim, hidden
+        hd.precision = KS_BF16 if precision == "bf16" else KS_F32
+        hd.mode = mode
+        for name in ("w1", "w2", "b2", "w3", "b3"):
+            setattr(hd, name, _ptr(self.heads_t[name]))
+        return hd
+
+    @property
+    def specs_ptr(self) -> int:
+        return self.t["specs"].data_ptr()
+
+
+def kernel_outputs(n_rows: int, n_specs: int, device="cuda", counts=True, t_roof=True,
+                   eta=True, t_kernel=True):
+    """Allocate per-record / per-pair output tensors and the struct."""
+    import torch
+    dev = torch.device(device)
+    o = {}
+    if counts:
+        for name in ("flops", "bytes", "blocks"):
+            o[name] = torch.empty(n_rows, dtype=torch.int64, device=dev)
+    for name, want in (("t_roof", t_roof), ("eta", eta), ("t_kernel", t_kernel)):
+        if want:
+            o[name] = torch.empty((n_specs, n_rows), dtype=torch.float32, device=dev)
+    s = ks_kernel_out()
+    for name in ("flops", "bytes", "blocks", "t_roof", "eta", "t_kernel"):
+        setattr(s, name, _ptr(o.get(name)) if name in o and o[name].numel() else None)
+    return o, s
+
+
+def step_outputs(n_steps: int, n_specs: int, device="cuda"):
+    import torch
+    dev = torch.device(device)
+    o = {name: torch.empty((n_specs, n_steps), dtype=torch.float64, device=dev)
+         for name in ("t_body", "t_gpu", "t_step")}
+    s = ks_step_out(*(_ptr(o[n]) for n in ("t_body", "t_gpu", "t_step")))
+    return o, s
+
+
+def current_stream() -> int:
+    import torch
+    return torch.cuda.current_stream().cuda_stream

@@ -1,0 +1,348 @@
+// Host side of the C ABI declared in include/ks.h: argument checks, the
+// workspace layout, the launch sequence and error reporting.
+#include <hip/hip_runtime_api.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "ks.h"
+#include "ks_internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+ks_status fail(ks_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+ks_status hip_fail(hipError_t e, const char *what) {
+  return fail(KS_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Workspace layout (every region 256-byte aligned):
+//   header  : 256 B (uint32 flag word at offset 0)
+//   agg     : 4 * n_steps uint64           per-step attention work
+//   range   : KS_NFAM * n_steps * 2 uint32 per (family, step) record range
+//   partial : n_specs * KS_NFAM * n_steps double
+//   carry   : n_specs * n_tiles double
+struct Layout {
+  size_t agg, range, partial, carry, total;
+};
+
+struct Tiles {
+  int32_t tile_off[KS_NFAM + 1];
+  int32_t wgt_off[KS_NFAM + 1];
+};
+
+Tiles tiles_of(const ks_desc *d) {
+  Tiles t;
+  t.tile_off[0] = t.wgt_off[0] = 0;
+  for (int f = 0; f < KS_NFAM; ++f) {
+    const int64_t rows = d->fam_off[f + 1] - d->fam_off[f];
+    const int64_t nt = (rows + ks::kTileRows - 1) / ks::kTileRows;
+    t.tile_off[f + 1] = t.tile_off[f] + (int32_t)nt;
+    t.wgt_off[f + 1] = t.wgt_off[f] + (int32_t)((nt + ks::kWgWaves - 1) / ks::kWgWaves);
+  }
+  return t;
+}
+
+Layout layout_of(const ks_desc *d, int32_t n_specs) {
+  const Tiles t = tiles_of(d);
+  const size_t S = (size_t)d->n_steps;
+  Layout L;
+  size_t off = 256;
+  L.agg = off;
+  off += align256(4 * S * sizeof(uint64_t));
+  L.range = off;
+  off += align256((size_t)KS_NFAM * S * 2 * sizeof(uint32_t));
+  L.partial = off;
+  off += align256((size_t)n_specs * KS_NFAM * S * sizeof(double));
+  L.carry = off;
+  off += align256((size_t)n_specs * (size_t)t.tile_off[KS_NFAM] * sizeof(double));
+  L.total = off;
+  return L;
+}
+
+ks_status check_desc(const ks_desc *d) {
+  if (!d) return fail(KS_EINVAL, "desc is NULL");
+  if (d->n_rows < 0 || d->n_rows >= (int64_t(1) << 32) - 1)
+    return fail(KS_ERANGE, "n_rows %lld outside [0, 2^32-1)", (long long)d->n_rows);
+  if (d->n_steps < 0 || d->n_steps >= (int64_t(1) << 32) - 1)
+    return fail(KS_ERANGE, "n_steps %lld outside [0, 2^32-1)", (long long)d->n_steps);
+  if (d->n_req < 0 || d->n_req >= (int64_t(1) << 32))
+    return fail(KS_ERANGE, "n_req %lld outside [0, 2^32)", (long long)d->n_req);
+  if (d->n_expert_rows < 0 || d->n_expert_rows >= (int64_t(1) << 32))
+    return fail(KS_ERANGE, "n_expert_rows %lld outside [0, 2^32)", (long long)d->n_expert_rows);
+  if (d->fam_off[0] != 0) return fail(KS_EINVAL, "fam_off[0] must be 0");
+  for (int f = 0; f < KS_NFAM; ++f)
+    if (d->fam_off[f + 1] < d->fam_off[f])
+      return fail(KS_EINVAL, "fam_off decreases at family %d", f);
+  if (d->fam_off[KS_NFAM] != d->n_rows)
+    return fail(KS_EINVAL, "fam_off[KS_NFAM] = %lld != n_rows = %lld", (long long)d->fam_off[KS_NFAM],
+                (long long)d->n_rows);
+  if (d->n_rows > 0 && (!d->step || !d->m || !d->n || !d->k || !d->a || !d->b))
+    return fail(KS_EINVAL, "a record array is NULL");
+  if (d->n_rows > 0 && d->n_steps == 0) return fail(KS_EINVAL, "records present but n_steps = 0");
+  if (!d->req_off) return fail(KS_EINVAL, "req_off is NULL");
+  if (d->n_req > 0 && (!d->req_q || !d->req_h)) return fail(KS_EINVAL, "req_q / req_h is NULL");
+  if (d->fam_off[KS_GROUPED_GEMM + 1] > d->fam_off[KS_GROUPED_GEMM] && !d->expert_rows && d->n_expert_rows > 0)
+    return fail(KS_EINVAL, "expert_rows is NULL");
+  if (d->elem_bytes < 1 || d->elem_bytes > 8) return fail(KS_ERANGE, "elem_bytes %u outside 1..8", d->elem_bytes);
+  return KS_OK;
+}
+
+ks_status head_kind(const ks_heads *h, int *kind) {
+  if (!h) return fail(KS_EINVAL, "heads is NULL");
+  if (h->mode == KS_ETA_ONE) {
+    *kind = ks::kEtaOne;
+    return KS_OK;
+  }
+  if (h->mode != KS_ETA_MLP) return fail(KS_EINVAL, "heads.mode %d unknown", h->mode);
+  if (!h->w1 || !h->w2 || !h->b2 || !h->w3 || !h->b3) return fail(KS_EINVAL, "a head parameter pointer is NULL");
+  const int in = h->in_dim, hid = h->hidden;
+  if (in != 16 && in != 32) return fail(KS_EINVAL, "heads.in_dim %d not 16 or 32", in);
+  if (h->precision == KS_F32) {
+    if (hid == 64) *kind = in == 16 ? ks::kF32_16_64 : ks::kF32_32_64;
+    else if (hid == 128) *kind = in == 16 ? ks::kF32_16_128 : ks::kF32_32_128;
+    else return fail(KS_EINVAL, "fp32 heads.hidden %d not 64 or 128", hid);
+  } else if (h->precision == KS_BF16) {
+    if (hid == 64) *kind = in == 16 ? ks::kBF16_16_64 : ks::kBF16_32_64;
+    else if (hid == 128) *kind = in == 16 ? ks::kBF16_16_128 : ks::kBF16_32_128;
+    else if (hid == 256) *kind = in == 16 ? ks::kBF16_16_256 : ks::kBF16_32_256;
+    else return fail(KS_EINVAL, "bf16 heads.hidden %d not 64, 128 or 256", hid);
+  } else {
+    return fail(KS_EINVAL, "heads.precision %d unknown", h->precision);
+  }
+  return KS_OK;
+}
+
+ks_status check_common(const ks_desc *d, const ks_spec *specs, int32_t n_specs, void *ws, size_t ws_bytes,
+                       Layout *L) {
+  ks_status st = check_desc(d);
+  if (st != KS_OK) return st;
+  if (n_specs < 1 || n_specs > (1 << 20)) return fail(KS_EINVAL, "n_specs %d outside 1..2^20", n_specs);
+  if (!specs) return fail(KS_EINVAL, "specs is NULL");
+  *L = layout_of(d, n_specs);
+  if (!ws) return fail(KS_EWORKSPACE, "workspace is NULL");
+  if (ws_bytes < L->total)
+    return fail(KS_EWORKSPACE, "workspace %zu bytes < %zu required", ws_bytes, L->total);
+  if (reinterpret_cast<uintptr_t>(ws) % 256)
+    return fail(KS_EWORKSPACE, "workspace not 256-byte aligned");
+  return KS_OK;
+}
+
+void fill_eval(ks::EvalParams &p, const ks_desc *d, const ks_spec *specs, int32_t n_specs, const ks_heads *h,
+               const ks_kernel_out *out, char *ws, const Layout &L) {
+  std::memset(&p, 0, sizeof p);
+  p.step = d->step;
+  p.m = d->m;
+  p.n = d->n;
+  p.k = d->k;
+  p.a = d->a;
+  p.b = d->b;
+  p.expert_rows = d->expert_rows;
+  p.n_expert_rows = d->expert_rows ? d->n_expert_rows : 0;
+  p.agg = reinterpret_cast<const uint64_t *>(ws + L.agg);
+  p.n_steps = d->n_steps;
+  p.elem_bytes = d->elem_bytes;
+  p.n_specs = n_specs;
+  p.specs = specs;
+  const Tiles t = tiles_of(d);
+  for (int f = 0; f <= KS_NFAM; ++f) {
+    p.fam_off[f] = d->fam_off[f];
+    p.tile_off[f] = t.tile_off[f];
+    p.wgt_off[f] = t.wgt_off[f];
+  }
+  p.n_tiles = t.tile_off[KS_NFAM];
+  if (h->mode == KS_ETA_MLP) {
+    p.w1 = h->w1;
+    p.w2 = h->w2;
+    p.b2 = h->b2;
+    p.w3 = h->w3;
+    p.b3 = h->b3;
+  }
+  if (out) {
+    p.o_flops = out->flops;
+    p.o_bytes = out->bytes;
+    p.o_blocks = out->blocks;
+    p.o_troof = out->t_roof;
+    p.o_eta = out->eta;
+    p.o_t = out->t_kernel;
+  }
+  p.err = reinterpret_cast<uint32_t *>(ws);
+}
+
+ks_status prologue(const ks_desc *d, char *ws, const Layout &L, hipStream_t s) {
+  hipError_t e = ks::launch_clear(reinterpret_cast<uint32_t *>(ws), s);
+  if (e != hipSuccess) return hip_fail(e, "clear launch");
+  e = ks::launch_attn_agg(d->req_off, d->req_q, d->req_h, d->n_steps, d->n_req,
+                          reinterpret_cast<uint64_t *>(ws + L.agg), reinterpret_cast<uint32_t *>(ws), s);
+  if (e != hipSuccess) return hip_fail(e, "attention aggregate launch");
+  return KS_OK;
+}
+
+const char *flag_text(uint32_t f) {
+  if (f & ks::kErrStep) return "a record's step index is >= n_steps";
+  if (f & ks::kErrOrder) return "record steps decrease within a family";
+  if (f & ks::kErrReq) return "request offsets out of order or beyond n_req";
+  if (f & ks::kErrExpert) return "grouped-GEMM expert offsets beyond n_expert_rows (or E > 1024)";
+  if (f & ks::kErrRange) return "a shape or count outside the documented limits";
+  if (f & ks::kErrSpec) return "a spec vector is not usable (non-positive peak, bandwidth or n_cu)";
+  return "unknown";
+}
+
+ks_status flag_status(uint32_t f) {
+  if (!f) return KS_OK;
+  const bool range = (f & (ks::kErrRange | ks::kErrSpec)) && !(f & (ks::kErrStep | ks::kErrOrder | ks::kErrReq | ks::kErrExpert));
+  return fail(range ? KS_ERANGE : KS_EINVAL, "device check: %s (flags 0x%x)", flag_text(f), f);
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t ks_workspace_bytes(const ks_desc *desc, int32_t n_specs) {
+  if (check_desc(desc) != KS_OK || n_specs < 1 || n_specs > (1 << 20)) return 0;
+  return layout_of(desc, n_specs).total;
+}
+
+ks_status ks_eval_kernels(const ks_desc *desc, const ks_spec *specs, int32_t n_specs, const ks_heads *heads,
+                          const ks_kernel_out *out, void *ws, size_t ws_bytes, hipStream_t stream) {
+  Layout L;
+  ks_status st = check_common(desc, specs, n_specs, ws, ws_bytes, &L);
+  if (st != KS_OK) return st;
+  int kind;
+  st = head_kind(heads, &kind);
+  if (st != KS_OK) return st;
+  if (!out) return fail(KS_EINVAL, "out is NULL");
+  char *w = static_cast<char *>(ws);
+  st = prologue(desc, w, L, stream);
+  if (st != KS_OK) return st;
+  ks::EvalParams p;
+  fill_eval(p, desc, specs, n_specs, heads, out, w, L);
+  hipError_t e = ks::launch_eval(kind, p, stream);
+  if (e != hipSuccess) return hip_fail(e, "evaluation launch");
+  return KS_OK;
+}
+
+ks_status ks_eval_steps(const ks_desc *desc, const ks_steps *steps, const ks_spec *specs, int32_t n_specs,
+                        const ks_heads *heads, const ks_host *host, const ks_step_out *out,
+                        const ks_kernel_out *kout, void *ws, size_t ws_bytes, hipStream_t stream) {
+  Layout L;
+  ks_status st = check_common(desc, specs, n_specs, ws, ws_bytes, &L);
+  if (st != KS_OK) return st;
+  int kind;
+  st = head_kind(heads, &kind);
+  if (st != KS_OK) return st;
+  if (!steps) return fail(KS_EINVAL, "steps is NULL");
+  if (steps->n_steps != desc->n_steps)
+    return fail(KS_EINVAL, "steps.n_steps %lld != desc.n_steps %lld", (long long)steps->n_steps,
+                (long long)desc->n_steps);
+  if (desc->n_steps > 0 && (!steps->layers || !steps->hidden || !steps->tp || !steps->n_launch))
+    return fail(KS_EINVAL, "a step array is NULL");
+  if (!host) return fail(KS_EINVAL, "host is NULL");
+  if (!out || (desc->n_steps > 0 && (!out->t_body || !out->t_gpu || !out->t_step)))
+    return fail(KS_EINVAL, "a step output is NULL");
+  char *w = static_cast<char *>(ws);
+  st = prologue(desc, w, L, stream);
+  if (st != KS_OK) return st;
+  ks::EvalParams p;
+  fill_eval(p, desc, specs, n_specs, heads, kout, w, L);
+  p.partial = reinterpret_cast<double *>(w + L.partial);
+  p.carry = reinterpret_cast<double *>(w + L.carry);
+  hipError_t e = ks::launch_eval(kind, p, stream);
+  if (e != hipSuccess) return hip_fail(e, "evaluation launch");
+
+  ks::FinishParams f;
+  std::memset(&f, 0, sizeof f);
+  f.agg = p.agg;
+  f.layers = steps->layers;
+  f.hidden = steps->hidden;
+  f.tp = steps->tp;
+  f.n_launch = steps->n_launch;
+  f.n_steps = desc->n_steps;
+  f.n_specs = n_specs;
+  f.elem_bytes = desc->elem_bytes;
+  f.specs = specs;
+  for (int i = 0; i <= KS_NFAM; ++i) {
+    f.fam_off[i] = p.fam_off[i];
+    f.tile_off[i] = p.tile_off[i];
+  }
+  f.step = desc->step;
+  f.partial = p.partial;
+  f.carry = p.carry;
+  f.n_tiles = p.n_tiles;
+  f.range = reinterpret_cast<uint32_t *>(w + L.range);
+  f.host = *host;
+  f.t_body = out->t_body;
+  f.t_gpu = out->t_gpu;
+  f.t_step = out->t_step;
+  e = ks::launch_finish(f, stream);
+  if (e != hipSuccess) return hip_fail(e, "step finish launch");
+  return KS_OK;
+}
+
+ks_status ks_validate(const ks_desc *desc, const ks_steps *steps, const ks_spec *specs, int32_t n_specs, void *ws,
+                      size_t ws_bytes, hipStream_t stream) {
+  Layout L;
+  ks_status st = check_common(desc, specs, n_specs, ws, ws_bytes, &L);
+  if (st != KS_OK) return st;
+  if (steps && steps->n_steps != desc->n_steps)
+    return fail(KS_EINVAL, "steps.n_steps %lld != desc.n_steps %lld", (long long)steps->n_steps,
+                (long long)desc->n_steps);
+  char *w = static_cast<char *>(ws);
+  st = prologue(desc, w, L, stream);
+  if (st != KS_OK) return st;
+  ks::ValidateParams v;
+  std::memset(&v, 0, sizeof v);
+  v.step = desc->step;
+  v.m = desc->m;
+  v.n = desc->n;
+  v.k = desc->k;
+  v.a = desc->a;
+  v.b = desc->b;
+  v.expert_rows = desc->expert_rows;
+  v.n_expert_rows = desc->expert_rows ? desc->n_expert_rows : 0;
+  v.n_rows = desc->n_rows;
+  for (int f = 0; f <= KS_NFAM; ++f) v.fam_off[f] = desc->fam_off[f];
+  v.n_steps = desc->n_steps;
+  v.req_off = desc->req_off;
+  v.req_q = desc->req_q;
+  v.req_h = desc->req_h;
+  v.n_req = desc->n_req;
+  v.agg = reinterpret_cast<const uint64_t *>(w + L.agg);
+  v.tp = steps ? steps->tp : nullptr;
+  v.specs = specs;
+  v.n_specs = n_specs;
+  v.err = reinterpret_cast<uint32_t *>(w);
+  hipError_t e = ks::launch_validate(v, stream);
+  if (e != hipSuccess) return hip_fail(e, "validate launch");
+  return ks_device_status(ws, ws_bytes, stream);
+}
+
+ks_status ks_device_status(const void *ws, size_t ws_bytes, hipStream_t stream) {
+  if (!ws || ws_bytes < 256) return fail(KS_EWORKSPACE, "workspace missing or too small");
+  uint32_t flag = 0;
+  hipError_t e = hipMemcpyAsync(&flag, ws, sizeof flag, hipMemcpyDeviceToHost, stream);
+  if (e != hipSuccess) return hip_fail(e, "flag copy");
+  e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) return hip_fail(e, "stream synchronize");
+  return flag_status(flag);
+}
+
+const char *ks_last_error(void) { return g_err.c_str(); }
+
+const char *ks_version(void) { return "ks 0.1.0 (gfx950)"; }
+
+}  // extern "C"

@@ -1,0 +1,102 @@
+// Internal interface between the C-ABI host code (ks_api.cpp) and the HIP
+// kernels (ks_kernels.hip).  Not installed; not part of the ABI.
+#pragma once
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+#include "ks.h"
+
+namespace ks {
+
+constexpr int kWave = 64;
+constexpr int kWgWaves = 4;
+constexpr int kWgThreads = kWave * kWgWaves;
+constexpr int kTileRows = 64;                 // records per wave tile
+constexpr int kWgRows = kTileRows * kWgWaves; // records per workgroup tile
+
+// flags raised by the kernels on bad device data (never faults)
+enum : uint32_t {
+  kErrStep = 1u,      // record step >= n_steps
+  kErrReq = 2u,       // request offsets out of order or out of bounds
+  kErrExpert = 4u,    // grouped-GEMM expert offsets out of bounds
+  kErrRange = 8u,     // a shape or count outside the documented limits
+  kErrOrder = 16u,    // steps decrease within a family
+  kErrSpec = 32u,     // spec vector not usable
+};
+
+// head kinds compiled into the evaluation kernel
+enum HeadKind : int {
+  kEtaOne = 0,
+  kF32_16_64, kF32_16_128, kF32_32_64, kF32_32_128,
+  kBF16_16_64, kBF16_16_128, kBF16_16_256, kBF16_32_64, kBF16_32_128, kBF16_32_256,
+  kNumKinds
+};
+
+struct EvalParams {
+  // records
+  const uint32_t *step, *m, *n, *k, *a, *b;
+  const uint32_t *expert_rows;
+  int64_t n_expert_rows;
+  const uint64_t *agg;         // [4][n_steps]: Q, KV, PAIRS, TILES
+  int64_t n_steps;
+  uint32_t elem_bytes;
+  int32_t n_specs;
+  const ks_spec *specs;
+  int64_t fam_off[KS_NFAM + 1];
+  int32_t tile_off[KS_NFAM + 1];   // wave-tile offsets per family
+  int32_t wgt_off[KS_NFAM + 1];    // workgroup-tile offsets per family
+  int32_t n_tiles;
+  // heads
+  const void *w1, *w2, *b2, *w3, *b3;
+  // per-record / per-pair outputs (nullable)
+  uint64_t *o_flops, *o_bytes, *o_blocks;
+  float *o_troof, *o_eta, *o_t;
+  // per-step partial sums (nullable: no step sums)
+  double *partial;   // [n_specs][KS_NFAM][n_steps]
+  double *carry;     // [n_specs][n_tiles]
+  uint32_t *err;
+};
+
+struct FinishParams {
+  const uint64_t *agg;                 // [4][n_steps]
+  const uint32_t *layers, *hidden, *tp, *n_launch;
+  int64_t n_steps;
+  int32_t n_specs;
+  uint32_t elem_bytes;
+  const ks_spec *specs;
+  int64_t fam_off[KS_NFAM + 1];
+  int32_t tile_off[KS_NFAM + 1];
+  const uint32_t *step;
+  const double *partial, *carry;
+  int32_t n_tiles;
+  uint32_t *range;                     // [KS_NFAM][n_steps][2]
+  ks_host host;
+  double *t_body, *t_gpu, *t_step;
+};
+
+struct ValidateParams {
+  const uint32_t *step, *m, *n, *k, *a, *b;
+  const uint32_t *expert_rows;
+  int64_t n_expert_rows;
+  int64_t n_rows;
+  int64_t fam_off[KS_NFAM + 1];
+  int64_t n_steps;
+  const uint32_t *req_off, *req_q, *req_h;
+  int64_t n_req;
+  const uint64_t *agg;
+  const uint32_t *tp;                  // nullable
+  const ks_spec *specs;
+  int32_t n_specs;
+  uint32_t *err;
+};
+
+hipError_t launch_clear(uint32_t *err, hipStream_t s);
+hipError_t launch_attn_agg(const uint32_t *req_off, const uint32_t *q, const uint32_t *h,
+                           int64_t n_steps, int64_t n_req, uint64_t *agg, uint32_t *err,
+                           hipStream_t s);
+hipError_t launch_eval(int kind, const EvalParams &p, hipStream_t s);
+hipError_t launch_finish(const FinishParams &p, hipStream_t s);
+hipError_t launch_validate(const ValidateParams &p, hipStream_t s);
+int eval_grid(int kind, int n_wgt);
+
+}  // namespace ks

@@ -1,0 +1,825 @@
+// HIP kernels of the batched kernel-latency evaluator, written for gfx950
+// (CDNA4: wave64, MFMA, 160 KB LDS per CU).
+//
+// Data flow of one evaluation (all on the caller's stream):
+//   k_clear      reset the workspace's bad-data flag
+//   k_attn_agg   per step: Q, KV, PAIRS, TILES of its request list (Sec. 5.8)
+//   k_eval<K>    per wave: 64 records of one family x every spec vector:
+//                exact counts (Eq. 1-2 operands), waves and u (Sec. 2.2),
+//                t_roof (Eq. 2), features and the family's efficiency head
+//                on MFMA (Sec. 5.3), t = max(t_roof eta, t0) (Eq. 2), and a
+//                wavefront segmented sum of t by step
+//   k_seg_range  per (family, step): the record range of that step
+//   k_finish     per (spec, step): body sum, all-reduce (Eq. 3), assembly (Eq. 4)
+#include <hip/hip_runtime.h>
+
+#include "ks_internal.h"
+
+namespace ks {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef short s16x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr uint32_t kNoKey = 0xFFFFFFFFu;
+
+// ------------------------------------------------------------------ helpers
+__device__ __forceinline__ float rcpf(float x) { return __builtin_amdgcn_rcpf(x); }
+__device__ __forceinline__ float log2f_fast(float x) { return __builtin_amdgcn_logf(x); }
+
+// ceil(x / d) for x + d < 2^52, through a float64 reciprocal and one
+// correction step each way (the product's error is below one unit there).
+__device__ __forceinline__ uint64_t ceil_div(uint64_t x, uint32_t d, double rcp_d) {
+  const uint64_t y = x + d - 1;
+  uint64_t q = (uint64_t)((double)y * rcp_d);
+  if (q * d > y) q -= 1;
+  else if ((q + 1) * d <= y) q += 1;
+  return q;
+}
+
+// two floats -> packed bfloat16 pair, round to nearest even
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  f32x2 v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
+// relu on a packed bfloat16 pair: a negative bf16 is a negative int16
+__device__ __forceinline__ uint32_t relu_bf16x2(uint32_t v) {
+  s16x2 s = __builtin_bit_cast(s16x2, v);
+  s16x2 z = {0, 0};
+  return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(s, z));
+}
+
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a),
+                                         __builtin_bit_cast(bf16x2, b), c, false);
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
+  return __builtin_bit_cast(float, bits16 << 16);
+}
+
+// Exchange lanes 32..63 of `lo` with lanes 0..31 of `hi`.
+__device__ __forceinline__ void swap32(uint32_t &lo, uint32_t &hi) {
+  auto r = __builtin_amdgcn_permlane32_swap(lo, hi, false, false);
+  lo = r[0];
+  hi = r[1];
+}
+
+// ------------------------------------------------------------ clear / agg
+__global__ void k_clear(uint32_t *err) {
+  if (threadIdx.x == 0) err[0] = 0;
+}
+
+// Per step j: over its requests r, Q = sum q, KV = sum (h + q),
+// PAIRS = sum (q h + q (q + 1) / 2), TILES = sum ceil(q / 128).
+__global__ void k_attn_agg(const uint32_t *__restrict__ req_off, const uint32_t *__restrict__ rq,
+                           const uint32_t *__restrict__ rh, int64_t n_steps, int64_t n_req,
+                           uint64_t *__restrict__ agg, uint32_t *err) {
+  for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n_steps;
+       j += (int64_t)gridDim.x * blockDim.x) {
+    uint32_t r0 = req_off[j], r1 = req_off[j + 1];
+    if (r0 > r1 || (int64_t)r1 > n_req) {
+      atomicOr(err, kErrReq);
+      r0 = r1 = 0;
+    }
+    uint64_t Q = 0, KV = 0, P = 0, T = 0;
+    for (uint32_t r = r0; r < r1; ++r) {
+      const uint64_t q = rq[r], h = rh[r];
+      Q += q;
+      KV += h + q;
+      P += q * h + ((q * (q + 1)) >> 1);
+      T += (q + 127) >> 7;
+    }
+    agg[j] = Q;
+    agg[n_steps + j] = KV;
+    agg[2 * n_steps + j] = P;
+    agg[3 * n_steps + j] = T;
+  }
+}
+
+// ------------------------------------------------------------ record counts
+struct Cnt {
+  uint64_t F, Bt, B, M;
+};
+
+// FLOPs F, bytes Bt, thread blocks B and feature row count M of one record.
+__device__ __forceinline__ Cnt record_counts(int fam, uint32_t m32, uint32_t n32, uint32_t k32,
+                                             uint32_t a32, uint32_t b32, uint32_t step,
+                                             const EvalParams &p, uint32_t &bad) {
+  const uint64_t dt = p.elem_bytes, M = m32, N = n32, K = k32, A = a32;
+  Cnt c{0, 0, 0, M};
+  switch (fam) {
+    case KS_GEMM:
+    case KS_LM_HEAD:
+      c.F = 2 * M * N * K;
+      c.Bt = dt * (M * K + K * N + M * N);
+      c.B = ((M + 127) >> 7) * ((N + 127) >> 7);
+      break;
+    case KS_GROUPED_GEMM: {
+      uint64_t ms = 0, act = 0, tiles = 0;
+      if ((uint64_t)b32 + A <= (uint64_t)p.n_expert_rows && A <= 1024) {
+        for (uint32_t e = 0; e < a32; ++e) {
+          const uint64_t me = p.expert_rows[b32 + e];
+          ms += me;
+          act += me > 0;
+          tiles += (me + 127) >> 7;
+        }
+      } else {
+        bad |= kErrExpert;
+      }
+      c.F = 2 * ms * N * K;
+      c.Bt = dt * (ms * K + act * K * N + ms * N);
+      c.B = tiles * ((N + 127) >> 7);
+      c.M = ms;
+      break;
+    }
+    case KS_ATTN_PREFILL:
+    case KS_ATTN_DECODE: {
+      uint64_t Q = 0, KV = 0, P = 0, T = 0;
+      if ((int64_t)step < p.n_steps) {
+        Q = p.agg[step];
+        KV = p.agg[p.n_steps + step];
+        P = p.agg[2 * p.n_steps + step];
+        T = p.agg[3 * p.n_steps + step];
+      }
+      c.F = 4 * N * K * P;
+      c.Bt = dt * (2 * N * K * Q + 2 * A * K * KV);
+      c.B = N * T;
+      c.M = Q;
+      break;
+    }
+    case KS_RMSNORM:
+      c.F = 4 * M * N;
+      c.Bt = dt * (2 * M * N + N);
+      c.B = M;
+      break;
+    case KS_ROPE:
+      c.F = 3 * M * N * K;
+      c.Bt = dt * (2 * M * N * K + M * K);
+      c.B = M;
+      break;
+    case KS_SILU_MUL:
+      c.F = 5 * M * N;
+      c.Bt = 3 * dt * M * N;
+      c.B = (M * N + 1023) >> 10;
+      break;
+    case KS_KV_WRITE:
+      c.F = 0;
+      c.Bt = 4 * dt * M * N * K;
+      c.B = M;
+      break;
+    default:  // KS_EMBED
+      c.F = 0;
+      c.Bt = 2 * dt * M * N + 4 * M;
+      c.B = M;
+      break;
+  }
+  return c;
+}
+
+// ------------------------------------------------------------ spec constants
+struct SpecC {
+  float rcp_p, rcp_bw, bw_over_p, l2, t0, rcp_t0, n_f, rcp_n;
+  double rcp_nd;
+  uint32_t n;
+};
+
+__device__ __forceinline__ SpecC load_spec(const ks_spec *__restrict__ sp) {
+  SpecC c;
+  const double P = sp->peak_flops, BW = sp->hbm_bw;
+  uint32_t n = sp->n_cu;
+  n = n < 1 ? 1 : n;
+  c.n = n;
+  c.rcp_p = (float)(1.0 / P);
+  c.rcp_bw = (float)(1.0 / BW);
+  c.bw_over_p = (float)(BW / P);
+  c.l2 = (float)sp->l2_bytes;
+  c.t0 = (float)sp->t0;
+  c.rcp_t0 = (float)(1.0 / fmax(sp->t0, 1e-9));
+  c.n_f = (float)n;
+  c.rcp_n = 1.0f / (float)n;
+  c.rcp_nd = 1.0 / (double)n;
+  return c;
+}
+
+// spec-independent per-record quantities
+struct RowC {
+  uint64_t B;
+  float Ff, Btf, Bf, rcp_bt1, ai, x0, xs[7];  // xs = x8 .. x14
+};
+
+__device__ __forceinline__ RowC row_consts(const Cnt &c, uint32_t n, uint32_t k) {
+  RowC r;
+  r.B = c.B;
+  r.Ff = (float)c.F;
+  r.Btf = (float)c.Bt;
+  r.Bf = (float)c.B;
+  r.rcp_bt1 = rcpf(fmaxf(r.Btf, 1.0f));
+  r.ai = r.Ff * r.rcp_bt1;
+  const float Bm1 = fmaxf(r.Bf, 1.0f);
+  r.x0 = log2f_fast(fmaxf(r.ai, 0x1p-10f)) * (1.0f / 16);
+  r.xs[0] = log2f_fast(1.0f + r.Ff) * (1.0f / 64);
+  r.xs[1] = log2f_fast(1.0f + r.Btf) * (1.0f / 48);
+  r.xs[2] = log2f_fast(1.0f + (float)c.M) * (1.0f / 24);
+  r.xs[3] = log2f_fast(1.0f + (float)n) * (1.0f / 24);
+  r.xs[4] = log2f_fast(1.0f + (float)k) * (1.0f / 24);
+  r.xs[5] = log2f_fast(1.0f + r.Ff * rcpf(Bm1)) * (1.0f / 48);
+  r.xs[6] = log2f_fast(1.0f + r.Btf * rcpf(Bm1)) * (1.0f / 40);
+  return r;
+}
+
+struct Roof {
+  float t_comp, t_mem, t_roof, u, W;
+};
+
+// waves, u and t_roof (Sec. 2.2, Eq. 2)
+__device__ __forceinline__ Roof roofline(const RowC &r, const SpecC &s) {
+  Roof o;
+  float wn = 0.0f;
+  if (r.B > 0) {
+    const uint64_t W = ceil_div(r.B, s.n, s.rcp_nd);
+    o.W = (float)W;
+    wn = (float)(W * s.n);
+    o.u = wn * rcpf(r.Bf);
+  } else {
+    o.W = 0.0f;
+    o.u = 1.0f;
+  }
+  o.t_comp = r.Ff * o.u * s.rcp_p;
+  o.t_mem = r.Btf * s.rcp_bw;
+  o.t_roof = fmaxf(o.t_comp, o.t_mem);
+  return o;
+}
+
+// the 16 dimensionless features (x[16 + i] = x[i]^2 for 32 inputs)
+template <int IN>
+__device__ __forceinline__ void features(const RowC &r, const SpecC &s, const Roof &o, float (&x)[IN]) {
+  x[0] = r.x0;
+  x[1] = log2f_fast(fmaxf(r.ai * s.bw_over_p, 0x1p-20f)) * (1.0f / 16);
+  x[2] = log2f_fast(1.0f + r.Bf * s.rcp_n) * (1.0f / 16);
+  x[3] = r.B > 0 ? r.Bf * rcpf(o.W * s.n_f) : 1.0f;
+  x[4] = log2f_fast(1.0f + o.W) * (1.0f / 16);
+  x[5] = fminf(1.0f, s.l2 * r.rcp_bt1);
+  x[6] = log2f_fast(fmaxf(o.t_roof * s.rcp_t0, 0x1p-20f)) * (1.0f / 16);
+  const float den = o.t_comp + o.t_mem;
+  x[7] = den > 0.0f ? o.t_comp * rcpf(den) : 0.0f;
+#pragma unroll
+  for (int i = 0; i < 7; ++i) x[8 + i] = r.xs[i];
+  x[15] = 1.0f;
+  if constexpr (IN == 32) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) x[16 + i] = x[i] * x[i];
+  }
+}
+
+// ------------------------------------------------------------ bf16 MFMA head
+// Orientation: hidden units are the MFMA rows (A = weights), the 64 records
+// of a wave are the columns (B = activations, two 32-column blocks), so the
+// C tile of one layer is already the B operand of the next one once the
+// hidden units are renumbered; the renumbering is folded into the order in
+// which W2's columns are staged in LDS.
+//
+// v_mfma_f32_32x32x16_bf16 lane layout (l = lane, g = l / 32):
+//   A[i][k]: lane l holds row l % 32, k = 8 g .. 8 g + 7
+//   B[k][j]: lane l holds col l % 32, k = 8 g .. 8 g + 7
+//   C[i][j]: lane l holds col l % 32, rows 8 jj + 4 g + ii, register 4 jj + ii
+template <int IN, int HID>
+struct HeadBF16 {
+  static constexpr int MB = HID / 32;   // 32-row blocks of every layer
+  static constexpr int KC1 = IN / 16;   // K chunks of layer 1
+  static constexpr int KC2 = HID / 16;  // K chunks of layer 2
+  static constexpr int W1_DW = MB * KC1 * 64 * 4;
+  static constexpr int W2_DW = MB * KC2 * 64 * 4;
+  static constexpr int B2_DW = MB * 2 * 16;
+  static constexpr int W3_DW = MB * 2 * 8;
+  static constexpr int OFF_W2 = W1_DW;
+  static constexpr int OFF_B2 = OFF_W2 + W2_DW;
+  static constexpr int OFF_W3 = OFF_B2 + B2_DW;
+  static constexpr int OFF_B3 = OFF_W3 + W3_DW;
+  static constexpr int LDS_DW = OFF_B3 + 4;
+  static constexpr bool kMlp = true;
+
+  // layer-2 K slot s (0..15) of chunk kc -> hidden unit of layer 1's C tile
+  __device__ static __forceinline__ int hid_of(int kc, int s) {
+    const int g = s >> 3, t = s & 7;
+    return (kc >> 1) * 32 + 8 * (2 * (kc & 1) + (t >> 2)) + 4 * g + (t & 3);
+  }
+  // C-tile register r of row-block mb, lane group g -> output unit
+  __device__ static __forceinline__ int out_of(int mb, int g, int r) {
+    return mb * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
+  }
+
+  __device__ static void stage(uint32_t *lds, int fam, const EvalParams &p) {
+    const uint16_t *w1 = (const uint16_t *)p.w1 + (size_t)fam * HID * IN;
+    const uint16_t *w2 = (const uint16_t *)p.w2 + (size_t)fam * HID * HID;
+    const uint16_t *b2 = (const uint16_t *)p.b2 + (size_t)fam * HID;
+    const uint16_t *w3 = (const uint16_t *)p.w3 + (size_t)fam * HID;
+    const uint16_t *b3 = (const uint16_t *)p.b3 + fam;
+    for (int d = threadIdx.x; d < W1_DW; d += kWgThreads) {
+      const int q = d & 3, lane = (d >> 2) & 63, frag = d >> 8;
+      const int kc = frag % KC1, mb = frag / KC1;
+      const int row = mb * 32 + (lane & 31);
+      const int k0 = kc * 16 + (lane >> 5) * 8 + 2 * q;
+      lds[d] = (uint32_t)w1[row * IN + k0] | ((uint32_t)w1[row * IN + k0 + 1] << 16);
+    }
+    for (int d = threadIdx.x; d < W2_DW; d += kWgThreads) {
+      const int q = d & 3, lane = (d >> 2) & 63, frag = d >> 8;
+      const int kc = frag % KC2, mb = frag / KC2;
+      const int row = mb * 32 + (lane & 31);
+      const int s0 = (lane >> 5) * 8 + 2 * q;
+      lds[OFF_W2 + d] = (uint32_t)w2[row * HID + hid_of(kc, s0)] |
+                        ((uint32_t)w2[row * HID + hid_of(kc, s0 + 1)] << 16);
+    }
+    for (int d = threadIdx.x; d < B2_DW; d += kWgThreads) {
+      const int r = d & 15, g = (d >> 4) & 1, mb = d >> 5;
+      lds[OFF_B2 + d] = __builtin_bit_cast(uint32_t, bf16_to_f32(b2[out_of(mb, g, r)]));
+    }
+    for (int d = threadIdx.x; d < W3_DW; d += kWgThreads) {
+      const int r = (d & 7) * 2, g = (d >> 3) & 1, mb = d >> 4;
+      lds[OFF_W3 + d] = (uint32_t)w3[out_of(mb, g, r)] | ((uint32_t)w3[out_of(mb, g, r + 1)] << 16);
+    }
+    if (threadIdx.x == 0) lds[OFF_B3] = __builtin_bit_cast(uint32_t, bf16_to_f32(b3[0]));
+  }
+
+  // z of the lane's own record; x: that record's features (fp32)
+  __device__ static __forceinline__ float mlp(const float (&x)[IN], const uint32_t *lds) {
+    const int lane = threadIdx.x & 63, g = lane >> 5;
+    // features -> bf16 pairs; the swap turns "own record" into the B layout
+    // of the two 32-record column blocks
+    uint32_t P[IN / 2];
+#pragma unroll
+    for (int c = 0; c < IN / 2; ++c) P[c] = pack_bf16(x[2 * c], x[2 * c + 1]);
+    u32x4 XB[2][KC1];
+#pragma unroll
+    for (int kc = 0; kc < KC1; ++kc) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        uint32_t lo = P[8 * kc + q], hi = P[8 * kc + 4 + q];
+        swap32(lo, hi);
+        XB[0][kc][q] = lo;
+        XB[1][kc][q] = hi;
+      }
+    }
+    // layer 1: h1 = relu(W1 x), rounded to bf16
+    u32x4 H1[2][MB][2];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      f32x16 c0 = {}, c1 = {};
+#pragma unroll
+      for (int kc = 0; kc < KC1; ++kc) {
+        const u32x4 a = *(const u32x4 *)(lds + ((mb * KC1 + kc) * 64 + lane) * 4);
+        c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                      __builtin_bit_cast(bf16x8, XB[0][kc]), c0, 0, 0, 0);
+        c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                      __builtin_bit_cast(bf16x8, XB[1][kc]), c1, 0, 0, 0);
+      }
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int r = 8 * h + 2 * q;
+          H1[0][mb][h][q] = relu_bf16x2(pack_bf16(c0[r], c0[r + 1]));
+          H1[1][mb][h][q] = relu_bf16x2(pack_bf16(c1[r], c1[r + 1]));
+        }
+      }
+    }
+    // layers 2 and 3: z = w3 . bf16(relu(W2 h1 + b2)) + b3; one 32-unit
+    // block of layer 2 at a time keeps only its weight fragments live
+    float z0 = 0.0f, z1 = 0.0f;
+#pragma unroll 1
+    for (int mb = 0; mb < MB; ++mb) {
+      f32x16 c0 = {}, c1 = {};
+#pragma unroll
+      for (int kc = 0; kc < KC2; ++kc) {
+        const u32x4 a = *(const u32x4 *)(lds + OFF_W2 + ((mb * KC2 + kc) * 64 + lane) * 4);
+        c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                      __builtin_bit_cast(bf16x8, H1[0][kc >> 1][kc & 1]), c0, 0, 0, 0);
+        c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                      __builtin_bit_cast(bf16x8, H1[1][kc >> 1][kc & 1]), c1, 0, 0, 0);
+      }
+      const float *b2 = (const float *)(lds + OFF_B2 + (mb * 2 + g) * 16);
+      const uint32_t *w3 = lds + OFF_W3 + (mb * 2 + g) * 8;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const float bl = b2[2 * q], bh = b2[2 * q + 1];
+        const uint32_t w = w3[q];
+        z0 = dot2_bf16(relu_bf16x2(pack_bf16(c0[2 * q] + bl, c0[2 * q + 1] + bh)), w, z0);
+        z1 = dot2_bf16(relu_bf16x2(pack_bf16(c1[2 * q] + bl, c1[2 * q + 1] + bh)), w, z1);
+      }
+    }
+    // lanes l and l ^ 32 hold the two halves of the same record's dot
+    // product; after the swap lane l < 32 adds block 0's halves of record l
+    // and lane l >= 32 block 1's halves of record l.
+    uint32_t a0 = __builtin_bit_cast(uint32_t, z0), a1 = __builtin_bit_cast(uint32_t, z1);
+    swap32(a0, a1);
+    return __builtin_bit_cast(float, a0) + __builtin_bit_cast(float, a1) +
+           __builtin_bit_cast(float, lds[OFF_B3]);
+  }
+};
+
+// ------------------------------------------------------------ fp32 MFMA head
+// Same orientation with v_mfma_f32_32x32x2_f32 (K = 2 per instruction):
+//   A[i][k]: lane l holds row l % 32, k = g;  B[k][j]: col l % 32, k = g;
+//   C as for the bf16 instruction.
+template <int IN, int HID>
+struct HeadF32 {
+  static constexpr int MB = HID / 32;
+  static constexpr int C1 = IN / 2;
+  static constexpr int W1_DW = MB * C1 * 64;
+  static constexpr int W2_DW = MB * MB * 64 * 16;
+  static constexpr int B2_DW = MB * 2 * 16;
+  static constexpr int W3_DW = MB * 2 * 16;
+  static constexpr int OFF_W2 = W1_DW;
+  static constexpr int OFF_B2 = OFF_W2 + W2_DW;
+  static constexpr int OFF_W3 = OFF_B2 + B2_DW;
+  static constexpr int OFF_B3 = OFF_W3 + W3_DW;
+  static constexpr int LDS_DW = OFF_B3 + 4;
+  static constexpr bool kMlp = true;
+
+  __device__ static __forceinline__ int out_of(int mb, int g, int r) {
+    return mb * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
+  }
+
+  __device__ static void stage(uint32_t *lds, int fam, const EvalParams &p) {
+    const float *w1 = (const float *)p.w1 + (size_t)fam * HID * IN;
+    const float *w2 = (const float *)p.w2 + (size_t)fam * HID * HID;
+    const float *b2 = (const float *)p.b2 + (size_t)fam * HID;
+    const float *w3 = (const float *)p.w3 + (size_t)fam * HID;
+    float *f = (float *)lds;
+    for (int d = threadIdx.x; d < W1_DW; d += kWgThreads) {
+      const int lane = d & 63, c = (d >> 6) % C1, mb = (d >> 6) / C1;
+      f[d] = w1[(mb * 32 + (lane & 31)) * IN + 2 * c + (lane >> 5)];
+    }
+    // [mb2][mb][lane][r]: W2[out = mb2 32 + l % 32][in = out_of(mb, g, r)]
+    for (int d = threadIdx.x; d < W2_DW; d += kWgThreads) {
+      const int r = d & 15, lane = (d >> 4) & 63, blk = d >> 10;
+      const int mb = blk % MB, mb2 = blk / MB;
+      f[OFF_W2 + d] = w2[(mb2 * 32 + (lane & 31)) * HID + out_of(mb, lane >> 5, r)];
+    }
+    for (int d = threadIdx.x; d < B2_DW; d += kWgThreads) {
+      const int r = d & 15, g = (d >> 4) & 1, mb = d >> 5;
+      f[OFF_B2 + d] = b2[out_of(mb, g, r)];
+      f[OFF_W3 + d] = w3[out_of(mb, g, r)];
+    }
+    if (threadIdx.x == 0) f[OFF_B3] = ((const float *)p.b3)[fam];
+  }
+
+  __device__ static __forceinline__ float mlp(const float (&x)[IN], const uint32_t *lds) {
+    const int lane = threadIdx.x & 63, g = lane >> 5;
+    const float *f = (const float *)lds;
+    float XB[2][C1];
+#pragma unroll
+    for (int c = 0; c < C1; ++c) {
+      uint32_t lo = __builtin_bit_cast(uint32_t, x[2 * c]);
+      uint32_t hi = __builtin_bit_cast(uint32_t, x[2 * c + 1]);
+      swap32(lo, hi);
+      XB[0][c] = __builtin_bit_cast(float, lo);
+      XB[1][c] = __builtin_bit_cast(float, hi);
+    }
+    f32x16 H1[2][MB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      f32x16 c0 = {}, c1 = {};
+#pragma unroll
+      for (int c = 0; c < C1; ++c) {
+        const float a = f[(mb * C1 + c) * 64 + lane];
+        c0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a, XB[0][c], c0, 0, 0, 0);
+        c1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a, XB[1][c], c1, 0, 0, 0);
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        c0[r] = fmaxf(c0[r], 0.0f);
+        c1[r] = fmaxf(c1[r], 0.0f);
+      }
+      H1[0][mb] = c0;
+      H1[1][mb] = c1;
+    }
+    float z0 = 0.0f, z1 = 0.0f;
+#pragma unroll 1
+    for (int mb2 = 0; mb2 < MB; ++mb2) {
+      f32x16 c0 = {}, c1 = {};
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const float *a = f + OFF_W2 + ((mb2 * MB + mb) * 64 + lane) * 16;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          c0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[r], H1[0][mb][r], c0, 0, 0, 0);
+          c1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[r], H1[1][mb][r], c1, 0, 0, 0);
+        }
+      }
+      const float *b2 = f + OFF_B2 + (mb2 * 2 + g) * 16;
+      const float *w3 = f + OFF_W3 + (mb2 * 2 + g) * 16;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        z0 = fmaf(w3[r], fmaxf(c0[r] + b2[r], 0.0f), z0);
+        z1 = fmaf(w3[r], fmaxf(c1[r] + b2[r], 0.0f), z1);
+      }
+    }
+    uint32_t a0 = __builtin_bit_cast(uint32_t, z0), a1 = __builtin_bit_cast(uint32_t, z1);
+    swap32(a0, a1);
+    return __builtin_bit_cast(float, a0) + __builtin_bit_cast(float, a1) + f[OFF_B3];
+  }
+};
+
+struct HeadOne {
+  static constexpr int LDS_DW = 1;
+  static constexpr bool kMlp = false;
+  __device__ static void stage(uint32_t *, int, const EvalParams &) {}
+  template <int IN>
+  __device__ static float mlp(const float (&)[IN], const uint32_t *) { return 0.0f; }
+};
+
+template <int KIND> struct KindOf;
+template <> struct KindOf<kEtaOne> { using H = HeadOne; static constexpr int IN = 16; };
+template <> struct KindOf<kF32_16_64> { using H = HeadF32<16, 64>; static constexpr int IN = 16; };
+template <> struct KindOf<kF32_16_128> { using H = HeadF32<16, 128>; static constexpr int IN = 16; };
+template <> struct KindOf<kF32_32_64> { using H = HeadF32<32, 64>; static constexpr int IN = 32; };
+template <> struct KindOf<kF32_32_128> { using H = HeadF32<32, 128>; static constexpr int IN = 32; };
+template <> struct KindOf<kBF16_16_64> { using H = HeadBF16<16, 64>; static constexpr int IN = 16; };
+template <> struct KindOf<kBF16_16_128> { using H = HeadBF16<16, 128>; static constexpr int IN = 16; };
+template <> struct KindOf<kBF16_16_256> { using H = HeadBF16<16, 256>; static constexpr int IN = 16; };
+template <> struct KindOf<kBF16_32_64> { using H = HeadBF16<32, 64>; static constexpr int IN = 32; };
+template <> struct KindOf<kBF16_32_128> { using H = HeadBF16<32, 128>; static constexpr int IN = 32; };
+template <> struct KindOf<kBF16_32_256> { using H = HeadBF16<32, 256>; static constexpr int IN = 32; };
+
+// ------------------------------------------------------------ evaluation
+// Workgroup = 4 waves; a workgroup tile is 4 consecutive 64-record wave
+// tiles of one family, so the family's head is staged in LDS once and
+// shared.  Workgroups stride over workgroup tiles and restage only when the
+// family changes (records are family-major).
+template <int KIND>
+__global__ __launch_bounds__(kWgThreads) void k_eval(EvalParams p) {
+  using H = typename KindOf<KIND>::H;
+  constexpr int IN = KindOf<KIND>::IN;
+  __shared__ uint32_t lds[H::LDS_DW];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n_wgt = p.wgt_off[KS_NFAM];
+  int staged = -1;
+  for (int wt = blockIdx.x; wt < n_wgt; wt += gridDim.x) {
+    int fam = 0;
+    while (wt >= p.wgt_off[fam + 1]) ++fam;
+    if constexpr (H::kMlp) {
+      if (fam != staged) {
+        __syncthreads();
+        H::stage(lds, fam, p);
+        __syncthreads();
+        staged = fam;
+      }
+    }
+    const int tile_in_fam = (wt - p.wgt_off[fam]) * kWgWaves + wave;
+    const int64_t fam_lo = p.fam_off[fam], fam_hi = p.fam_off[fam + 1];
+    const int64_t row0 = fam_lo + (int64_t)tile_in_fam * kTileRows;
+    if (row0 >= fam_hi) continue;  // an idle wave of the family's last workgroup tile
+    const int nvalid = (int)((fam_hi - row0) < kTileRows ? (fam_hi - row0) : kTileRows);
+    const bool valid = lane < nvalid;
+    const int64_t row = row0 + (valid ? lane : 0);
+
+    const uint32_t st = p.step[row];
+    uint32_t bad = 0;
+    if ((int64_t)st >= p.n_steps) bad |= kErrStep;
+    const uint32_t nn = p.n[row], kk = p.k[row];
+    const Cnt c = record_counts(fam, p.m[row], nn, kk, p.a[row], p.b[row], st, p, bad);
+    if (valid && bad) atomicOr(p.err, bad);
+    const bool live = valid && !(bad & kErrStep);
+    if (valid) {
+      if (p.o_flops) p.o_flops[row] = c.F;
+      if (p.o_bytes) p.o_bytes[row] = c.Bt;
+      if (p.o_blocks) p.o_blocks[row] = c.B;
+    }
+    const RowC rc = row_consts(c, nn, kk);
+
+    // segment structure of this tile (spec-independent): keys are sorted
+    const uint32_t key = live ? st : kNoKey;
+    const uint32_t key_dn = __shfl_down(key, 1);
+    const bool is_tail = live && (lane == 63 || key_dn != key);
+    const uint32_t key0 = __shfl(key, 0);
+    const uint32_t prev = row0 > fam_lo ? p.step[row0 - 1] : kNoKey;
+    const bool to_carry = is_tail && key == key0 && prev == key0;
+    const int tile_id = p.tile_off[fam] + tile_in_fam;
+
+    for (int s = 0; s < p.n_specs; ++s) {
+      const SpecC sc = load_spec(p.specs + s);
+      const Roof o = roofline(rc, sc);
+      float eta = 1.0f;
+      if constexpr (H::kMlp) {
+        float x[IN];
+        features<IN>(rc, sc, o, x);
+        const float z = H::mlp(x, lds);
+        eta = 1.0f + __expf(-z);
+      }
+      const float t = fmaxf(o.t_roof * eta, sc.t0);
+      if (valid) {
+        const size_t i = (size_t)s * (size_t)p.fam_off[KS_NFAM] + (size_t)row;
+        if (p.o_troof) p.o_troof[i] = o.t_roof;
+        if (p.o_eta) p.o_eta[i] = eta;
+        if (p.o_t) p.o_t[i] = t;
+      }
+      if (p.partial) {
+        // segmented inclusive scan over the sorted step keys
+        double v = live ? (double)t : 0.0;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+          const double w = __shfl_up(v, off);
+          const uint32_t kw = __shfl_up(key, off);
+          if (lane >= off && kw == key) v += w;
+        }
+        if (is_tail) {
+          if (to_carry)
+            p.carry[(size_t)s * p.n_tiles + tile_id] = v;
+          else
+            p.partial[((size_t)s * KS_NFAM + fam) * p.n_steps + key] = v;
+        }
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------ step finish
+__device__ __forceinline__ uint32_t lower_bound(const uint32_t *__restrict__ a, uint32_t lo, uint32_t hi,
+                                                uint32_t v) {
+  while (lo < hi) {
+    const uint32_t mid = lo + ((hi - lo) >> 1);
+    if (a[mid] < v) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+
+// record range [r0, r1) of step j within family f
+__global__ void k_seg_range(FinishParams p) {
+  const int64_t total = (int64_t)KS_NFAM * p.n_steps;
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int f = (int)(idx / p.n_steps);
+    const uint32_t j = (uint32_t)(idx - (int64_t)f * p.n_steps);
+    const uint32_t lo = (uint32_t)p.fam_off[f], hi = (uint32_t)p.fam_off[f + 1];
+    const uint32_t r0 = lower_bound(p.step, lo, hi, j);
+    const uint32_t r1 = lower_bound(p.step, r0, hi, j + 1);
+    p.range[2 * idx] = r0;
+    p.range[2 * idx + 1] = r1;
+  }
+}
+
+// per (spec, step): t_body, t_comm (Eq. 3, two all-reduces per layer),
+// t_gpu and t_step (Eq. 4)
+__global__ void k_finish(FinishParams p) {
+  const int64_t total = (int64_t)p.n_specs * p.n_steps;
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int s = (int)(idx / p.n_steps);
+    const int64_t j = idx - (int64_t)s * p.n_steps;
+    double body = 0.0;
+    for (int f = 0; f < KS_NFAM; ++f) {
+      const uint32_t r0 = p.range[2 * (f * p.n_steps + j)];
+      const uint32_t r1 = p.range[2 * (f * p.n_steps + j) + 1];
+      if (r0 >= r1) continue;
+      body += p.partial[((size_t)s * KS_NFAM + f) * p.n_steps + j];
+      const int64_t base = p.fam_off[f];
+      const int t_first = p.tile_off[f] + (int)((r0 - base) / kTileRows);
+      const int t_last = p.tile_off[f] + (int)((r1 - 1 - base) / kTileRows);
+      for (int t = t_first + 1; t <= t_last; ++t) body += p.carry[(size_t)s * p.n_tiles + t];
+    }
+    const ks_spec sp = p.specs[s];
+    const double P = (double)p.tp[j];
+    const double S = (double)p.agg[j] * (double)p.hidden[j] * (double)p.elem_bytes;
+    double t_ar = 0.0;
+    if (P > 1.0)
+      t_ar = sp.ar_alpha0 + sp.ar_alpha_log2p * log2(P) + 2.0 * (P - 1.0) / P * S / sp.ar_beta;
+    const double comm = 2.0 * (double)p.layers[j] * t_ar;
+    const double gpu = p.host.body_scale * body + comm;
+    const double step = fmax(gpu + (double)p.n_launch[j] * p.host.c_disp, p.host.ell) +
+                        fmax(0.0, p.host.c_ovl - gpu) + p.host.c_tail;
+    p.t_body[idx] = body;
+    p.t_gpu[idx] = gpu;
+    p.t_step[idx] = step;
+  }
+}
+
+// ------------------------------------------------------------ validation
+__global__ void k_validate(ValidateParams p) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  uint32_t bad = 0;
+  for (int64_t i = t0; i < p.n_rows; i += stride) {
+    int f = 0;
+    while (i >= p.fam_off[f + 1]) ++f;
+    const uint32_t st = p.step[i];
+    if ((int64_t)st >= p.n_steps) bad |= kErrStep;
+    if (i > p.fam_off[f] && p.step[i - 1] > st) bad |= kErrOrder;
+    const uint32_t m = p.m[i], n = p.n[i], k = p.k[i], a = p.a[i], b = p.b[i];
+    if (m >= (1u << 24) || n >= (1u << 18) || k >= (1u << 18)) bad |= kErrRange;
+    if ((f == KS_ATTN_PREFILL || f == KS_ATTN_DECODE) && (n >= 4096u || k >= 4096u || a >= 4096u))
+      bad |= kErrRange;
+    if (f == KS_GROUPED_GEMM) {
+      if (a > 1024u || (uint64_t)b + a > (uint64_t)p.n_expert_rows) {
+        bad |= kErrExpert;
+      } else {
+        uint64_t ms = 0;
+        for (uint32_t e = 0; e < a; ++e) ms += p.expert_rows[b + e];
+        if (ms >= (1ull << 24)) bad |= kErrRange;
+      }
+    }
+  }
+  for (int64_t j = t0; j < p.n_steps; j += stride) {
+    if (p.req_off[j] > p.req_off[j + 1] || (int64_t)p.req_off[j + 1] > p.n_req) bad |= kErrReq;
+    if (p.agg[2 * p.n_steps + j] >= (1ull << 40)) bad |= kErrRange;
+    if (p.tp && p.tp[j] < 1u) bad |= kErrRange;
+  }
+  if (t0 == 0 && p.n_steps > 0 && p.req_off[0] != 0) bad |= kErrReq;
+  for (int64_t r = t0; r < p.n_req; r += stride)
+    if (p.req_q[r] >= (1u << 24) || p.req_h[r] >= (1u << 24)) bad |= kErrRange;
+  for (int64_t s = t0; s < p.n_specs; s += stride) {
+    const ks_spec sp = p.specs[s];
+    const bool ok = sp.peak_flops > 0.0 && sp.peak_flops < 1e30 && sp.hbm_bw > 0.0 && sp.hbm_bw < 1e30 &&
+                    sp.t0 >= 0.0 && sp.t0 < 1e3 && sp.l2_bytes >= 0.0 && sp.l2_bytes < 1e30 &&
+                    sp.ar_beta > 0.0 && sp.ar_beta < 1e30 && sp.ar_alpha0 >= 0.0 && sp.ar_alpha0 < 1e3 &&
+                    sp.ar_alpha_log2p >= 0.0 && sp.ar_alpha_log2p < 1e3 && sp.n_cu >= 1u && sp.n_cu <= 65535u;
+    if (!ok) bad |= kErrSpec;
+  }
+  if (bad) atomicOr(p.err, bad);
+}
+
+// ------------------------------------------------------------ launchers
+static int grid_for(int64_t n, int block, int cap) {
+  int64_t g = (n + block - 1) / block;
+  if (g < 1) g = 1;
+  return (int)(g < cap ? g : cap);
+}
+
+hipError_t launch_clear(uint32_t *err, hipStream_t s) {
+  hipLaunchKernelGGL(k_clear, dim3(1), dim3(64), 0, s, err);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_agg(const uint32_t *req_off, const uint32_t *q, const uint32_t *h, int64_t n_steps,
+                           int64_t n_req, uint64_t *agg, uint32_t *err, hipStream_t s) {
+  if (n_steps == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_attn_agg, dim3(grid_for(n_steps, 256, 4096)), dim3(256), 0, s, req_off, q, h, n_steps,
+                     n_req, agg, err);
+  return hipGetLastError();
+}
+
+template <int KIND>
+static int lds_bytes() {
+  return (int)sizeof(uint32_t) * KindOf<KIND>::H::LDS_DW;
+}
+
+int eval_grid(int kind, int n_wgt) {
+  // workgroups resident per CU: bounded by LDS (160 KB per CU) and by the
+  // register budget of the head kernels; eta = 1 streams want many.
+  static const int lds[kNumKinds] = {
+      lds_bytes<kEtaOne>(), lds_bytes<kF32_16_64>(), lds_bytes<kF32_16_128>(), lds_bytes<kF32_32_64>(),
+      lds_bytes<kF32_32_128>(), lds_bytes<kBF16_16_64>(), lds_bytes<kBF16_16_128>(),
+      lds_bytes<kBF16_16_256>(), lds_bytes<kBF16_32_64>(), lds_bytes<kBF16_32_128>(),
+      lds_bytes<kBF16_32_256>()};
+  int per_cu = kind == kEtaOne ? 8 : 2;
+  const int by_lds = (160 * 1024) / (lds[kind] > 0 ? lds[kind] : 1);
+  if (by_lds < per_cu) per_cu = by_lds < 1 ? 1 : by_lds;
+  const int cap = 256 * per_cu;
+  return n_wgt < cap ? (n_wgt < 1 ? 1 : n_wgt) : cap;
+}
+
+template <int KIND>
+static hipError_t launch_kind(const EvalParams &p, hipStream_t s) {
+  const int grid = eval_grid(KIND, p.wgt_off[KS_NFAM]);
+  hipLaunchKernelGGL(k_eval<KIND>, dim3(grid), dim3(kWgThreads), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_eval(int kind, const EvalParams &p, hipStream_t s) {
+  if (p.wgt_off[KS_NFAM] == 0) return hipSuccess;
+  switch (kind) {
+    case kEtaOne: return launch_kind<kEtaOne>(p, s);
+    case kF32_16_64: return launch_kind<kF32_16_64>(p, s);
+    case kF32_16_128: return launch_kind<kF32_16_128>(p, s);
+    case kF32_32_64: return launch_kind<kF32_32_64>(p, s);
+    case kF32_32_128: return launch_kind<kF32_32_128>(p, s);
+    case kBF16_16_64: return launch_kind<kBF16_16_64>(p, s);
+    case kBF16_16_128: return launch_kind<kBF16_16_128>(p, s);
+    case kBF16_16_256: return launch_kind<kBF16_16_256>(p, s);
+    case kBF16_32_64: return launch_kind<kBF16_32_64>(p, s);
+    case kBF16_32_128: return launch_kind<kBF16_32_128>(p, s);
+    case kBF16_32_256: return launch_kind<kBF16_32_256>(p, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_finish(const FinishParams &p, hipStream_t s) {
+  if (p.n_steps == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_seg_range, dim3(grid_for((int64_t)KS_NFAM * p.n_steps, 256, 4096)), dim3(256), 0, s, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_finish, dim3(grid_for((int64_t)p.n_specs * p.n_steps, 256, 8192)), dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_validate(const ValidateParams &p, hipStream_t s) {
+  hipLaunchKernelGGL(k_validate, dim3(1024), dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
+}  // namespace ks

@@ -1,0 +1,147 @@
+"""The C-ABI library: loads, exports every declared symbol, matches the
+header's struct layout, and rejects bad host arguments before any launch.
+CPU only (no compute call reaches a GPU)."""
+import ctypes as C
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2606_28565_amd import abi
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ks.h")
+
+
+def _declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w]+\**\s+\**(ks_\w+)\s*\(", src, flags=re.M)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = abi.load()
+    names = _declared_functions()
+    assert {"ks_eval_kernels", "ks_eval_steps", "ks_workspace_bytes", "ks_validate",
+            "ks_device_status", "ks_last_error", "ks_version"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert abi.ks_version().startswith("ks ")
+
+
+def test_struct_layout_matches_header(tmp_path):
+    """Compile a C probe of offsetof/sizeof against include/ks.h and compare
+    with the ctypes mirrors."""
+    structs = {"ks_desc": abi.ks_desc, "ks_spec": abi.ks_spec, "ks_heads": abi.ks_heads,
+               "ks_steps": abi.ks_steps, "ks_host": abi.ks_host,
+               "ks_kernel_out": abi.ks_kernel_out, "ks_step_out": abi.ks_step_out}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "ks.h"', "int main(void){"]
+    for s, cls in structs.items():
+        lines.append(f'printf("{s} size %zu\\n", sizeof({s}));')
+        for f, _ in cls._fields_:
+            lines.append(f'printf("{s} {f} %zu\\n", offsetof({s}, {f}));')
+    lines.append("return 0;}")
+    c = tmp_path / "probe.c"
+    c.write_text("\n".join(lines))
+    exe = tmp_path / "probe"
+    subprocess.run(["gcc", "-D__HIP_PLATFORM_AMD__", "-I", os.path.join(ROOT, "include"),
+                    "-I", "/opt/rocm/include", str(c), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split("\n")
+    got = {}
+    for line in out:
+        if line:
+            s, f, v = line.split()
+            got[(s, f)] = int(v)
+    for s, cls in structs.items():
+        assert got[(s, "size")] == C.sizeof(cls), s
+        for f, _ in cls._fields_:
+            assert got[(s, f)] == getattr(cls, f).offset, (s, f)
+
+
+def _desc(n_rows=10, n_steps=2):
+    d = abi.ks_desc()
+    d.n_rows = n_rows
+    for f in range(abi.NFAM + 1):
+        d.fam_off[f] = 0 if f == 0 else n_rows
+    for name in ("step", "m", "n", "k", "a", "b", "req_off", "req_q", "req_h"):
+        setattr(d, name, 0x1000)
+    d.n_steps = n_steps
+    d.n_req = 3
+    d.elem_bytes = 2
+    return d
+
+
+def _call_eval(d, n_specs=1, heads=None, out=True, ws=0x100000, ws_bytes=1 << 30, specs=0x2000):
+    h = heads or abi.ks_heads(16, 64, abi.KS_F32, abi.KS_ETA_ONE)
+    o = abi.ks_kernel_out()
+    return abi.ks_eval_kernels(d, specs, n_specs, h, o if out else None, ws, ws_bytes, None, check=False) \
+        if out else abi.load().ks_eval_kernels(C.byref(d), specs, n_specs, C.byref(h), None, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("mutate,status,needle", [
+    (lambda d: setattr(d, "step", None), abi.KS_EINVAL, "record array"),
+    (lambda d: d.fam_off.__setitem__(3, 1), abi.KS_EINVAL, "fam_off"),
+    (lambda d: [d.fam_off.__setitem__(i, 9) for i in range(1, abi.NFAM + 1)], abi.KS_EINVAL, "!= n_rows"),
+    (lambda d: setattr(d, "req_off", None), abi.KS_EINVAL, "req_off"),
+    (lambda d: setattr(d, "elem_bytes", 0), abi.KS_ERANGE, "elem_bytes"),
+    (lambda d: setattr(d, "n_rows", -1), abi.KS_ERANGE, "n_rows"),
+    (lambda d: setattr(d, "n_steps", 0), abi.KS_EINVAL, "n_steps"),
+])
+def test_bad_descriptor_rejected_on_host(mutate, status, needle):
+    d = _desc()
+    mutate(d)
+    assert _call_eval(d) == status
+    assert needle in abi.ks_last_error()
+
+
+def test_bad_specs_heads_workspace_rejected_on_host():
+    d = _desc()
+    assert _call_eval(d, n_specs=0) == abi.KS_EINVAL
+    assert _call_eval(d, specs=None) == abi.KS_EINVAL
+    assert _call_eval(d, ws=None) == abi.KS_EWORKSPACE
+    assert _call_eval(d, ws_bytes=16) == abi.KS_EWORKSPACE
+    assert _call_eval(d, ws=0x100010) == abi.KS_EWORKSPACE     # misaligned
+    bad_heads = [abi.ks_heads(24, 64, abi.KS_F32, abi.KS_ETA_MLP, 1, 1, 1, 1, 1),
+                 abi.ks_heads(16, 256, abi.KS_F32, abi.KS_ETA_MLP, 1, 1, 1, 1, 1),
+                 abi.ks_heads(16, 96, abi.KS_BF16, abi.KS_ETA_MLP, 1, 1, 1, 1, 1),
+                 abi.ks_heads(16, 64, 7, abi.KS_ETA_MLP, 1, 1, 1, 1, 1),
+                 abi.ks_heads(16, 64, abi.KS_F32, abi.KS_ETA_MLP, 1, None, 1, 1, 1),
+                 abi.ks_heads(16, 64, abi.KS_F32, 5)]
+    for h in bad_heads:
+        assert _call_eval(d, heads=h) == abi.KS_EINVAL, abi.ks_last_error()
+    assert abi.load().ks_eval_kernels(C.byref(d), 0x2000, 1, C.byref(abi.ks_heads(16, 64, 0, 1)),
+                                      None, 0x100000, 1 << 30, None) == abi.KS_EINVAL
+
+
+def test_eval_steps_host_checks():
+    d = _desc()
+    lib = abi.load()
+    st = abi.ks_steps(3, 0x10, 0x10, 0x10, 0x10)      # n_steps mismatch
+    h = abi.ks_heads(16, 64, abi.KS_F32, abi.KS_ETA_ONE)
+    host = abi.ks_host(0, 0, 0, 0, 1)
+    so = abi.ks_step_out(0x10, 0x10, 0x10)
+    r = lib.ks_eval_steps(C.byref(d), C.byref(st), 0x2000, 1, C.byref(h), C.byref(host),
+                          C.byref(so), None, 0x100000, 1 << 30, None)
+    assert r == abi.KS_EINVAL and "n_steps" in abi.ks_last_error()
+    st.n_steps = 2
+    so.t_gpu = None
+    r = lib.ks_eval_steps(C.byref(d), C.byref(st), 0x2000, 1, C.byref(h), C.byref(host),
+                          C.byref(so), None, 0x100000, 1 << 30, None)
+    assert r == abi.KS_EINVAL and "step output" in abi.ks_last_error()
+
+
+def test_workspace_bytes_grows_with_specs():
+    d = _desc(n_rows=1000, n_steps=10)
+    a, b = abi.ks_workspace_bytes(d, 1), abi.ks_workspace_bytes(d, 64)
+    assert 0 < a < b and a % 256 == 0 and b % 256 == 0
+    assert abi.ks_workspace_bytes(d, 0) == 0
+
+
+def test_missing_library_fails_loudly(tmp_path):
+    with pytest.raises(RuntimeError, match="no fallback"):
+        abi._lib, saved = None, abi._lib
+        try:
+            abi.load(str(tmp_path / "nope.so"))
+        finally:
+            abi._lib = saved

@@ -1,0 +1,235 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 oracle.
+
+Tolerances (design notes, "Oracle and parity"): counts bit-exact; t_roof and
+fp32-head outputs 1e-5 relative; bf16-head eta 1e-2 relative and z within
+ZTOL absolute; given the GPU's eta, t = max(t_roof eta, t0) to 1e-5; step
+outputs 1e-5 (fp32 heads, eta = 1) and 1e-2 (bf16 heads)."""
+import numpy as np
+import pytest
+import torch  # noqa: F401  (runtime loads at collection, not inside a timed test)
+
+from oracle import ks_oracle as o
+from workload import gen
+from tests import gpu_helpers as g
+from tests.helpers import make_desc, spec, steprec
+
+pytestmark = pytest.mark.gpu
+
+REL = 1e-5
+REL_BF16 = 1e-2
+# |z_gpu - z_oracle| for std-0.1 bf16 heads: a flipped bf16 rounding of one
+# hidden activation moves z by about |w3| 2^-8 |h2| ~ 0.1 * 2e-4; even all
+# 256 activations of both layers flipping the same way stay below 5e-3.
+ZTOL = 5e-3
+
+
+def _z_from_eta(eta):
+    return -np.log(np.asarray(eta, np.float64) - 1.0)
+
+
+def _check_kernels(wl, gpu, ref, bf16, eta_one=False, ztol=ZTOL):
+    c = ref["counts"]
+    np.testing.assert_array_equal(gpu["flops"], c["F"])
+    np.testing.assert_array_equal(gpu["bytes"], c["Bt"])
+    np.testing.assert_array_equal(gpu["blocks"], c["B"])
+    assert g.rel_err(gpu["t_roof"], ref["t_roof"]).max() <= REL
+    if eta_one:
+        assert (gpu["eta"] == 1.0).all()
+        assert g.rel_err(gpu["t_kernel"], ref["t"]).max() <= REL
+        return
+    t0 = wl.specs["t0"][: gpu["eta"].shape[0], None]
+    cond = np.maximum(ref["t_roof"] * gpu["eta"].astype(np.float64), t0)
+    assert g.rel_err(gpu["t_kernel"], cond).max() <= REL
+    if bf16:
+        assert g.rel_err(gpu["eta"], ref["eta"]).max() <= REL_BF16
+        dz = np.abs(_z_from_eta(gpu["eta"]) - ref["z"])
+        assert dz.max() <= ztol, dz.max()
+        assert g.rel_err(gpu["t_kernel"], ref["t"]).max() <= REL_BF16
+    else:
+        assert g.rel_err(gpu["eta"], ref["eta"]).max() <= REL
+        assert g.rel_err(gpu["t_kernel"], ref["t"]).max() <= REL
+
+
+def _check_steps(wl, gpu, ref_steps, bf16, n_specs):
+    tol = REL_BF16 if bf16 else REL
+    for key in ("t_body", "t_gpu", "t_step"):
+        e = g.rel_err(gpu[key], ref_steps[key][:n_specs])
+        assert e.max() <= tol, (key, e.max())
+
+
+def _steps_given_eta(wl, gpu, ref_k, n_specs):
+    """Oracle step terms with the GPU's eta substituted: isolates the
+    aggregation and assembly from the head."""
+    t0 = wl.specs["t0"][:n_specs, None]
+    t = np.maximum(ref_k["t_roof"][:n_specs] * gpu["eta"].astype(np.float64), t0)
+    kern = dict(ref_k)
+    kern["t"] = t
+    return o.eval_steps(wl.desc, wl.steps, wl.specs, wl.host, spec_ids=range(n_specs), kern=kern)
+
+
+# ------------------------------------------------------------------- c1 ----
+@pytest.fixture(scope="module")
+def c1():
+    wl = gen.config1()
+    return wl, o.eval_kernels(wl.desc, wl.specs, wl.heads)
+
+
+def test_c1_kernels_fp32_head(c1):
+    wl, ref = c1
+    gpu = g.eval_kernels(wl)
+    _check_kernels(wl, gpu, ref, bf16=False)
+
+
+def test_c1_steps_fp32_head(c1):
+    wl, ref = c1
+    gpu = g.eval_steps(wl)
+    rs = o.eval_steps(wl.desc, wl.steps, wl.specs, wl.host, wl.heads, kern=ref)
+    _check_steps(wl, gpu, rs, bf16=False, n_specs=2)
+    _check_kernels(wl, gpu, ref, bf16=False)
+
+
+def test_c1_eta_one():
+    wl = gen.config1()
+    ref = o.eval_kernels(wl.desc, wl.specs, eta_one=True)
+    gpu = g.eval_steps(wl, eta_one=True)
+    _check_kernels(wl, gpu, ref, bf16=False, eta_one=True)
+    rs = o.eval_steps(wl.desc, wl.steps, wl.specs, wl.host, eta_one=True, kern=ref)
+    _check_steps(wl, gpu, rs, bf16=False, n_specs=2)
+
+
+def test_c1_deterministic():
+    wl = gen.config1(0, 200)
+    a = g.eval_steps(wl)
+    b = g.eval_steps(wl)
+    for key in a:
+        np.testing.assert_array_equal(a[key], b[key])
+
+
+# ------------------------------------------------------------ bf16 heads ----
+def _bf16_case(wl, n_specs=None):
+    n_specs = n_specs or wl.n_specs
+    ref = o.eval_kernels(wl.desc, wl.specs, wl.heads, spec_ids=range(n_specs))
+    gpu = g.eval_steps(wl, n_specs=n_specs)
+    _check_kernels(wl, gpu, ref, bf16=True)
+    rs = o.eval_steps(wl.desc, wl.steps, wl.specs, wl.host, wl.heads, spec_ids=range(n_specs), kern=ref)
+    _check_steps(wl, gpu, rs, bf16=True, n_specs=n_specs)
+    ge = _steps_given_eta(wl, gpu, ref, n_specs)
+    _check_steps(wl, gpu, ge, bf16=False, n_specs=n_specs)
+    return gpu, ref
+
+
+def test_c4_subset_bf16_16_128():
+    _bf16_case(gen.config4(n_specs=24, grid_steps=25, c1_steps=40))
+
+
+def test_c3_moe_subset():
+    _bf16_case(gen.config3(0, 30))
+
+
+def test_c5_subset_bf16_32_256():
+    _bf16_case(gen.config5(0, 24))
+
+
+@pytest.mark.parametrize("shape_idx", range(6))
+def test_c2_shape_subsets_with_tp(shape_idx):
+    _bf16_case(gen.config2(shape_idx, 0, 12))
+
+
+def test_c4_full_size_sampled():
+    """The 256-spec capacity grid at full size, in the launch configuration
+    the benchmark times; sampled (spec, step) outputs against the oracle run
+    on just those steps' records."""
+    wl = gen.config4()
+    gpu = g.eval_steps(wl)
+    rng = np.random.default_rng(11)
+    steps = np.unique(np.concatenate([[0, 999, 1000, wl.desc.n_steps - 1],
+                                      rng.integers(0, wl.desc.n_steps, 4)]))
+    specs = np.unique(np.concatenate([[0, wl.n_specs - 1], rng.integers(0, wl.n_specs, 4)]))
+    rows = np.nonzero(np.isin(wl.desc.step, steps))[0]
+    ref = o.eval_kernels(wl.desc, wl.specs, wl.heads, spec_ids=specs, rows=rows)
+    ge = np.maximum(ref["t_roof"] * gpu["eta"][specs][:, rows], wl.specs["t0"][specs, None])
+    assert g.rel_err(gpu["t_kernel"][specs][:, rows], ge).max() <= REL
+    assert g.rel_err(gpu["eta"][specs][:, rows], ref["eta"]).max() <= REL_BF16
+    c = ref["counts"]
+    np.testing.assert_array_equal(gpu["flops"][rows], c["F"])
+    for si, s in enumerate(specs):
+        body = np.bincount(wl.desc.step[rows], weights=ref["t"][si], minlength=wl.desc.n_steps)[steps]
+        body_ge = np.bincount(wl.desc.step[rows], weights=ge[si], minlength=wl.desc.n_steps)[steps]
+        assert g.rel_err(gpu["t_body"][s, steps], body).max() <= REL_BF16
+        assert g.rel_err(gpu["t_body"][s, steps], body_ge).max() <= REL
+
+
+# --------------------------------------------------------------- all kinds --
+KINDS = [("f32", 16, 64), ("f32", 16, 128), ("f32", 32, 64), ("f32", 32, 128),
+         ("bf16", 16, 64), ("bf16", 16, 128), ("bf16", 16, 256),
+         ("bf16", 32, 64), ("bf16", 32, 128), ("bf16", 32, 256)]
+
+
+@pytest.mark.parametrize("precision,in_dim,hidden", KINDS)
+@pytest.mark.parametrize("std", [0.1, 0.5])
+def test_every_head_kind(precision, in_dim, hidden, std):
+    wl = gen.config1(0, 6).with_heads(gen.make_heads(in_dim, hidden, precision, std=std))
+    ref = o.eval_kernels(wl.desc, wl.specs, wl.heads)
+    gpu = g.eval_kernels(wl)
+    # larger weights scale the effect of one flipped bf16 rounding
+    _check_kernels(wl, gpu, ref, bf16=precision == "bf16", ztol=ZTOL * (std / 0.1) ** 2)
+
+
+# ------------------------------------------------------------- edge cases --
+def _wl(desc, n_steps, heads=None, tp=1, layers=1, specs=None):
+    return gen.Workload("edge", desc, steprec(n_steps, layers=layers, hidden=64, tp=tp, n_launch=1),
+                        specs or spec(P=1e15, BW=4e12, n_cu=132, t0=2e-6),
+                        heads or gen.make_heads(16, 64, "f32"), gen.HostConsts())
+
+
+def _edge_check(wl):
+    ref = o.eval_kernels(wl.desc, wl.specs, wl.heads)
+    gpu = g.eval_steps(wl)
+    _check_kernels(wl, gpu, ref, bf16=wl.heads.precision == "bf16")
+    rs = o.eval_steps(wl.desc, wl.steps, wl.specs, wl.host, wl.heads, kern=ref)
+    _check_steps(wl, gpu, rs, bf16=wl.heads.precision == "bf16", n_specs=wl.n_specs)
+
+
+def test_single_record():
+    _edge_check(_wl(make_desc([(gen.GEMM, 0, 77, 300, 129, 0, 0)], [[(1, 5)]]), 1))
+
+
+def test_zero_work_and_empty_request_step():
+    rows = [(gen.EMBED, 0, 0, 64, 0, 0, 0), (gen.ATTN_DECODE, 1, 0, 8, 128, 2, 0),
+            (gen.ATTN_DECODE, 0, 0, 8, 128, 2, 0), (gen.SILU_MUL, 1, 0, 10, 0, 0, 0)]
+    _edge_check(_wl(make_desc(rows, [[], [(3, 7)]]), 2))
+
+
+def test_ragged_segments_crossing_tiles():
+    """One family whose step segments straddle 64-record tiles in every way:
+    lengths 1, 63, 64, 65, 130, 200 and single records between them."""
+    rows, reqs = [], []
+    lens = [1, 63, 64, 65, 1, 130, 1, 200, 2, 64]
+    for j, L in enumerate(lens):
+        reqs.append([(1 + j, 100 * j)])
+        rows += [(gen.GEMM, j, 3 + i, 128 + i, 64, 0, 0) for i in range(L)]
+        rows.append((gen.RMSNORM, j, 5 + j, 4096, 0, 0, 0))
+    _edge_check(_wl(make_desc(rows, reqs), len(lens)))
+
+
+def test_steps_missing_from_families_and_tp_comm():
+    rows = [(gen.GEMM, 0, 4, 4096, 4096, 0, 0), (gen.GEMM, 2, 9, 4096, 4096, 0, 0),
+            (gen.ATTN_PREFILL, 1, 0, 8, 128, 1, 0), (gen.LM_HEAD, 3, 2, 8000, 4096, 0, 0)]
+    reqs = [[(4, 0)], [(300, 5), (1, 9)], [(9, 1)], [(1, 1), (1, 2)]]
+    _edge_check(_wl(make_desc(rows, reqs), 4, tp=4, layers=3))
+
+
+def test_grouped_gemm_with_empty_experts():
+    rows = [(gen.GROUPED_GEMM, 0, 0, 256, 512, 4, 0), (gen.GROUPED_GEMM, 0, 0, 512, 256, 4, 4),
+            (gen.GROUPED_GEMM, 1, 0, 256, 512, 3, 8)]
+    experts = [0, 5, 0, 300, 0, 0, 0, 0, 129, 1, 0]
+    _edge_check(_wl(make_desc(rows, [[(3, 1)], [(5, 2)]], expert_rows=experts), 2,
+                    heads=gen.make_heads(16, 128, "bf16")))
+
+
+def test_many_specs_single_step():
+    rng = np.random.default_rng(4)
+    n = 37
+    sp = gen.specs_grid(n, 99)
+    rows = [(gen.GEMM, 0, int(m), 4096, 4096, 0, 0) for m in rng.integers(1, 5000, 70)]
+    _edge_check(_wl(make_desc(rows, [[(5, 9)]]), 1, specs=sp, heads=gen.make_heads(16, 128, "bf16")))
