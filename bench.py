@@ -75,7 +75,7 @@ def main() -> int:
     ap.add_argument("--eta-one", action="store_true", help="eta = 1 (pure roofline) mode")
     ap.add_argument("--per-pair", action="store_true", help="also write per-pair t_roof/eta/t_kernel")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-specs", type=int, default=2)
+    ap.add_argument("--cpu-specs", type=int, default=16)
     ap.add_argument("--cpu-threads", type=int, default=0)
     args = ap.parse_args()
 

@@ -292,12 +292,13 @@ def spec_at(specs, s):
 
 
 def eval_kernels(desc, specs, heads=None, eta_one=False, emulate_bf16=None,
-                 spec_ids=None, rows=None):
+                 spec_ids=None, rows=None, keep_features=False):
     """Per-kernel latency model for every (spec, record) pair.
 
     heads: a ``workload.gen.Heads``; eta_one forces eta = 1 (pure roofline).
     emulate_bf16 defaults to True for bf16 heads.  spec_ids / rows restrict
     the evaluation to a subset (counts are still exact per record).
+    keep_features also returns the feature vectors ("x").
     Returns counts (per record) and float64 arrays [n_spec_ids, n_sel_rows]."""
     cnt = kernel_counts(desc)
     n_specs = len(specs["peak_flops"])
@@ -310,6 +311,8 @@ def eval_kernels(desc, specs, heads=None, eta_one=False, emulate_bf16=None,
     out = {key: np.zeros((len(spec_ids), len(rows))) for key in
            ("t_roof", "eta", "t", "z", "t_comp", "t_mem", "u")}
     out["W"] = np.zeros((len(spec_ids), len(rows)), U64)
+    if keep_features and not eta_one:
+        out["x"] = np.zeros((len(spec_ids), len(rows), heads.in_dim))
     for si, s in enumerate(spec_ids):
         sp = spec_at(specs, s)
         rf = roofline(sub["F"], sub["Bt"], sub["B"], sp)
@@ -318,6 +321,8 @@ def eval_kernels(desc, specs, heads=None, eta_one=False, emulate_bf16=None,
             eta = np.ones(len(rows))
         else:
             x = features(sub, desc.n[rows], desc.k[rows], rf, sp, heads.in_dim)
+            if keep_features:
+                out["x"][si] = x
             z = np.zeros(len(rows))
             for f in np.unique(fam):
                 sel = fam == f
