@@ -19,6 +19,9 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # generated code on purpose.
 DEVICE_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
                 "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                # MFMA results stay in ordinary VGPRs: the epilogues are VALU
+                # work, and accumulator-register round trips cost a VALU op each
+                "-mllvm", "-amdgpu-mfma-vgpr-form",
                 "-Wall", "-Wno-unused-function"]
 HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall"]
 

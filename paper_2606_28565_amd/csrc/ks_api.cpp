@@ -32,12 +32,13 @@ constexpr size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 // Workspace layout (every region 256-byte aligned):
 //   header  : 256 B (uint32 flag word at offset 0)
+//   specc   : n_specs * 64 B               per-spec loop constants
 //   agg     : 4 * n_steps uint64           per-step attention work
 //   range   : KS_NFAM * n_steps * 2 uint32 per (family, step) record range
 //   partial : n_specs * KS_NFAM * n_steps double
 //   carry   : n_specs * n_tiles double
 struct Layout {
-  size_t agg, range, partial, carry, total;
+  size_t specc, agg, range, partial, carry, total;
 };
 
 struct Tiles {
@@ -62,6 +63,8 @@ Layout layout_of(const ks_desc *d, int32_t n_specs) {
   const size_t S = (size_t)d->n_steps;
   Layout L;
   size_t off = 256;
+  L.specc = off;
+  off += align256((size_t)n_specs * sizeof(ks::SpecC));
   L.agg = off;
   off += align256(4 * S * sizeof(uint64_t));
   L.range = off;
@@ -157,7 +160,7 @@ void fill_eval(ks::EvalParams &p, const ks_desc *d, const ks_spec *specs, int32_
   p.n_steps = d->n_steps;
   p.elem_bytes = d->elem_bytes;
   p.n_specs = n_specs;
-  p.specs = specs;
+  p.spec_c = reinterpret_cast<const ks::SpecC *>(ws + L.specc);
   const Tiles t = tiles_of(d);
   for (int f = 0; f <= KS_NFAM; ++f) {
     p.fam_off[f] = d->fam_off[f];
@@ -183,9 +186,12 @@ void fill_eval(ks::EvalParams &p, const ks_desc *d, const ks_spec *specs, int32_
   p.err = reinterpret_cast<uint32_t *>(ws);
 }
 
-ks_status prologue(const ks_desc *d, char *ws, const Layout &L, hipStream_t s) {
+ks_status prologue(const ks_desc *d, const ks_spec *specs, int32_t n_specs, char *ws, const Layout &L,
+                   hipStream_t s) {
   hipError_t e = ks::launch_clear(reinterpret_cast<uint32_t *>(ws), s);
   if (e != hipSuccess) return hip_fail(e, "clear launch");
+  e = ks::launch_spec_prep(specs, n_specs, reinterpret_cast<ks::SpecC *>(ws + L.specc), s);
+  if (e != hipSuccess) return hip_fail(e, "spec constants launch");
   e = ks::launch_attn_agg(d->req_off, d->req_q, d->req_h, d->n_steps, d->n_req,
                           reinterpret_cast<uint64_t *>(ws + L.agg), reinterpret_cast<uint32_t *>(ws), s);
   if (e != hipSuccess) return hip_fail(e, "attention aggregate launch");
@@ -227,7 +233,7 @@ ks_status ks_eval_kernels(const ks_desc *desc, const ks_spec *specs, int32_t n_s
   if (st != KS_OK) return st;
   if (!out) return fail(KS_EINVAL, "out is NULL");
   char *w = static_cast<char *>(ws);
-  st = prologue(desc, w, L, stream);
+  st = prologue(desc, specs, n_specs, w, L, stream);
   if (st != KS_OK) return st;
   ks::EvalParams p;
   fill_eval(p, desc, specs, n_specs, heads, out, w, L);
@@ -255,7 +261,7 @@ ks_status ks_eval_steps(const ks_desc *desc, const ks_steps *steps, const ks_spe
   if (!out || (desc->n_steps > 0 && (!out->t_body || !out->t_gpu || !out->t_step)))
     return fail(KS_EINVAL, "a step output is NULL");
   char *w = static_cast<char *>(ws);
-  st = prologue(desc, w, L, stream);
+  st = prologue(desc, specs, n_specs, w, L, stream);
   if (st != KS_OK) return st;
   ks::EvalParams p;
   fill_eval(p, desc, specs, n_specs, heads, kout, w, L);
@@ -302,7 +308,7 @@ ks_status ks_validate(const ks_desc *desc, const ks_steps *steps, const ks_spec 
     return fail(KS_EINVAL, "steps.n_steps %lld != desc.n_steps %lld", (long long)steps->n_steps,
                 (long long)desc->n_steps);
   char *w = static_cast<char *>(ws);
-  st = prologue(desc, w, L, stream);
+  st = prologue(desc, specs, n_specs, w, L, stream);
   if (st != KS_OK) return st;
   ks::ValidateParams v;
   std::memset(&v, 0, sizeof v);

@@ -32,6 +32,17 @@ enum HeadKind : int {
   kNumKinds
 };
 
+// Per-spec constants of the inner loop, computed once per call into the
+// workspace (64 bytes each) so the evaluation kernel reads them with scalar
+// loads instead of redoing float64 divisions in every wave.
+struct alignas(16) SpecC {
+  float rcp_p, rcp_bw, bw_over_p, l2, t0, rcp_t0, n_f, rcp_n;
+  double rcp_nd;
+  uint32_t n, pad0;
+  uint32_t pad[4];
+};
+static_assert(sizeof(SpecC) == 64, "SpecC is one 64-byte record");
+
 struct EvalParams {
   // records
   const uint32_t *step, *m, *n, *k, *a, *b;
@@ -41,7 +52,7 @@ struct EvalParams {
   int64_t n_steps;
   uint32_t elem_bytes;
   int32_t n_specs;
-  const ks_spec *specs;
+  const SpecC *spec_c;             // [n_specs], in the workspace
   int64_t fam_off[KS_NFAM + 1];
   int32_t tile_off[KS_NFAM + 1];   // wave-tile offsets per family
   int32_t wgt_off[KS_NFAM + 1];    // workgroup-tile offsets per family
@@ -91,6 +102,7 @@ struct ValidateParams {
 };
 
 hipError_t launch_clear(uint32_t *err, hipStream_t s);
+hipError_t launch_spec_prep(const ks_spec *specs, int32_t n_specs, SpecC *out, hipStream_t s);
 hipError_t launch_attn_agg(const uint32_t *req_off, const uint32_t *q, const uint32_t *h,
                            int64_t n_steps, int64_t n_req, uint64_t *agg, uint32_t *err,
                            hipStream_t s);

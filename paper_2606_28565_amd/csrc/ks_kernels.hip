@@ -75,29 +75,40 @@ __global__ void k_clear(uint32_t *err) {
 }
 
 // Per step j: over its requests r, Q = sum q, KV = sum (h + q),
-// PAIRS = sum (q h + q (q + 1) / 2), TILES = sum ceil(q / 128).
+// PAIRS = sum (q h + q (q + 1) / 2), TILES = sum ceil(q / 128).  One wave
+// per step: lanes stride over the requests, then a butterfly reduction.
 __global__ void k_attn_agg(const uint32_t *__restrict__ req_off, const uint32_t *__restrict__ rq,
                            const uint32_t *__restrict__ rh, int64_t n_steps, int64_t n_req,
                            uint64_t *__restrict__ agg, uint32_t *err) {
-  for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n_steps;
-       j += (int64_t)gridDim.x * blockDim.x) {
+  const int lane = threadIdx.x & 63;
+  const int64_t waves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t j = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6; j < n_steps; j += waves) {
     uint32_t r0 = req_off[j], r1 = req_off[j + 1];
     if (r0 > r1 || (int64_t)r1 > n_req) {
-      atomicOr(err, kErrReq);
+      if (lane == 0) atomicOr(err, kErrReq);
       r0 = r1 = 0;
     }
     uint64_t Q = 0, KV = 0, P = 0, T = 0;
-    for (uint32_t r = r0; r < r1; ++r) {
+    for (uint32_t r = r0 + lane; r < r1; r += 64) {
       const uint64_t q = rq[r], h = rh[r];
       Q += q;
       KV += h + q;
       P += q * h + ((q * (q + 1)) >> 1);
       T += (q + 127) >> 7;
     }
-    agg[j] = Q;
-    agg[n_steps + j] = KV;
-    agg[2 * n_steps + j] = P;
-    agg[3 * n_steps + j] = T;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      Q += __shfl_xor(Q, off);
+      KV += __shfl_xor(KV, off);
+      P += __shfl_xor(P, off);
+      T += __shfl_xor(T, off);
+    }
+    if (lane == 0) {
+      agg[j] = Q;
+      agg[n_steps + j] = KV;
+      agg[2 * n_steps + j] = P;
+      agg[3 * n_steps + j] = T;
+    }
   }
 }
 
@@ -182,28 +193,24 @@ __device__ __forceinline__ Cnt record_counts(int fam, uint32_t m32, uint32_t n32
 }
 
 // ------------------------------------------------------------ spec constants
-struct SpecC {
-  float rcp_p, rcp_bw, bw_over_p, l2, t0, rcp_t0, n_f, rcp_n;
-  double rcp_nd;
-  uint32_t n;
-};
-
-__device__ __forceinline__ SpecC load_spec(const ks_spec *__restrict__ sp) {
-  SpecC c;
-  const double P = sp->peak_flops, BW = sp->hbm_bw;
-  uint32_t n = sp->n_cu;
-  n = n < 1 ? 1 : n;
+__global__ void k_spec_prep(const ks_spec *__restrict__ specs, int32_t n_specs, SpecC *__restrict__ out) {
+  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= n_specs) return;
+  const ks_spec sp = specs[s];
+  SpecC c = {};
+  const double P = sp.peak_flops, BW = sp.hbm_bw;
+  const uint32_t n = sp.n_cu < 1 ? 1u : sp.n_cu;
   c.n = n;
   c.rcp_p = (float)(1.0 / P);
   c.rcp_bw = (float)(1.0 / BW);
   c.bw_over_p = (float)(BW / P);
-  c.l2 = (float)sp->l2_bytes;
-  c.t0 = (float)sp->t0;
-  c.rcp_t0 = (float)(1.0 / fmax(sp->t0, 1e-9));
+  c.l2 = (float)sp.l2_bytes;
+  c.t0 = (float)sp.t0;
+  c.rcp_t0 = (float)(1.0 / fmax(sp.t0, 1e-9));
   c.n_f = (float)n;
-  c.rcp_n = 1.0f / (float)n;
+  c.rcp_n = (float)(1.0 / (double)n);
   c.rcp_nd = 1.0 / (double)n;
-  return c;
+  out[s] = c;
 }
 
 // spec-independent per-record quantities
@@ -392,7 +399,9 @@ struct HeadBF16 {
     float z0 = 0.0f, z1 = 0.0f;
 #pragma unroll 1
     for (int mb = 0; mb < MB; ++mb) {
-      f32x16 c0 = {}, c1 = {};
+      // the bias enters as the accumulator input of the first product
+      const f32x16 bias = *(const f32x16 *)(lds + OFF_B2 + (mb * 2 + g) * 16);
+      f32x16 c0 = bias, c1 = bias;
 #pragma unroll
       for (int kc = 0; kc < KC2; ++kc) {
         const u32x4 a = *(const u32x4 *)(lds + OFF_W2 + ((mb * KC2 + kc) * 64 + lane) * 4);
@@ -401,14 +410,12 @@ struct HeadBF16 {
         c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
                                                       __builtin_bit_cast(bf16x8, H1[1][kc >> 1][kc & 1]), c1, 0, 0, 0);
       }
-      const float *b2 = (const float *)(lds + OFF_B2 + (mb * 2 + g) * 16);
       const uint32_t *w3 = lds + OFF_W3 + (mb * 2 + g) * 8;
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
-        const float bl = b2[2 * q], bh = b2[2 * q + 1];
         const uint32_t w = w3[q];
-        z0 = dot2_bf16(relu_bf16x2(pack_bf16(c0[2 * q] + bl, c0[2 * q + 1] + bh)), w, z0);
-        z1 = dot2_bf16(relu_bf16x2(pack_bf16(c1[2 * q] + bl, c1[2 * q + 1] + bh)), w, z1);
+        z0 = dot2_bf16(relu_bf16x2(pack_bf16(c0[2 * q], c0[2 * q + 1])), w, z0);
+        z1 = dot2_bf16(relu_bf16x2(pack_bf16(c1[2 * q], c1[2 * q + 1])), w, z1);
       }
     }
     // lanes l and l ^ 32 hold the two halves of the same record's dot
@@ -501,7 +508,8 @@ struct HeadF32 {
     float z0 = 0.0f, z1 = 0.0f;
 #pragma unroll 1
     for (int mb2 = 0; mb2 < MB; ++mb2) {
-      f32x16 c0 = {}, c1 = {};
+      const f32x16 bias = *(const f32x16 *)(f + OFF_B2 + (mb2 * 2 + g) * 16);
+      f32x16 c0 = bias, c1 = bias;
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
         const float *a = f + OFF_W2 + ((mb2 * MB + mb) * 64 + lane) * 16;
@@ -511,12 +519,11 @@ struct HeadF32 {
           c1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[r], H1[1][mb][r], c1, 0, 0, 0);
         }
       }
-      const float *b2 = f + OFF_B2 + (mb2 * 2 + g) * 16;
       const float *w3 = f + OFF_W3 + (mb2 * 2 + g) * 16;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        z0 = fmaf(w3[r], fmaxf(c0[r] + b2[r], 0.0f), z0);
-        z1 = fmaf(w3[r], fmaxf(c1[r] + b2[r], 0.0f), z1);
+        z0 = fmaf(w3[r], fmaxf(c0[r], 0.0f), z0);
+        z1 = fmaf(w3[r], fmaxf(c1[r], 0.0f), z1);
       }
     }
     uint32_t a0 = __builtin_bit_cast(uint32_t, z0), a1 = __builtin_bit_cast(uint32_t, z1);
@@ -600,9 +607,34 @@ __global__ __launch_bounds__(kWgThreads) void k_eval(EvalParams p) {
     const uint32_t prev = row0 > fam_lo ? p.step[row0 - 1] : kNoKey;
     const bool to_carry = is_tail && key == key0 && prev == key0;
     const int tile_id = p.tile_off[fam] + tile_in_fam;
+    // Segmented inclusive scan over the sorted step keys, as a tree: round r
+    // adds the partial of lane - 2^r when that lane holds the same key
+    // (factor 1) and nothing otherwise (factor 0).  Each lane's sum is built
+    // by at most 6 levels of pairwise adds of positive terms, so its fp32
+    // rounding error stays below 6 * 2^-24 relative; tiles and families are
+    // then summed in fp64.  A tail lane stores its segment's sum: into the
+    // tile's carry slot if the segment continues from the previous tile,
+    // else into the (spec, family, step) partial.
+    float fac[6];
+#pragma unroll
+    for (int r = 0; r < 6; ++r) {
+      const uint32_t kw = __shfl_up(key, 1 << r);
+      fac[r] = (lane >= (1 << r) && kw == key) ? 1.0f : 0.0f;
+    }
+    double *dst = nullptr;
+    size_t dst_stride = 0;
+    if (p.partial && is_tail) {
+      if (to_carry) {
+        dst = p.carry + tile_id;
+        dst_stride = (size_t)p.n_tiles;
+      } else {
+        dst = p.partial + (size_t)fam * p.n_steps + key;
+        dst_stride = (size_t)KS_NFAM * p.n_steps;
+      }
+    }
 
     for (int s = 0; s < p.n_specs; ++s) {
-      const SpecC sc = load_spec(p.specs + s);
+      const SpecC sc = p.spec_c[s];
       const Roof o = roofline(rc, sc);
       float eta = 1.0f;
       if constexpr (H::kMlp) {
@@ -619,20 +651,10 @@ __global__ __launch_bounds__(kWgThreads) void k_eval(EvalParams p) {
         if (p.o_t) p.o_t[i] = t;
       }
       if (p.partial) {
-        // segmented inclusive scan over the sorted step keys
-        double v = live ? (double)t : 0.0;
+        float v = live ? t : 0.0f;
 #pragma unroll
-        for (int off = 1; off < 64; off <<= 1) {
-          const double w = __shfl_up(v, off);
-          const uint32_t kw = __shfl_up(key, off);
-          if (lane >= off && kw == key) v += w;
-        }
-        if (is_tail) {
-          if (to_carry)
-            p.carry[(size_t)s * p.n_tiles + tile_id] = v;
-          else
-            p.partial[((size_t)s * KS_NFAM + fam) * p.n_steps + key] = v;
-        }
+        for (int r = 0; r < 6; ++r) v = fmaf(__shfl_up(v, 1 << r), fac[r], v);
+        if (dst) dst[(size_t)s * dst_stride] = (double)v;
       }
     }
   }
@@ -758,8 +780,14 @@ hipError_t launch_clear(uint32_t *err, hipStream_t s) {
 hipError_t launch_attn_agg(const uint32_t *req_off, const uint32_t *q, const uint32_t *h, int64_t n_steps,
                            int64_t n_req, uint64_t *agg, uint32_t *err, hipStream_t s) {
   if (n_steps == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_attn_agg, dim3(grid_for(n_steps, 256, 4096)), dim3(256), 0, s, req_off, q, h, n_steps,
+  // one wave per step, four waves per workgroup
+  hipLaunchKernelGGL(k_attn_agg, dim3(grid_for(n_steps, 4, 8192)), dim3(256), 0, s, req_off, q, h, n_steps,
                      n_req, agg, err);
+  return hipGetLastError();
+}
+
+hipError_t launch_spec_prep(const ks_spec *specs, int32_t n_specs, SpecC *out, hipStream_t s) {
+  hipLaunchKernelGGL(k_spec_prep, dim3(grid_for(n_specs, 256, 4096)), dim3(256), 0, s, specs, n_specs, out);
   return hipGetLastError();
 }
 
