@@ -352,11 +352,10 @@ struct HeadBF16 {
     if (threadIdx.x == 0) lds[OFF_B3] = __builtin_bit_cast(uint32_t, bf16_to_f32(b3[0]));
   }
 
-  // z of the lane's own record; x: that record's features (fp32)
-  __device__ static __forceinline__ float mlp(const float (&x)[IN], const uint32_t *lds) {
+  // The 256-unit heads: layer 2 one 32-unit block at a time in a loop, which
+  // keeps only that block's weight fragments and accumulators live.
+  __device__ static __forceinline__ float mlp_loop(const float (&x)[IN], const uint32_t *lds) {
     const int lane = threadIdx.x & 63, g = lane >> 5;
-    // features -> bf16 pairs; the swap turns "own record" into the B layout
-    // of the two 32-record column blocks
     uint32_t P[IN / 2];
 #pragma unroll
     for (int c = 0; c < IN / 2; ++c) P[c] = pack_bf16(x[2 * c], x[2 * c + 1]);
@@ -371,60 +370,206 @@ struct HeadBF16 {
         XB[1][kc][q] = hi;
       }
     }
-    // layer 1: h1 = relu(W1 x), rounded to bf16
-    u32x4 H1[2][MB][2];
+    u32x4 H0[MB][2], H1[MB][2];
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
       f32x16 c0 = {}, c1 = {};
 #pragma unroll
       for (int kc = 0; kc < KC1; ++kc) {
         const u32x4 a = *(const u32x4 *)(lds + ((mb * KC1 + kc) * 64 + lane) * 4);
-        c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
-                                                      __builtin_bit_cast(bf16x8, XB[0][kc]), c0, 0, 0, 0);
-        c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
-                                                      __builtin_bit_cast(bf16x8, XB[1][kc]), c1, 0, 0, 0);
+        c0 = mfma(a, XB[0][kc], c0);
+        c1 = mfma(a, XB[1][kc], c1);
       }
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int r = 8 * h + 2 * q;
-          H1[0][mb][h][q] = relu_bf16x2(pack_bf16(c0[r], c0[r + 1]));
-          H1[1][mb][h][q] = relu_bf16x2(pack_bf16(c1[r], c1[r + 1]));
-        }
-      }
+      pack_h1(c0, c1, H0[mb], H1[mb]);
     }
-    // layers 2 and 3: z = w3 . bf16(relu(W2 h1 + b2)) + b3; one 32-unit
-    // block of layer 2 at a time keeps only its weight fragments live
     float z0 = 0.0f, z1 = 0.0f;
 #pragma unroll 1
     for (int mb = 0; mb < MB; ++mb) {
-      // the bias enters as the accumulator input of the first product
-      const f32x16 bias = *(const f32x16 *)(lds + OFF_B2 + (mb * 2 + g) * 16);
-      f32x16 c0 = bias, c1 = bias;
+      f32x16 c0 = *(const f32x16 *)(lds + OFF_B2 + (mb * 2 + g) * 16), c1 = c0;
 #pragma unroll
       for (int kc = 0; kc < KC2; ++kc) {
         const u32x4 a = *(const u32x4 *)(lds + OFF_W2 + ((mb * KC2 + kc) * 64 + lane) * 4);
-        c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
-                                                      __builtin_bit_cast(bf16x8, H1[0][kc >> 1][kc & 1]), c0, 0, 0, 0);
-        c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
-                                                      __builtin_bit_cast(bf16x8, H1[1][kc >> 1][kc & 1]), c1, 0, 0, 0);
+        c0 = mfma(a, H0[kc >> 1][kc & 1], c0);
+        c1 = mfma(a, H1[kc >> 1][kc & 1], c1);
       }
-      const uint32_t *w3 = lds + OFF_W3 + (mb * 2 + g) * 8;
+      epilogue(c0, c1, lds + OFF_W3 + (mb * 2 + g) * 8, z0, z1);
+    }
+    uint32_t u0 = __builtin_bit_cast(uint32_t, z0), u1 = __builtin_bit_cast(uint32_t, z1);
+    swap32(u0, u1);
+    return __builtin_bit_cast(float, u0) + __builtin_bit_cast(float, u1) +
+           __builtin_bit_cast(float, lds[OFF_B3]);
+  }
+
+  // relu + bf16 rounding of a 32-unit block of layer 1 (both column blocks)
+  __device__ static __forceinline__ void pack_h1(const f32x16 &c0, const f32x16 &c1, u32x4 (&h0)[2],
+                                                 u32x4 (&h1)[2]) {
 #pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const uint32_t w = w3[q];
-        z0 = dot2_bf16(relu_bf16x2(pack_bf16(c0[2 * q], c0[2 * q + 1])), w, z0);
-        z1 = dot2_bf16(relu_bf16x2(pack_bf16(c1[2 * q], c1[2 * q + 1])), w, z1);
+    for (int h = 0; h < 2; ++h) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int r = 8 * h + 2 * q;
+        h0[h][q] = relu_bf16x2(pack_bf16(c0[r], c0[r + 1]));
+        h1[h][q] = relu_bf16x2(pack_bf16(c1[r], c1[r + 1]));
       }
     }
-    // lanes l and l ^ 32 hold the two halves of the same record's dot
-    // product; after the swap lane l < 32 adds block 0's halves of record l
-    // and lane l >= 32 block 1's halves of record l.
-    uint32_t a0 = __builtin_bit_cast(uint32_t, z0), a1 = __builtin_bit_cast(uint32_t, z1);
-    swap32(a0, a1);
-    return __builtin_bit_cast(float, a0) + __builtin_bit_cast(float, a1) +
-           __builtin_bit_cast(float, lds[OFF_B3]);
+  }
+
+  // layer 3 over one 32-unit block of layer 2: z += w3 . bf16(relu(h2))
+  template <typename W3>
+  __device__ static __forceinline__ void epilogue(const f32x16 &c0, const f32x16 &c1, const W3 &w3,
+                                                  float &z0, float &z1) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const uint32_t w = w3[q];
+      z0 = dot2_bf16(relu_bf16x2(pack_bf16(c0[2 * q], c0[2 * q + 1])), w, z0);
+      z1 = dot2_bf16(relu_bf16x2(pack_bf16(c1[2 * q], c1[2 * q + 1])), w, z1);
+    }
+  }
+
+  __device__ static __forceinline__ f32x16 mfma(const u32x4 &a, const u32x4 &b, const f32x16 &c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
+                                                   c, 0, 0, 0);
+  }
+
+  __device__ static __forceinline__ void fence() { __builtin_amdgcn_sched_barrier(0); }
+
+  __device__ static __forceinline__ u32x4 frag_w1(const uint32_t *lds, int mb, int kc, int lane) {
+    return *(const u32x4 *)(lds + ((mb * KC1 + kc) * 64 + lane) * 4);
+  }
+  __device__ static __forceinline__ u32x4 frag_w2(const uint32_t *lds, int mb, int kc, int lane) {
+    return *(const u32x4 *)(lds + OFF_W2 + ((mb * KC2 + kc) * 64 + lane) * 4);
+  }
+
+  // relu + bf16 rounding of register pairs [2 q0, 2 q1) of one layer-1 block
+  __device__ static __forceinline__ void pack_part(const f32x16 &c0, const f32x16 &c1, u32x4 (&h0)[2],
+                                                   u32x4 (&h1)[2], int q0, int q1) {
+#pragma unroll
+    for (int q = q0; q < q1; ++q) {
+      h0[q >> 2][q & 3] = relu_bf16x2(pack_bf16(c0[2 * q], c0[2 * q + 1]));
+      h1[q >> 2][q & 3] = relu_bf16x2(pack_bf16(c1[2 * q], c1[2 * q + 1]));
+    }
+  }
+
+  // z of the lane's own record; x: that record's features (fp32).
+  //
+  // A SIMD's VALU and matrix core only overlap when VALU work is issued in
+  // the shadow of in-flight MFMAs of the same wave, and the compiler does not
+  // interleave on its own.  So the body is scheduled by hand: straight-line
+  // groups fenced by sched_barrier, each holding the LDS prefetch of a later
+  // weight fragment, one MFMA pair, and a few VALU ops of another stage:
+  //   layer 1, block mb      | relu/bf16 packing of layer-1 block mb-1
+  //   layer 2, block 0       | packing of the last layer-1 block
+  //   layer 2, block mb >= 1 | epilogue of layer-2 block mb-1 (relu, bf16,
+  //                            dot with w3)
+  // Only the features, the last epilogue and the tail stay exposed.
+  __device__ static __forceinline__ float mlp(const float (&x)[IN], const uint32_t *lds) {
+    static_assert(MB >= 2 && 8 % KC2 == 0 || MB > 4, "the pipelined head splits 8 register pairs over the chunks");
+    if constexpr (MB > 4) {
+      return mlp_loop(x, lds);
+    } else {
+      const int lane = threadIdx.x & 63, g = lane >> 5;
+      // features -> bf16 pairs; the swap turns "own record" into the B
+      // layout of the two 32-record column blocks
+      uint32_t P[IN / 2];
+#pragma unroll
+      for (int c = 0; c < IN / 2; ++c) P[c] = pack_bf16(x[2 * c], x[2 * c + 1]);
+      u32x4 XB[2][KC1];
+#pragma unroll
+      for (int kc = 0; kc < KC1; ++kc) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          uint32_t lo = P[8 * kc + q], hi = P[8 * kc + 4 + q];
+          swap32(lo, hi);
+          XB[0][kc][q] = lo;
+          XB[1][kc][q] = hi;
+        }
+      }
+      // ---- layer 1 | packing of the previous layer-1 block
+      u32x4 H0[MB][2], H1[MB][2];
+      f32x16 a1[2][2];
+      u32x4 w1f[KC1];
+#pragma unroll
+      for (int kc = 0; kc < KC1; ++kc) w1f[kc] = frag_w1(lds, 0, kc, lane);
+      fence();
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        u32x4 cur[KC1];
+#pragma unroll
+        for (int kc = 0; kc < KC1; ++kc) {
+          cur[kc] = w1f[kc];
+          if (mb + 1 < MB) w1f[kc] = frag_w1(lds, mb + 1, kc, lane);
+        }
+        a1[mb & 1][0] = f32x16{};
+        a1[mb & 1][1] = f32x16{};
+#pragma unroll
+        for (int kc = 0; kc < KC1; ++kc) {
+          a1[mb & 1][0] = mfma(cur[kc], XB[0][kc], a1[mb & 1][0]);
+          a1[mb & 1][1] = mfma(cur[kc], XB[1][kc], a1[mb & 1][1]);
+        }
+        if (mb > 0) pack_part(a1[(mb - 1) & 1][0], a1[(mb - 1) & 1][1], H0[mb - 1], H1[mb - 1], 0, 8);
+        fence();
+      }
+      // ---- layer 2: weight fragments prefetched two chunks ahead
+      constexpr int NCH = MB * KC2;   // (block, chunk) pairs in order
+      u32x4 wf[3];
+      wf[0] = frag_w2(lds, 0, 0, lane);
+      wf[1] = frag_w2(lds, 0, 1, lane);
+      f32x16 bias = *(const f32x16 *)(lds + OFF_B2 + g * 16);
+      f32x16 c0 = {}, c1 = {}, p0 = {}, p1 = {};
+      uint32_t w3r[8];
+      float z0 = 0.0f, z1 = 0.0f;
+      fence();
+#pragma unroll
+      for (int i = 0; i < NCH; ++i) {
+        const int mb = i / KC2, kc = i % KC2;
+        if (i + 2 < NCH) wf[(i + 2) % 3] = frag_w2(lds, (i + 2) / KC2, (i + 2) % KC2, lane);
+        if (kc == 0 && mb > 0) {
+          // block mb-1's accumulators become the epilogue's inputs
+          p0 = c0;
+          p1 = c1;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) w3r[q] = lds[OFF_W3 + ((mb - 1) * 2 + g) * 8 + q];
+        }
+        const u32x4 a = wf[i % 3];
+        if (kc == 0) {
+          c1 = mfma(a, H1[0][0], bias);
+          c0 = mfma(a, H0[0][0], bias);
+        } else {
+          c0 = mfma(a, H0[kc >> 1][kc & 1], c0);
+          c1 = mfma(a, H1[kc >> 1][kc & 1], c1);
+        }
+        if (kc == KC2 / 2 && mb + 1 < MB) bias = *(const f32x16 *)(lds + OFF_B2 + ((mb + 1) * 2 + g) * 16);
+        if (mb == 0) {
+          // pack the last layer-1 block over the first PG groups, all of
+          // which come before chunk 2 (MB - 1), its first consumer
+          constexpr int PG = 2 * (MB - 1) < 4 ? 2 * (MB - 1) : 4;
+          if (kc < PG) pack_part(a1[(MB - 1) & 1][0], a1[(MB - 1) & 1][1], H0[MB - 1], H1[MB - 1],
+                                 kc * 8 / PG, (kc + 1) * 8 / PG);
+        } else {
+          // chunk kc's share of block mb-1's epilogue: register pairs
+          // [8 kc / KC2, 8 (kc + 1) / KC2) of the 8
+#pragma unroll
+          for (int q = kc * 8 / KC2; q < (kc + 1) * 8 / KC2; ++q) {
+            z0 = dot2_bf16(relu_bf16x2(pack_bf16(p0[2 * q], p0[2 * q + 1])), w3r[q], z0);
+            z1 = dot2_bf16(relu_bf16x2(pack_bf16(p1[2 * q], p1[2 * q + 1])), w3r[q], z1);
+          }
+          // an empty use pins this part here; otherwise the dot chain, whose
+          // result is only needed at the end, is sunk below every MFMA
+          asm volatile("" ::"v"(z0), "v"(z1));
+        }
+        fence();
+      }
+#pragma unroll
+      for (int q = 0; q < 8; ++q) w3r[q] = lds[OFF_W3 + ((MB - 1) * 2 + g) * 8 + q];
+      epilogue(c0, c1, w3r, z0, z1);
+      // lanes l and l ^ 32 hold the two halves of the same record's dot
+      // product; after the swap lane l < 32 adds block 0's halves of record
+      // l and lane l >= 32 block 1's halves of record l.
+      uint32_t u0 = __builtin_bit_cast(uint32_t, z0), u1 = __builtin_bit_cast(uint32_t, z1);
+      swap32(u0, u1);
+      return __builtin_bit_cast(float, u0) + __builtin_bit_cast(float, u1) +
+             __builtin_bit_cast(float, lds[OFF_B3]);
+    }
   }
 };
 
@@ -540,6 +685,8 @@ struct HeadOne {
   __device__ static float mlp(const float (&)[IN], const uint32_t *) { return 0.0f; }
 };
 
+// kMinWg: workgroups per CU the register allocator must fit (2 = two waves
+// per SIMD, at most 256 registers per lane).
 template <int KIND> struct KindOf;
 template <> struct KindOf<kEtaOne> { using H = HeadOne; static constexpr int IN = 16; };
 template <> struct KindOf<kF32_16_64> { using H = HeadF32<16, 64>; static constexpr int IN = 16; };
@@ -553,13 +700,61 @@ template <> struct KindOf<kBF16_32_64> { using H = HeadBF16<32, 64>; static cons
 template <> struct KindOf<kBF16_32_128> { using H = HeadBF16<32, 128>; static constexpr int IN = 32; };
 template <> struct KindOf<kBF16_32_256> { using H = HeadBF16<32, 256>; static constexpr int IN = 32; };
 
+// ------------------------------------------------------------ segmented scan
+// Inclusive scan of a wave's 64 values, segmented by sorted keys, with DPP
+// lane moves (no LDS round trips).  Within rows of 16 lanes: add lanes
+// l-1, l-2, l-3, then l-4 (lanes 4..15) and l-8 (lanes 8..15); across rows:
+// lane 15 of each row into rows 1 and 3, lane 31 into rows 2 and 3.  Each
+// step adds a contiguous partial that ends where the lane's current partial
+// begins; its factor is 1 when that source lane holds the same key (then, the
+// keys being sorted, every lane between does too) and 0 otherwise.  Sums are
+// built in at most 7 levels of adds of non-negative terms, so the fp32 result
+// errs by at most 7 * 2^-24 relative; tiles and families are then summed in
+// fp64.
+template <int CTRL, int ROW, int BANK>
+__device__ __forceinline__ float dpp(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, ROW, BANK, true));
+}
+
+__device__ __forceinline__ void seg_factors(uint32_t key, int lane, float (&f)[7]) {
+  const int c = lane & 15, row = lane >> 4;
+  const uint32_t k1 = __shfl(key, lane - 1), k2 = __shfl(key, lane - 2), k3 = __shfl(key, lane - 3);
+  const uint32_t k4 = __shfl(key, lane - 4), k8 = __shfl(key, lane - 8);
+  const uint32_t k15 = __shfl(key, row * 16 - 1), k31 = __shfl(key, 31);
+  f[0] = (c >= 1 && k1 == key) ? 1.0f : 0.0f;
+  f[1] = (c >= 2 && k2 == key) ? 1.0f : 0.0f;
+  f[2] = (c >= 3 && k3 == key) ? 1.0f : 0.0f;
+  f[3] = (c >= 4 && k4 == key) ? 1.0f : 0.0f;
+  f[4] = (c >= 8 && k8 == key) ? 1.0f : 0.0f;
+  f[5] = ((row & 1) && k15 == key) ? 1.0f : 0.0f;
+  f[6] = (row >= 2 && k31 == key) ? 1.0f : 0.0f;
+}
+
+__device__ __forceinline__ float seg_scan(float v0, const float (&f)[7]) {
+  float v = v0;
+  v = fmaf(dpp<0x111, 0xf, 0xf>(v0), f[0], v);   // row_shr:1
+  v = fmaf(dpp<0x112, 0xf, 0xf>(v0), f[1], v);   // row_shr:2
+  v = fmaf(dpp<0x113, 0xf, 0xf>(v0), f[2], v);   // row_shr:3
+  v = fmaf(dpp<0x114, 0xf, 0xe>(v), f[3], v);    // row_shr:4, lanes 4..15 of each row
+  v = fmaf(dpp<0x118, 0xf, 0xc>(v), f[4], v);    // row_shr:8, lanes 8..15 of each row
+  v = fmaf(dpp<0x142, 0xa, 0xf>(v), f[5], v);    // row_bcast:15 into rows 1, 3
+  v = fmaf(dpp<0x143, 0xc, 0xf>(v), f[6], v);    // row_bcast:31 into rows 2, 3
+  return v;
+}
+
 // ------------------------------------------------------------ evaluation
 // Workgroup = 4 waves; a workgroup tile is 4 consecutive 64-record wave
 // tiles of one family, so the family's head is staged in LDS once and
 // shared.  Workgroups stride over workgroup tiles and restage only when the
 // family changes (records are family-major).
+template <int KIND> struct MinWg { static constexpr int value = 1; };
+template <> struct MinWg<kBF16_16_64> { static constexpr int value = 2; };
+template <> struct MinWg<kBF16_16_128> { static constexpr int value = 2; };
+template <> struct MinWg<kBF16_32_64> { static constexpr int value = 2; };
+template <> struct MinWg<kBF16_32_128> { static constexpr int value = 2; };
+
 template <int KIND>
-__global__ __launch_bounds__(kWgThreads) void k_eval(EvalParams p) {
+__global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalParams p) {
   using H = typename KindOf<KIND>::H;
   constexpr int IN = KindOf<KIND>::IN;
   __shared__ uint32_t lds[H::LDS_DW];
@@ -607,20 +802,11 @@ __global__ __launch_bounds__(kWgThreads) void k_eval(EvalParams p) {
     const uint32_t prev = row0 > fam_lo ? p.step[row0 - 1] : kNoKey;
     const bool to_carry = is_tail && key == key0 && prev == key0;
     const int tile_id = p.tile_off[fam] + tile_in_fam;
-    // Segmented inclusive scan over the sorted step keys, as a tree: round r
-    // adds the partial of lane - 2^r when that lane holds the same key
-    // (factor 1) and nothing otherwise (factor 0).  Each lane's sum is built
-    // by at most 6 levels of pairwise adds of positive terms, so its fp32
-    // rounding error stays below 6 * 2^-24 relative; tiles and families are
-    // then summed in fp64.  A tail lane stores its segment's sum: into the
-    // tile's carry slot if the segment continues from the previous tile,
-    // else into the (spec, family, step) partial.
-    float fac[6];
-#pragma unroll
-    for (int r = 0; r < 6; ++r) {
-      const uint32_t kw = __shfl_up(key, 1 << r);
-      fac[r] = (lane >= (1 << r) && kw == key) ? 1.0f : 0.0f;
-    }
+    // A tail lane stores its segment's sum (seg_scan): into the tile's carry
+    // slot if the segment continues from the previous tile, else into the
+    // (spec, family, step) partial.
+    float fac[7];
+    seg_factors(key, lane, fac);
     double *dst = nullptr;
     size_t dst_stride = 0;
     if (p.partial && is_tail) {
@@ -633,8 +819,10 @@ __global__ __launch_bounds__(kWgThreads) void k_eval(EvalParams p) {
       }
     }
 
+    SpecC sc_next = p.spec_c[0];
     for (int s = 0; s < p.n_specs; ++s) {
-      const SpecC sc = p.spec_c[s];
+      const SpecC sc = sc_next;
+      sc_next = p.spec_c[s + 1 < p.n_specs ? s + 1 : s];   // in flight during this spec
       const Roof o = roofline(rc, sc);
       float eta = 1.0f;
       if constexpr (H::kMlp) {
@@ -651,9 +839,7 @@ __global__ __launch_bounds__(kWgThreads) void k_eval(EvalParams p) {
         if (p.o_t) p.o_t[i] = t;
       }
       if (p.partial) {
-        float v = live ? t : 0.0f;
-#pragma unroll
-        for (int r = 0; r < 6; ++r) v = fmaf(__shfl_up(v, 1 << r), fac[r], v);
+        const float v = seg_scan(live ? t : 0.0f, fac);
         if (dst) dst[(size_t)s * dst_stride] = (double)v;
       }
     }
