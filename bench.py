@@ -32,16 +32,59 @@ METRIC = "kernel latency predictions/sec and step evals/sec at 1 GPU; % of HBM/M
 PEAK = {"bf16": 2.5e15, "f32": 157.3e12, "hbm": 8.0e12}
 
 
+C5_BATCH_STEPS = 88_640      # 88,640 steps x 722 kernels = 64.0 M records
+
+
 def _workload(name: str):
+    """(workload, description, oracle sample) for each benchmark workload.
+    The oracle sample bounds the CPU baseline to ~10-30 s of work."""
     from workload import gen
     if name == "c4":
-        return gen.config4(), "c4-capacity-grid: llama-7b c1 trace + S2 trace prefix, 256 specs"
+        return (gen.config4(), "c4-capacity-grid: llama-7b c1 trace + S2 trace prefix, 256 specs",
+                {"specs": 16, "steps": None})
     if name == "c1":
-        return gen.config1(), "c1-llama7b: 1000 steps, 2 datasheet specs, fp32 heads"
+        return gen.config1(), "c1-llama7b: 1000 steps, 2 datasheet specs, fp32 heads", {"specs": 2, "steps": None}
     if name == "c5-batch":
-        wl = gen.config5(0, 2000)
-        return wl, "c5-70b-prefix: first 2000 steps, 2 datasheet specs, bf16 32-256-256 heads"
+        wl = gen.config5(0, C5_BATCH_STEPS)
+        return (wl, f"c5-70b-prefix: one 64M-record batch (steps 0..{C5_BATCH_STEPS}), 2 datasheet specs, "
+                    "bf16 32-256-256 heads", {"specs": 2, "steps": 300})
     raise SystemExit(f"unknown workload {name}")
+
+
+def kernel_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("ks_kernels.hip", "ks_internal.h"):
+        with open(os.path.join(ROOT, "paper_2606_28565_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(key: str):
+    """HBM bytes per launch of the evaluation kernel from the committed
+    rocprofv3 FETCH_SIZE / WRITE_SIZE summary, scaled by the copy-kernel
+    calibration; None if absent or taken on a different kernel source."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        rec = json.load(fh).get(key)
+    if not rec or rec.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    return rec["hbm_bytes_per_launch"]
+
+
+def copy_calibration(nbytes: int, reps: int) -> None:
+    """A plain device-to-device copy of nbytes, reps times: the reference
+    whose FETCH_SIZE / WRITE_SIZE counters scale the evaluation kernel's."""
+    import torch
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": nbytes, "reps": reps}), flush=True)
 
 
 def head_flops_per_pair(in_dim: int, hidden: int) -> int:
@@ -49,20 +92,29 @@ def head_flops_per_pair(in_dim: int, hidden: int) -> int:
     return 2 * (in_dim * hidden + hidden * hidden + hidden)
 
 
-def cpu_baseline(wl, n_spec_sample: int, threads: int):
-    """The oracle as it stands, on all records x the first n_spec_sample
-    spec vectors (a bounded sample of the same workload)."""
+def cpu_baseline(wl, sample: dict, eta_one: bool, threads: int):
+    """The oracle as it stands, on a bounded sample of the same workload:
+    the first sample["specs"] spec vectors and, if sample["steps"] is set,
+    only the records of the first sample["steps"] steps."""
     from threadpoolctl import threadpool_limits
     from oracle import ks_oracle as o
-    spec_ids = list(range(min(n_spec_sample, wl.n_specs)))
+    spec_ids = list(range(min(sample["specs"], wl.n_specs)))
+    rows = None
+    if sample["steps"] is not None:
+        import numpy as np
+        rows = np.nonzero(wl.desc.step < sample["steps"])[0]
     with threadpool_limits(limits=threads):
         t = time.perf_counter()
-        k = o.eval_kernels(wl.desc, wl.specs, wl.heads, spec_ids=spec_ids)
-        o.eval_steps(wl.desc, wl.steps, wl.specs, wl.host, wl.heads, spec_ids=spec_ids, kern=k)
+        k = o.eval_kernels(wl.desc, wl.specs, None if eta_one else wl.heads, eta_one=eta_one,
+                           spec_ids=spec_ids, rows=rows)
+        if rows is None:
+            o.eval_steps(wl.desc, wl.steps, wl.specs, wl.host, spec_ids=spec_ids, kern=k)
         dt = time.perf_counter() - t
-    pairs = wl.desc.n_rows * len(spec_ids)
+    n = wl.desc.n_rows if rows is None else len(rows)
+    pairs = n * len(spec_ids)
+    what = f"all {n} records" if rows is None else f"the {n} records of steps 0..{sample['steps']}"
     return {"value": pairs / dt, "unit": "predictions/s", "cores": threads, "kind": "oracle",
-            "sample": f"all {wl.desc.n_rows} records x {len(spec_ids)} of {wl.n_specs} spec vectors "
+            "sample": f"{what} x {len(spec_ids)} of {wl.n_specs} spec vectors "
                       f"({pairs} predictions, {dt:.1f} s, fp64 numpy, {threads} BLAS threads)"}
 
 
@@ -75,8 +127,9 @@ def main() -> int:
     ap.add_argument("--eta-one", action="store_true", help="eta = 1 (pure roofline) mode")
     ap.add_argument("--per-pair", action="store_true", help="also write per-pair t_roof/eta/t_kernel")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-specs", type=int, default=16)
     ap.add_argument("--cpu-threads", type=int, default=0)
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device copy of BYTES (counter calibration)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -94,9 +147,12 @@ def main() -> int:
         b.build()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration, max(args.steps, 1))
+        return 0
 
     print(f"[bench] generating workload {args.workload}", file=sys.stderr, flush=True)
-    wl, wdesc = _workload(args.workload)
+    wl, wdesc, sample = _workload(args.workload)
     di = abi.DeviceInputs(wl)
     heads = di.make_heads(wl.heads.precision, wl.heads.in_dim, wl.heads.hidden,
                           abi.KS_ETA_ONE if args.eta_one else abi.KS_ETA_MLP)
@@ -133,8 +189,8 @@ def main() -> int:
     value = pairs / (ms * 1e-3)
     step_evals = wl.desc.n_steps * di.n_specs / (ms * 1e-3)
     if args.eta_one:
-        # record stream: 6 u32 fields in, and for every pair nothing but the
-        # step partial; traffic is the records (24 B) read once
+        # record stream: 6 u32 fields (24 B) read once per record; per pair
+        # only the per-step partial sums are written
         alg = wl.desc.n_rows * 24.0
         bound, unit, peak = "hbm", "GB/s", PEAK["hbm"] / 1e9
         achieved = alg / (ms * 1e-3) / 1e9
@@ -160,15 +216,15 @@ def main() -> int:
                    "per_pair_outputs": bool(args.per_pair)},
         "step_evals_per_s": step_evals,
         "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
-                     "frac": achieved / peak, "traffic": None,
+                     "frac": achieved / peak,
+                     "traffic": recorded_traffic(f"{args.workload}{'-eta1' if args.eta_one else ''}"),
                      "note": "achieved = algorithmic work of the evaluation kernel per call / "
                              "HIP-event time of the whole call (all five kernels)"},
     }
     if not args.no_cpu_baseline:
         threads = args.cpu_threads or min(16, os.cpu_count() or 1)
-        print(f"[bench] cpu baseline: oracle, {args.cpu_specs} specs, {threads} threads",
-              file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_specs, threads)
+        print(f"[bench] cpu baseline: oracle on {sample}, {threads} threads", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(wl, sample, args.eta_one, threads)
         try:
             model = subprocess.run(["lscpu"], capture_output=True, text=True).stdout
             model = [l.split(":", 1)[1].strip() for l in model.splitlines() if l.startswith("Model name")]

@@ -217,7 +217,12 @@ def roofline(F, Bt, B, spec):
 # features": arithmetic intensity and its position relative to the ridge,
 # per-SM work and occupancy, wave count, L2 residency)
 # --------------------------------------------------------------------------
+K_UNUSED = (RMSNORM, SILU_MUL, EMBED)    # families whose records carry no K
+
+
 def features(cnt, n, k, rf, spec, in_dim=16):
+    """k: the records' K field, already zeroed for the families that carry
+    no K (see effective_k)."""
     F = cnt["F"].astype(np.float64)
     Bt = cnt["Bt"].astype(np.float64)
     B = cnt["B"].astype(np.float64)
@@ -287,6 +292,13 @@ def kernel_latency(t_roof, eta, t0):
 # --------------------------------------------------------------------------
 # per-kernel evaluation for every spec vector
 # --------------------------------------------------------------------------
+def effective_k(desc, rows):
+    """K as the features use it: the record's k, or 0 for families without K."""
+    k = desc.k[rows].astype(np.int64)
+    fam = desc.family()[rows]
+    return np.where(np.isin(fam, K_UNUSED), 0, k)
+
+
 def spec_at(specs, s):
     return {key: (int(v[s]) if key == "n_cu" else float(v[s])) for key, v in specs.items()}
 
@@ -320,7 +332,7 @@ def eval_kernels(desc, specs, heads=None, eta_one=False, emulate_bf16=None,
             z = np.full(len(rows), np.inf)
             eta = np.ones(len(rows))
         else:
-            x = features(sub, desc.n[rows], desc.k[rows], rf, sp, heads.in_dim)
+            x = features(sub, desc.n[rows], effective_k(desc, rows), rf, sp, heads.in_dim)
             if keep_features:
                 out["x"][si] = x
             z = np.zeros(len(rows))

@@ -187,8 +187,9 @@ void fill_eval(ks::EvalParams &p, const ks_desc *d, const ks_spec *specs, int32_
 }
 
 ks_status prologue(const ks_desc *d, const ks_spec *specs, int32_t n_specs, char *ws, const Layout &L,
-                   hipStream_t s) {
-  hipError_t e = ks::launch_clear(reinterpret_cast<uint32_t *>(ws), s);
+                   bool with_range, hipStream_t s) {
+  hipError_t e = ks::launch_clear(reinterpret_cast<uint32_t *>(ws), reinterpret_cast<uint32_t *>(ws + L.range),
+                                  with_range ? 2 * (int64_t)KS_NFAM * d->n_steps : 0, s);
   if (e != hipSuccess) return hip_fail(e, "clear launch");
   e = ks::launch_spec_prep(specs, n_specs, reinterpret_cast<ks::SpecC *>(ws + L.specc), s);
   if (e != hipSuccess) return hip_fail(e, "spec constants launch");
@@ -233,7 +234,7 @@ ks_status ks_eval_kernels(const ks_desc *desc, const ks_spec *specs, int32_t n_s
   if (st != KS_OK) return st;
   if (!out) return fail(KS_EINVAL, "out is NULL");
   char *w = static_cast<char *>(ws);
-  st = prologue(desc, specs, n_specs, w, L, stream);
+  st = prologue(desc, specs, n_specs, w, L, false, stream);
   if (st != KS_OK) return st;
   ks::EvalParams p;
   fill_eval(p, desc, specs, n_specs, heads, out, w, L);
@@ -261,12 +262,13 @@ ks_status ks_eval_steps(const ks_desc *desc, const ks_steps *steps, const ks_spe
   if (!out || (desc->n_steps > 0 && (!out->t_body || !out->t_gpu || !out->t_step)))
     return fail(KS_EINVAL, "a step output is NULL");
   char *w = static_cast<char *>(ws);
-  st = prologue(desc, specs, n_specs, w, L, stream);
+  st = prologue(desc, specs, n_specs, w, L, true, stream);
   if (st != KS_OK) return st;
   ks::EvalParams p;
   fill_eval(p, desc, specs, n_specs, heads, kout, w, L);
   p.partial = reinterpret_cast<double *>(w + L.partial);
   p.carry = reinterpret_cast<double *>(w + L.carry);
+  p.range = reinterpret_cast<uint32_t *>(w + L.range);
   hipError_t e = ks::launch_eval(kind, p, stream);
   if (e != hipSuccess) return hip_fail(e, "evaluation launch");
 
@@ -285,11 +287,10 @@ ks_status ks_eval_steps(const ks_desc *desc, const ks_steps *steps, const ks_spe
     f.fam_off[i] = p.fam_off[i];
     f.tile_off[i] = p.tile_off[i];
   }
-  f.step = desc->step;
   f.partial = p.partial;
   f.carry = p.carry;
   f.n_tiles = p.n_tiles;
-  f.range = reinterpret_cast<uint32_t *>(w + L.range);
+  f.range = p.range;
   f.host = *host;
   f.t_body = out->t_body;
   f.t_gpu = out->t_gpu;
@@ -308,7 +309,7 @@ ks_status ks_validate(const ks_desc *desc, const ks_steps *steps, const ks_spec 
     return fail(KS_EINVAL, "steps.n_steps %lld != desc.n_steps %lld", (long long)steps->n_steps,
                 (long long)desc->n_steps);
   char *w = static_cast<char *>(ws);
-  st = prologue(desc, specs, n_specs, w, L, stream);
+  st = prologue(desc, specs, n_specs, w, L, false, stream);
   if (st != KS_OK) return st;
   ks::ValidateParams v;
   std::memset(&v, 0, sizeof v);

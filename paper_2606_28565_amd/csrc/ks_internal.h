@@ -65,6 +65,7 @@ struct EvalParams {
   // per-step partial sums (nullable: no step sums)
   double *partial;   // [n_specs][KS_NFAM][n_steps]
   double *carry;     // [n_specs][n_tiles]
+  uint32_t *range;   // [KS_NFAM][n_steps][2] record range of each (family, step); nullable
   uint32_t *err;
 };
 
@@ -77,10 +78,9 @@ struct FinishParams {
   const ks_spec *specs;
   int64_t fam_off[KS_NFAM + 1];
   int32_t tile_off[KS_NFAM + 1];
-  const uint32_t *step;
   const double *partial, *carry;
   int32_t n_tiles;
-  uint32_t *range;                     // [KS_NFAM][n_steps][2]
+  const uint32_t *range;               // [KS_NFAM][n_steps][2]
   ks_host host;
   double *t_body, *t_gpu, *t_step;
 };
@@ -101,7 +101,7 @@ struct ValidateParams {
   uint32_t *err;
 };
 
-hipError_t launch_clear(uint32_t *err, hipStream_t s);
+hipError_t launch_clear(uint32_t *err, uint32_t *range, int64_t n_range, hipStream_t s);
 hipError_t launch_spec_prep(const ks_spec *specs, int32_t n_specs, SpecC *out, hipStream_t s);
 hipError_t launch_attn_agg(const uint32_t *req_off, const uint32_t *q, const uint32_t *h,
                            int64_t n_steps, int64_t n_req, uint64_t *agg, uint32_t *err,

@@ -2,14 +2,14 @@
 // (CDNA4: wave64, MFMA, 160 KB LDS per CU).
 //
 // Data flow of one evaluation (all on the caller's stream):
-//   k_clear      reset the workspace's bad-data flag
+//   k_clear      reset the workspace's bad-data flag and step-range table
 //   k_attn_agg   per step: Q, KV, PAIRS, TILES of its request list (Sec. 5.8)
 //   k_eval<K>    per wave: 64 records of one family x every spec vector:
 //                exact counts (Eq. 1-2 operands), waves and u (Sec. 2.2),
 //                t_roof (Eq. 2), features and the family's efficiency head
-//                on MFMA (Sec. 5.3), t = max(t_roof eta, t0) (Eq. 2), and a
-//                wavefront segmented sum of t by step
-//   k_seg_range  per (family, step): the record range of that step
+//                on MFMA (Sec. 5.3), t = max(t_roof eta, t0) (Eq. 2), a
+//                wavefront segmented sum of t by step, and each (family,
+//                step) record range
 //   k_finish     per (spec, step): body sum, all-reduce (Eq. 3), assembly (Eq. 4)
 #include <hip/hip_runtime.h>
 
@@ -70,26 +70,33 @@ __device__ __forceinline__ void swap32(uint32_t &lo, uint32_t &hi) {
 }
 
 // ------------------------------------------------------------ clear / agg
-__global__ void k_clear(uint32_t *err) {
-  if (threadIdx.x == 0) err[0] = 0;
+// Reset the flag word and, when step sums are wanted, the per-(family,
+// step) range table (an empty range marks a family without that step).
+__global__ void k_clear(uint32_t *err, uint32_t *range, int64_t n_range) {
+  const int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i0 == 0) err[0] = 0;
+  for (int64_t i = i0; i < n_range; i += (int64_t)gridDim.x * blockDim.x) range[i] = 0;
 }
 
 // Per step j: over its requests r, Q = sum q, KV = sum (h + q),
-// PAIRS = sum (q h + q (q + 1) / 2), TILES = sum ceil(q / 128).  One wave
-// per step: lanes stride over the requests, then a butterfly reduction.
+// PAIRS = sum (q h + q (q + 1) / 2), TILES = sum ceil(q / 128).  A group of
+// 16 lanes per step strides over its requests, then a butterfly reduction
+// within the group.
+constexpr int kAggLanes = 16;
+
 __global__ void k_attn_agg(const uint32_t *__restrict__ req_off, const uint32_t *__restrict__ rq,
                            const uint32_t *__restrict__ rh, int64_t n_steps, int64_t n_req,
                            uint64_t *__restrict__ agg, uint32_t *err) {
-  const int lane = threadIdx.x & 63;
-  const int64_t waves = ((int64_t)gridDim.x * blockDim.x) >> 6;
-  for (int64_t j = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6; j < n_steps; j += waves) {
+  const int sub = threadIdx.x & (kAggLanes - 1);
+  const int64_t groups = ((int64_t)gridDim.x * blockDim.x) / kAggLanes;
+  for (int64_t j = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kAggLanes; j < n_steps; j += groups) {
     uint32_t r0 = req_off[j], r1 = req_off[j + 1];
     if (r0 > r1 || (int64_t)r1 > n_req) {
-      if (lane == 0) atomicOr(err, kErrReq);
+      if (sub == 0) atomicOr(err, kErrReq);
       r0 = r1 = 0;
     }
     uint64_t Q = 0, KV = 0, P = 0, T = 0;
-    for (uint32_t r = r0 + lane; r < r1; r += 64) {
+    for (uint32_t r = r0 + sub; r < r1; r += kAggLanes) {
       const uint64_t q = rq[r], h = rh[r];
       Q += q;
       KV += h + q;
@@ -97,13 +104,13 @@ __global__ void k_attn_agg(const uint32_t *__restrict__ req_off, const uint32_t 
       T += (q + 127) >> 7;
     }
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
+    for (int off = kAggLanes / 2; off > 0; off >>= 1) {
       Q += __shfl_xor(Q, off);
       KV += __shfl_xor(KV, off);
       P += __shfl_xor(P, off);
       T += __shfl_xor(T, off);
     }
-    if (lane == 0) {
+    if (sub == 0) {
       agg[j] = Q;
       agg[n_steps + j] = KV;
       agg[2 * n_steps + j] = P;
@@ -463,7 +470,7 @@ struct HeadBF16 {
   //                            dot with w3)
   // Only the features, the last epilogue and the tail stay exposed.
   __device__ static __forceinline__ float mlp(const float (&x)[IN], const uint32_t *lds) {
-    static_assert(MB >= 2 && 8 % KC2 == 0 || MB > 4, "the pipelined head splits 8 register pairs over the chunks");
+    static_assert((MB >= 2 && 8 % KC2 == 0) || MB > 4, "the pipelined head splits 8 register pairs over the chunks");
     if constexpr (MB > 4) {
       return mlp_loop(x, lds);
     } else {
@@ -753,6 +760,51 @@ template <> struct MinWg<kBF16_16_128> { static constexpr int value = 2; };
 template <> struct MinWg<kBF16_32_64> { static constexpr int value = 2; };
 template <> struct MinWg<kBF16_32_128> { static constexpr int value = 2; };
 
+// One wave's tile: 64 consecutive records of one family (nvalid = 0 for an
+// idle wave of a family's last workgroup tile).
+struct Tile {
+  int fam, tile_in_fam, nvalid;
+  int64_t row0, fam_lo, fam_hi;
+};
+
+__device__ __forceinline__ Tile locate(const EvalParams &p, int wt, int wave) {
+  Tile t;
+  int fam = 0;
+  while (wt >= p.wgt_off[fam + 1]) ++fam;
+  t.fam = fam;
+  t.tile_in_fam = (wt - p.wgt_off[fam]) * kWgWaves + wave;
+  t.fam_lo = p.fam_off[fam];
+  t.fam_hi = p.fam_off[fam + 1];
+  t.row0 = t.fam_lo + (int64_t)t.tile_in_fam * kTileRows;
+  const int64_t left = t.fam_hi - t.row0;
+  t.nvalid = left <= 0 ? 0 : (left < kTileRows ? (int)left : kTileRows);
+  return t;
+}
+
+// The record fields a lane's family uses (the others are never read), plus
+// the steps just before and after the tile within its family.
+struct Fields {
+  uint32_t st, m, n, k, a, b, prev, next;
+};
+
+__device__ __forceinline__ Fields load_fields(const EvalParams &p, const Tile &t, int lane) {
+  Fields f = {0, 0, 0, 0, 0, 0, kNoKey, kNoKey};
+  if (t.nvalid == 0) return f;
+  const int64_t row = t.row0 + (lane < t.nvalid ? lane : 0);
+  const int fam = t.fam;
+  const bool grouped = fam == KS_GROUPED_GEMM;
+  const bool attn = fam == KS_ATTN_PREFILL || fam == KS_ATTN_DECODE;
+  f.st = p.step[row];
+  f.n = p.n[row];
+  if (!grouped && !attn) f.m = p.m[row];
+  if (fam != KS_RMSNORM && fam != KS_SILU_MUL && fam != KS_EMBED) f.k = p.k[row];
+  if (grouped || attn) f.a = p.a[row];
+  if (grouped) f.b = p.b[row];
+  if (t.row0 > t.fam_lo) f.prev = p.step[t.row0 - 1];
+  if (t.row0 + kTileRows < t.fam_hi) f.next = p.step[t.row0 + kTileRows];
+  return f;
+}
+
 template <int KIND>
 __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalParams p) {
   using H = typename KindOf<KIND>::H;
@@ -761,9 +813,21 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n_wgt = p.wgt_off[KS_NFAM];
   int staged = -1;
+  // the next tile's fields are loaded while the current one is evaluated
+  Tile tn = {};
+  Fields fn = {0, 0, 0, 0, 0, 0, kNoKey, kNoKey};
+  if ((int)blockIdx.x < n_wgt) {
+    tn = locate(p, blockIdx.x, wave);
+    fn = load_fields(p, tn, lane);
+  }
   for (int wt = blockIdx.x; wt < n_wgt; wt += gridDim.x) {
-    int fam = 0;
-    while (wt >= p.wgt_off[fam + 1]) ++fam;
+    const Tile tc = tn;
+    const Fields fc = fn;
+    if (wt + (int)gridDim.x < n_wgt) {
+      tn = locate(p, wt + gridDim.x, wave);
+      fn = load_fields(p, tn, lane);
+    }
+    const int fam = tc.fam;
     if constexpr (H::kMlp) {
       if (fam != staged) {
         __syncthreads();
@@ -772,19 +836,14 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
         staged = fam;
       }
     }
-    const int tile_in_fam = (wt - p.wgt_off[fam]) * kWgWaves + wave;
-    const int64_t fam_lo = p.fam_off[fam], fam_hi = p.fam_off[fam + 1];
-    const int64_t row0 = fam_lo + (int64_t)tile_in_fam * kTileRows;
-    if (row0 >= fam_hi) continue;  // an idle wave of the family's last workgroup tile
-    const int nvalid = (int)((fam_hi - row0) < kTileRows ? (fam_hi - row0) : kTileRows);
+    if (tc.nvalid == 0) continue;
+    const int nvalid = tc.nvalid;
     const bool valid = lane < nvalid;
-    const int64_t row = row0 + (valid ? lane : 0);
+    const int64_t row = tc.row0 + (valid ? lane : 0);
 
-    const uint32_t st = p.step[row];
     uint32_t bad = 0;
-    if ((int64_t)st >= p.n_steps) bad |= kErrStep;
-    const uint32_t nn = p.n[row], kk = p.k[row];
-    const Cnt c = record_counts(fam, p.m[row], nn, kk, p.a[row], p.b[row], st, p, bad);
+    if ((int64_t)fc.st >= p.n_steps) bad |= kErrStep;
+    const Cnt c = record_counts(fam, fc.m, fc.n, fc.k, fc.a, fc.b, fc.st, p, bad);
     if (valid && bad) atomicOr(p.err, bad);
     const bool live = valid && !(bad & kErrStep);
     if (valid) {
@@ -792,16 +851,24 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
       if (p.o_bytes) p.o_bytes[row] = c.Bt;
       if (p.o_blocks) p.o_blocks[row] = c.B;
     }
-    const RowC rc = row_consts(c, nn, kk);
+    const RowC rc = row_consts(c, fc.n, fc.k);
 
     // segment structure of this tile (spec-independent): keys are sorted
-    const uint32_t key = live ? st : kNoKey;
+    const uint32_t key = live ? fc.st : kNoKey;
     const uint32_t key_dn = __shfl_down(key, 1);
     const bool is_tail = live && (lane == 63 || key_dn != key);
     const uint32_t key0 = __shfl(key, 0);
-    const uint32_t prev = row0 > fam_lo ? p.step[row0 - 1] : kNoKey;
-    const bool to_carry = is_tail && key == key0 && prev == key0;
-    const int tile_id = p.tile_off[fam] + tile_in_fam;
+    const bool to_carry = is_tail && key == key0 && fc.prev == key0;
+    const int tile_id = p.tile_off[fam] + tc.tile_in_fam;
+    if (p.range) {
+      // the (family, step) record range, written where its global first
+      // and last records are
+      const uint32_t key_up = __shfl_up(key, 1);
+      const bool head = live && (lane == 0 ? fc.prev != key : key_up != key);
+      const bool tail = live && (lane == nvalid - 1 ? fc.next != key : key_dn != key);
+      if (head) p.range[2 * ((size_t)fam * p.n_steps + key)] = (uint32_t)row;
+      if (tail) p.range[2 * ((size_t)fam * p.n_steps + key) + 1] = (uint32_t)(row + 1);
+    }
     // A tail lane stores its segment's sum (seg_scan): into the tile's carry
     // slot if the segment continues from the previous tile, else into the
     // (spec, family, step) partial.
@@ -847,31 +914,6 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
 }
 
 // ------------------------------------------------------------ step finish
-__device__ __forceinline__ uint32_t lower_bound(const uint32_t *__restrict__ a, uint32_t lo, uint32_t hi,
-                                                uint32_t v) {
-  while (lo < hi) {
-    const uint32_t mid = lo + ((hi - lo) >> 1);
-    if (a[mid] < v) lo = mid + 1;
-    else hi = mid;
-  }
-  return lo;
-}
-
-// record range [r0, r1) of step j within family f
-__global__ void k_seg_range(FinishParams p) {
-  const int64_t total = (int64_t)KS_NFAM * p.n_steps;
-  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
-       idx += (int64_t)gridDim.x * blockDim.x) {
-    const int f = (int)(idx / p.n_steps);
-    const uint32_t j = (uint32_t)(idx - (int64_t)f * p.n_steps);
-    const uint32_t lo = (uint32_t)p.fam_off[f], hi = (uint32_t)p.fam_off[f + 1];
-    const uint32_t r0 = lower_bound(p.step, lo, hi, j);
-    const uint32_t r1 = lower_bound(p.step, r0, hi, j + 1);
-    p.range[2 * idx] = r0;
-    p.range[2 * idx + 1] = r1;
-  }
-}
-
 // per (spec, step): t_body, t_comm (Eq. 3, two all-reduces per layer),
 // t_gpu and t_step (Eq. 4)
 __global__ void k_finish(FinishParams p) {
@@ -882,11 +924,15 @@ __global__ void k_finish(FinishParams p) {
     const int64_t j = idx - (int64_t)s * p.n_steps;
     double body = 0.0;
     for (int f = 0; f < KS_NFAM; ++f) {
-      const uint32_t r0 = p.range[2 * (f * p.n_steps + j)];
-      const uint32_t r1 = p.range[2 * (f * p.n_steps + j) + 1];
+      // clamped to the family's rows: a range left half-written by unsorted
+      // input (reported by ks_validate) still indexes only this family's tiles
+      const int64_t base = p.fam_off[f], top = p.fam_off[f + 1];
+      int64_t r0 = p.range[2 * (f * p.n_steps + j)];
+      int64_t r1 = p.range[2 * (f * p.n_steps + j) + 1];
+      r0 = r0 < base ? base : (r0 > top ? top : r0);
+      r1 = r1 < base ? base : (r1 > top ? top : r1);
       if (r0 >= r1) continue;
       body += p.partial[((size_t)s * KS_NFAM + f) * p.n_steps + j];
-      const int64_t base = p.fam_off[f];
       const int t_first = p.tile_off[f] + (int)((r0 - base) / kTileRows);
       const int t_last = p.tile_off[f] + (int)((r1 - 1 - base) / kTileRows);
       for (int t = t_first + 1; t <= t_last; ++t) body += p.carry[(size_t)s * p.n_tiles + t];
@@ -958,17 +1004,16 @@ static int grid_for(int64_t n, int block, int cap) {
   return (int)(g < cap ? g : cap);
 }
 
-hipError_t launch_clear(uint32_t *err, hipStream_t s) {
-  hipLaunchKernelGGL(k_clear, dim3(1), dim3(64), 0, s, err);
+hipError_t launch_clear(uint32_t *err, uint32_t *range, int64_t n_range, hipStream_t s) {
+  hipLaunchKernelGGL(k_clear, dim3(grid_for(n_range, 256, 2048)), dim3(256), 0, s, err, range, n_range);
   return hipGetLastError();
 }
 
 hipError_t launch_attn_agg(const uint32_t *req_off, const uint32_t *q, const uint32_t *h, int64_t n_steps,
                            int64_t n_req, uint64_t *agg, uint32_t *err, hipStream_t s) {
   if (n_steps == 0) return hipSuccess;
-  // one wave per step, four waves per workgroup
-  hipLaunchKernelGGL(k_attn_agg, dim3(grid_for(n_steps, 4, 8192)), dim3(256), 0, s, req_off, q, h, n_steps,
-                     n_req, agg, err);
+  hipLaunchKernelGGL(k_attn_agg, dim3(grid_for(n_steps, 256 / kAggLanes, 8192)), dim3(256), 0, s, req_off, q, h,
+                     n_steps, n_req, agg, err);
   return hipGetLastError();
 }
 
@@ -1024,9 +1069,6 @@ hipError_t launch_eval(int kind, const EvalParams &p, hipStream_t s) {
 
 hipError_t launch_finish(const FinishParams &p, hipStream_t s) {
   if (p.n_steps == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_seg_range, dim3(grid_for((int64_t)KS_NFAM * p.n_steps, 256, 4096)), dim3(256), 0, s, p);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_finish, dim3(grid_for((int64_t)p.n_specs * p.n_steps, 256, 8192)), dim3(256), 0, s, p);
   return hipGetLastError();
 }

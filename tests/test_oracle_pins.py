@@ -205,7 +205,7 @@ def test_features_zero_work_limits():
     sp = o.spec_at(spec(), 0)
     c = o.kernel_counts(d)
     rf = o.roofline(c["F"], c["Bt"], c["B"], sp)
-    x = o.features(c, d.n, d.k, rf, sp)[0]
+    x = o.features(c, d.n, o.effective_k(d, np.arange(1)), rf, sp)[0]
     assert x[0] == -10 / 16 and x[1] == -20 / 16 and x[6] == -20 / 16
     assert x[3] == 1.0 and x[4] == 0.0 and x[5] == 1.0 and x[7] == 0.0
 

@@ -307,6 +307,10 @@ def build(traces: list[Trace]) -> tuple[Desc, StepRec]:
         nreq = np.diff(tr.req_off)
         tokens = step_tokens(tr)
         msrc = {"T": tokens, "2T": s.top_k * tokens, "R": nreq, "0": np.zeros(S, np.int64)}
+        for v in msrc.values():
+            assert v.size == 0 or (v.min() >= 0 and v.max() < 2 ** 32), "m does not fit u32"
+        assert step0 + S < 2 ** 32
+        msrc32 = {key: v.astype(np.uint32) for key, v in msrc.items()}
         lt = _layer_templates(s)
         attn_fam = np.where(tr.prefill, ATTN_PREFILL, ATTN_DECODE)
         for f in range(NFAM):
@@ -325,22 +329,26 @@ def build(traces: list[Trace]) -> tuple[Desc, StepRec]:
             nt = len(tpls)
             reps = s.layers if per_layer else 1
             cnt = reps * nt
-            st = np.repeat(sel, cnt)
-            slot = np.tile(np.arange(cnt), len(sel))
-            layer = slot // nt
-            which = slot % nt
-            n_arr = np.array([t.n for t in tpls], np.int64)[which]
-            k_arr = np.array([t.k for t in tpls], np.int64)[which]
-            a_arr = np.array([t.a for t in tpls], np.int64)[which]
-            m_arr = np.zeros(len(st), np.int64)
-            for ti, t in enumerate(tpls):
-                w = which == ti
-                m_arr[w] = msrc[t.m_src][st[w]]
-            b_arr = np.zeros(len(st), np.int64)
-            if any(t.grouped for t in tpls):
-                b_arr = np.where(np.array([t.grouped for t in tpls])[which],
-                                 e0 + (st * s.layers + layer) * s.experts, 0)
-            per_fam[f].append((st + step0, m_arr, n_arr, k_arr, a_arr, b_arr))
+            ns = len(sel)
+            # (step, slot) tables; slot = layer * nt + template
+            slot_tpl = [tpls[q % nt] for q in range(cnt)]
+            u32 = np.uint32
+            st = np.repeat((sel + step0).astype(u32), cnt)
+            n_arr = np.tile(np.array([t.n for t in slot_tpl], u32), ns)
+            k_arr = np.tile(np.array([t.k for t in slot_tpl], u32), ns)
+            a_arr = np.tile(np.array([t.a for t in slot_tpl], u32), ns)
+            m2 = np.empty((ns, cnt), u32)
+            for q, t in enumerate(slot_tpl):
+                m2[:, q] = msrc32[t.m_src][sel]
+            m_arr = m2.reshape(-1)
+            b2 = np.zeros((ns, cnt), u32)
+            for q, t in enumerate(slot_tpl):
+                if t.grouped:
+                    v = e0 + (sel * s.layers + q // nt) * s.experts
+                    assert v.size == 0 or (v.min() >= 0 and v.max() + s.experts <= 2 ** 32)
+                    b2[:, q] = v
+            b_arr = b2.reshape(-1)
+            per_fam[f].append((st, m_arr, n_arr, k_arr, a_arr, b_arr))
         req_off.append(tr.req_off[1:] + r0)
         req_q.append(tr.req_q)
         req_h.append(tr.req_h)
@@ -367,6 +375,8 @@ def build(traces: list[Trace]) -> tuple[Desc, StepRec]:
     def cat(xs, dt=np.uint32):
         if not xs:
             return np.zeros(0, dt)
+        if all(x.dtype == dt for x in xs):
+            return np.concatenate(xs) if len(xs) > 1 else xs[0]
         x = np.concatenate(xs)
         if x.size:
             assert x.min() >= 0 and x.max() < 2 ** 32, "field does not fit u32"
