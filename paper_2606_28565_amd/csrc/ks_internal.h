@@ -38,7 +38,8 @@ enum HeadKind : int {
 struct alignas(16) SpecC {
   float rcp_p, rcp_bw, bw_over_p, l2, t0, rcp_t0, n_f, rcp_n;
   double rcp_nd;
-  uint32_t n, pad0;
+  uint32_t n;
+  float lr;  // log2(BW / P)
   uint32_t pad[4];
 };
 static_assert(sizeof(SpecC) == 64, "SpecC is one 64-byte record");
@@ -102,13 +103,12 @@ struct ValidateParams {
 };
 
 hipError_t launch_clear(uint32_t *err, uint32_t *range, int64_t n_range, hipStream_t s);
-hipError_t launch_spec_prep(const ks_spec *specs, int32_t n_specs, SpecC *out, hipStream_t s);
+hipError_t launch_spec_prep(const ks_spec *specs, int32_t n_specs, SpecC *out, uint32_t *err, hipStream_t s);
 hipError_t launch_attn_agg(const uint32_t *req_off, const uint32_t *q, const uint32_t *h,
                            int64_t n_steps, int64_t n_req, uint64_t *agg, uint32_t *err,
                            hipStream_t s);
 hipError_t launch_eval(int kind, const EvalParams &p, hipStream_t s);
 hipError_t launch_finish(const FinishParams &p, hipStream_t s);
 hipError_t launch_validate(const ValidateParams &p, hipStream_t s);
-int eval_grid(int kind, int n_wgt);
 
 }  // namespace ks

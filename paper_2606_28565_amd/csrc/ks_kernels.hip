@@ -13,6 +13,8 @@
 //   k_finish     per (spec, step): body sum, all-reduce (Eq. 3), assembly (Eq. 4)
 #include <hip/hip_runtime.h>
 
+#include <atomic>
+
 #include "ks_internal.h"
 
 namespace ks {
@@ -200,17 +202,25 @@ __device__ __forceinline__ Cnt record_counts(int fam, uint32_t m32, uint32_t n32
 }
 
 // ------------------------------------------------------------ spec constants
-__global__ void k_spec_prep(const ks_spec *__restrict__ specs, int32_t n_specs, SpecC *__restrict__ out) {
+__global__ void k_spec_prep(const ks_spec *__restrict__ specs, int32_t n_specs, SpecC *__restrict__ out,
+                            uint32_t *err) {
   const int s = blockIdx.x * blockDim.x + threadIdx.x;
   if (s >= n_specs) return;
   const ks_spec sp = specs[s];
   SpecC c = {};
   const double P = sp.peak_flops, BW = sp.hbm_bw;
-  const uint32_t n = sp.n_cu < 1 ? 1u : sp.n_cu;
+  // n_cu outside 1 .. 65535 is clamped and flagged (the wave count relies on
+  // 24-bit products of it)
+  uint32_t n = sp.n_cu;
+  if (n < 1u || n > 65535u) {
+    atomicOr(err, kErrSpec);
+    n = n < 1u ? 1u : 65535u;
+  }
   c.n = n;
   c.rcp_p = (float)(1.0 / P);
   c.rcp_bw = (float)(1.0 / BW);
   c.bw_over_p = (float)(BW / P);
+  c.lr = (float)log2(BW / P);
   c.l2 = (float)sp.l2_bytes;
   c.t0 = (float)sp.t0;
   c.rcp_t0 = (float)(1.0 / fmax(sp.t0, 1e-9));
@@ -223,7 +233,7 @@ __global__ void k_spec_prep(const ks_spec *__restrict__ specs, int32_t n_specs, 
 // spec-independent per-record quantities
 struct RowC {
   uint64_t B;
-  float Ff, Btf, Bf, rcp_bt1, ai, x0, xs[7];  // xs = x8 .. x14
+  float Ff, Btf, Bf, rcp_b, rcp_bt1, la, x0, xs[7];  // la = log2(AI); xs = x8 .. x14
 };
 
 __device__ __forceinline__ RowC row_consts(const Cnt &c, uint32_t n, uint32_t k) {
@@ -232,33 +242,46 @@ __device__ __forceinline__ RowC row_consts(const Cnt &c, uint32_t n, uint32_t k)
   r.Ff = (float)c.F;
   r.Btf = (float)c.Bt;
   r.Bf = (float)c.B;
+  r.rcp_b = rcpf(fmaxf(r.Bf, 1.0f));
   r.rcp_bt1 = rcpf(fmaxf(r.Btf, 1.0f));
-  r.ai = r.Ff * r.rcp_bt1;
-  const float Bm1 = fmaxf(r.Bf, 1.0f);
-  r.x0 = log2f_fast(fmaxf(r.ai, 0x1p-10f)) * (1.0f / 16);
+  // log2(0) = -inf for F = 0; every use clamps it from below
+  r.la = log2f_fast(r.Ff * r.rcp_bt1);
+  r.x0 = fmaxf(r.la, -10.0f) * (1.0f / 16);
   r.xs[0] = log2f_fast(1.0f + r.Ff) * (1.0f / 64);
   r.xs[1] = log2f_fast(1.0f + r.Btf) * (1.0f / 48);
   r.xs[2] = log2f_fast(1.0f + (float)c.M) * (1.0f / 24);
   r.xs[3] = log2f_fast(1.0f + (float)n) * (1.0f / 24);
   r.xs[4] = log2f_fast(1.0f + (float)k) * (1.0f / 24);
-  r.xs[5] = log2f_fast(1.0f + r.Ff * rcpf(Bm1)) * (1.0f / 48);
-  r.xs[6] = log2f_fast(1.0f + r.Btf * rcpf(Bm1)) * (1.0f / 40);
+  r.xs[5] = log2f_fast(1.0f + r.Ff * r.rcp_b) * (1.0f / 48);
+  r.xs[6] = log2f_fast(1.0f + r.Btf * r.rcp_b) * (1.0f / 40);
   return r;
 }
+
+// Block counts below 2^23 (every record of the workloads): the wave count
+// in fp32 and 24-bit integer products.  With B < 2^23, fl(B fl(1/N)) is
+// within 1/N of B/N, so its ceiling is exact unless B/N is an integer k,
+// where it may come out k + 1; one test of (W - 1) N >= B corrects that.
+// W N <= B + N < 2^24, so the products are exact.
+constexpr uint32_t kSmallB = 1u << 23;
 
 struct Roof {
   float t_comp, t_mem, t_roof, u, W;
 };
 
 // waves, u and t_roof (Sec. 2.2, Eq. 2)
+template <bool kSmall>
 __device__ __forceinline__ Roof roofline(const RowC &r, const SpecC &s) {
   Roof o;
-  float wn = 0.0f;
-  if (r.B > 0) {
+  if constexpr (kSmall) {
+    const uint32_t B = (uint32_t)r.B;
+    uint32_t W = (uint32_t)ceilf(r.Bf * s.rcp_n);
+    if (W > 0u && __umul24(W - 1u, s.n) >= B) W -= 1u;
+    o.W = (float)W;
+    o.u = B > 0u ? (float)__umul24(W, s.n) * r.rcp_b : 1.0f;
+  } else if (r.B > 0) {
     const uint64_t W = ceil_div(r.B, s.n, s.rcp_nd);
     o.W = (float)W;
-    wn = (float)(W * s.n);
-    o.u = wn * rcpf(r.Bf);
+    o.u = (float)(W * s.n) * r.rcp_b;
   } else {
     o.W = 0.0f;
     o.u = 1.0f;
@@ -269,13 +292,15 @@ __device__ __forceinline__ Roof roofline(const RowC &r, const SpecC &s) {
   return o;
 }
 
-// the 16 dimensionless features (x[16 + i] = x[i]^2 for 32 inputs)
+// the 16 dimensionless features (x[16 + i] = x[i]^2 for 32 inputs);
+// x1 = log2(AI / ridge) = log2(AI) + log2(BW / P), and the last-wave
+// occupancy B / (W N) is 1 / u
 template <int IN>
 __device__ __forceinline__ void features(const RowC &r, const SpecC &s, const Roof &o, float (&x)[IN]) {
   x[0] = r.x0;
-  x[1] = log2f_fast(fmaxf(r.ai * s.bw_over_p, 0x1p-20f)) * (1.0f / 16);
-  x[2] = log2f_fast(1.0f + r.Bf * s.rcp_n) * (1.0f / 16);
-  x[3] = r.B > 0 ? r.Bf * rcpf(o.W * s.n_f) : 1.0f;
+  x[1] = fmaxf(r.la + s.lr, -20.0f) * (1.0f / 16);
+  x[2] = log2f_fast(fmaf(r.Bf, s.rcp_n, 1.0f)) * (1.0f / 16);
+  x[3] = rcpf(o.u);
   x[4] = log2f_fast(1.0f + o.W) * (1.0f / 16);
   x[5] = fminf(1.0f, s.l2 * r.rcp_bt1);
   x[6] = log2f_fast(fmaxf(o.t_roof * s.rcp_t0, 0x1p-20f)) * (1.0f / 16);
@@ -852,6 +877,9 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
       if (p.o_blocks) p.o_blocks[row] = c.B;
     }
     const RowC rc = row_consts(c, fc.n, fc.k);
+    // wave-uniform; the eta = 1 stream keeps the float64 path, which measured
+    // faster there (the head kinds spend their time in the spec loop)
+    const bool small = H::kMlp && __ballot(c.B >= kSmallB) == 0;
 
     // segment structure of this tile (spec-independent): keys are sorted
     const uint32_t key = live ? fc.st : kNoKey;
@@ -890,7 +918,7 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
     for (int s = 0; s < p.n_specs; ++s) {
       const SpecC sc = sc_next;
       sc_next = p.spec_c[s + 1 < p.n_specs ? s + 1 : s];   // in flight during this spec
-      const Roof o = roofline(rc, sc);
+      const Roof o = small ? roofline<true>(rc, sc) : roofline<false>(rc, sc);
       float eta = 1.0f;
       if constexpr (H::kMlp) {
         float x[IN];
@@ -1017,34 +1045,48 @@ hipError_t launch_attn_agg(const uint32_t *req_off, const uint32_t *q, const uin
   return hipGetLastError();
 }
 
-hipError_t launch_spec_prep(const ks_spec *specs, int32_t n_specs, SpecC *out, hipStream_t s) {
-  hipLaunchKernelGGL(k_spec_prep, dim3(grid_for(n_specs, 256, 4096)), dim3(256), 0, s, specs, n_specs, out);
+hipError_t launch_spec_prep(const ks_spec *specs, int32_t n_specs, SpecC *out, uint32_t *err, hipStream_t s) {
+  hipLaunchKernelGGL(k_spec_prep, dim3(grid_for(n_specs, 256, 4096)), dim3(256), 0, s, specs, n_specs, out, err);
   return hipGetLastError();
 }
 
-template <int KIND>
-static int lds_bytes() {
-  return (int)sizeof(uint32_t) * KindOf<KIND>::H::LDS_DW;
-}
+// The persistent grid: as many workgroups as are resident at once (the
+// occupancy the compiled kernel's registers and LDS allow, times the CU
+// count), so no workgroup of the head kinds waits for another to finish.
+// Cached per device and kind.
+constexpr int kMaxDevices = 64;
+static std::atomic<int> g_resident[kMaxDevices][kNumKinds];
 
-int eval_grid(int kind, int n_wgt) {
-  // workgroups resident per CU: bounded by LDS (160 KB per CU) and by the
-  // register budget of the head kernels; eta = 1 streams want many.
-  static const int lds[kNumKinds] = {
-      lds_bytes<kEtaOne>(), lds_bytes<kF32_16_64>(), lds_bytes<kF32_16_128>(), lds_bytes<kF32_32_64>(),
-      lds_bytes<kF32_32_128>(), lds_bytes<kBF16_16_64>(), lds_bytes<kBF16_16_128>(),
-      lds_bytes<kBF16_16_256>(), lds_bytes<kBF16_32_64>(), lds_bytes<kBF16_32_128>(),
-      lds_bytes<kBF16_32_256>()};
-  int per_cu = kind == kEtaOne ? 8 : 2;
-  const int by_lds = (160 * 1024) / (lds[kind] > 0 ? lds[kind] : 1);
-  if (by_lds < per_cu) per_cu = by_lds < 1 ? 1 : by_lds;
-  const int cap = 256 * per_cu;
-  return n_wgt < cap ? (n_wgt < 1 ? 1 : n_wgt) : cap;
+template <int KIND>
+static hipError_t resident_wgs(int *out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::atomic<int> *slot = dev < kMaxDevices ? &g_resident[dev][KIND] : nullptr;
+  int r = slot ? slot->load(std::memory_order_relaxed) : 0;
+  if (r == 0) {
+    int per_cu = 0, n_cu = 0;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_eval<KIND>, kWgThreads, 0);
+    if (e != hipSuccess) return e;
+    e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    // the eta = 1 stream is latency-bound: one workgroup per CU beyond the
+    // resident ones measured faster (the extra ones start as others retire)
+    if (KIND == kEtaOne) per_cu += 1;
+    r = (per_cu < 1 ? 1 : per_cu) * (n_cu < 1 ? 1 : n_cu);
+    if (slot) slot->store(r, std::memory_order_relaxed);
+  }
+  *out = r;
+  return hipSuccess;
 }
 
 template <int KIND>
 static hipError_t launch_kind(const EvalParams &p, hipStream_t s) {
-  const int grid = eval_grid(KIND, p.wgt_off[KS_NFAM]);
+  int cap = 0;
+  const hipError_t e = resident_wgs<KIND>(&cap);
+  if (e != hipSuccess) return e;
+  const int n_wgt = p.wgt_off[KS_NFAM];
+  const int grid = n_wgt < cap ? n_wgt : cap;
   hipLaunchKernelGGL(k_eval<KIND>, dim3(grid), dim3(kWgThreads), 0, s, p);
   return hipGetLastError();
 }
