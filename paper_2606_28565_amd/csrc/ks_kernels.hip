@@ -14,6 +14,7 @@
 #include <hip/hip_runtime.h>
 
 #include <atomic>
+#include <utility>
 
 #include "ks_internal.h"
 
@@ -482,6 +483,170 @@ struct HeadBF16 {
     }
   }
 
+  // ---- hidden 128: a fixed schedule of MFMA groups
+  // A group is one weight fragment times the two 32-record column blocks
+  // (two MFMAs, 64 cycles of the matrix core), followed by a slice of VALU
+  // work of another stage.  The table interleaves layer-1 blocks with the
+  // first layer-2 chunks so that each layer-1 block is packed (relu, bf16)
+  // in the groups right after it and before the chunk that consumes it,
+  // and starts each layer-2 block's epilogue one group after that block's
+  // last MFMA (and finishes it within the next block), so no VALU op waits
+  // on an MFMA that is still in flight behind it and the matrix core never
+  // drains.
+  struct Grp {
+    int mk, mb, kc;       // MFMA: 0 none, 1 layer 1, 2 layer 2; block; chunk
+    int vk, vb, vj, vn;   // VALU: 0 none, 1 pack (vj = half), 2 epilogue (pairs vj .. vj + vn - 1)
+  };
+  static constexpr int kNoV = 0, kPackV = 1, kEpiV = 2;
+  static constexpr Grp kSched16[] = {
+      {1, 0, 0, 0, 0, 0, 0}, {1, 1, 0, 1, 0, 0, 0}, {2, 0, 0, 1, 0, 1, 0}, {1, 2, 0, 1, 1, 0, 0},
+      {2, 0, 1, 1, 1, 1, 0}, {1, 3, 0, 1, 2, 0, 0}, {2, 0, 2, 1, 2, 1, 0}, {2, 0, 3, 1, 3, 0, 0},
+      {2, 0, 4, 1, 3, 1, 0}, {2, 0, 5, 0, 0, 0, 0}, {2, 0, 6, 0, 0, 0, 0}, {2, 0, 7, 0, 0, 0, 0},
+      {2, 1, 0, 0, 0, 0, 0}, {2, 1, 1, 2, 0, 0, 2}, {2, 1, 2, 2, 0, 2, 1}, {2, 1, 3, 2, 0, 3, 1},
+      {2, 1, 4, 2, 0, 4, 1}, {2, 1, 5, 2, 0, 5, 1}, {2, 1, 6, 2, 0, 6, 1}, {2, 1, 7, 2, 0, 7, 1},
+      {2, 2, 0, 0, 0, 0, 0}, {2, 2, 1, 2, 1, 0, 2}, {2, 2, 2, 2, 1, 2, 1}, {2, 2, 3, 2, 1, 3, 1},
+      {2, 2, 4, 2, 1, 4, 1}, {2, 2, 5, 2, 1, 5, 1}, {2, 2, 6, 2, 1, 6, 1}, {2, 2, 7, 2, 1, 7, 1},
+      {2, 3, 0, 0, 0, 0, 0}, {2, 3, 1, 2, 2, 0, 2}, {2, 3, 2, 2, 2, 2, 1}, {2, 3, 3, 2, 2, 3, 1},
+      {2, 3, 4, 2, 2, 4, 1}, {2, 3, 5, 2, 2, 5, 1}, {2, 3, 6, 2, 2, 6, 1}, {2, 3, 7, 2, 2, 7, 1}};
+  static constexpr Grp kSched32[] = {
+      {1, 0, 0, 0, 0, 0, 0}, {1, 0, 1, 0, 0, 0, 0}, {1, 1, 0, 0, 0, 0, 0}, {1, 1, 1, 1, 0, 0, 0},
+      {2, 0, 0, 1, 0, 1, 0}, {1, 2, 0, 1, 1, 0, 0}, {2, 0, 1, 1, 1, 1, 0}, {1, 2, 1, 0, 0, 0, 0},
+      {1, 3, 0, 0, 0, 0, 0}, {2, 0, 2, 1, 2, 0, 0}, {1, 3, 1, 1, 2, 1, 0}, {2, 0, 3, 0, 0, 0, 0},
+      {2, 0, 4, 1, 3, 0, 0}, {2, 0, 5, 1, 3, 1, 0}, {2, 0, 6, 0, 0, 0, 0}, {2, 0, 7, 0, 0, 0, 0},
+      {2, 1, 0, 0, 0, 0, 0}, {2, 1, 1, 2, 0, 0, 2}, {2, 1, 2, 2, 0, 2, 1}, {2, 1, 3, 2, 0, 3, 1},
+      {2, 1, 4, 2, 0, 4, 1}, {2, 1, 5, 2, 0, 5, 1}, {2, 1, 6, 2, 0, 6, 1}, {2, 1, 7, 2, 0, 7, 1},
+      {2, 2, 0, 0, 0, 0, 0}, {2, 2, 1, 2, 1, 0, 2}, {2, 2, 2, 2, 1, 2, 1}, {2, 2, 3, 2, 1, 3, 1},
+      {2, 2, 4, 2, 1, 4, 1}, {2, 2, 5, 2, 1, 5, 1}, {2, 2, 6, 2, 1, 6, 1}, {2, 2, 7, 2, 1, 7, 1},
+      {2, 3, 0, 0, 0, 0, 0}, {2, 3, 1, 2, 2, 0, 2}, {2, 3, 2, 2, 2, 2, 1}, {2, 3, 3, 2, 2, 3, 1},
+      {2, 3, 4, 2, 2, 4, 1}, {2, 3, 5, 2, 2, 5, 1}, {2, 3, 6, 2, 2, 6, 1}, {2, 3, 7, 2, 2, 7, 1}};
+  static constexpr int kNG = KC1 == 1 ? 36 : 40;
+  __device__ static constexpr Grp sched(int i) { return KC1 == 1 ? kSched16[i] : kSched32[i]; }
+
+  struct S4 {
+    u32x4 XB[2][KC1];
+    u32x4 frag[3];
+    f32x16 a1[2][2];
+    u32x4 H0[MB][2], H1[MB][2];
+    f32x16 c0, c1, p0, p1, bias;
+    uint32_t w3r[2][8];
+    float zacc[4];
+    const uint32_t *lb;
+    int lane, g;
+  };
+
+  // weight fragment of group I, from the lane's base address in LDS plus a
+  // constant offset
+  template <int I>
+  __device__ static __forceinline__ u32x4 frag_of(const uint32_t *lb) {
+    constexpr Grp q = sched(I);
+    constexpr int off = q.mk == 1 ? (q.mb * KC1 + q.kc) * 256 : OFF_W2 + (q.mb * KC2 + q.kc) * 256;
+    return *(const u32x4 *)(lb + off);
+  }
+
+  // one dot product pair of the layer-3 epilogue of the block held in p0/p1
+  __device__ static __forceinline__ void epi_pair(S4 &st, int slot, int j) {
+    const uint32_t w = st.w3r[slot][j];
+    st.zacc[j & 1] = dot2_bf16(relu_bf16x2(pack_bf16(st.p0[2 * j], st.p0[2 * j + 1])), w, st.zacc[j & 1]);
+    st.zacc[2 + (j & 1)] =
+        dot2_bf16(relu_bf16x2(pack_bf16(st.p1[2 * j], st.p1[2 * j + 1])), w, st.zacc[2 + (j & 1)]);
+  }
+
+  template <int I>
+  __device__ static __forceinline__ void group(S4 &st, const uint32_t *lds) {
+    constexpr Grp q = sched(I);
+    // weight fragment of the group two ahead
+    if constexpr (I + 2 < kNG) st.frag[(I + 2) % 3] = frag_of<I + 2>(st.lb);
+    const u32x4 a = st.frag[I % 3];
+    if constexpr (q.mk == 1) {
+      f32x16 &x0 = st.a1[q.mb & 1][0], &x1 = st.a1[q.mb & 1][1];
+      if constexpr (q.kc == 0) {
+        x0 = mfma(a, st.XB[0][0], f32x16{});
+        x1 = mfma(a, st.XB[1][0], f32x16{});
+      } else {
+        x0 = mfma(a, st.XB[0][q.kc], x0);
+        x1 = mfma(a, st.XB[1][q.kc], x1);
+      }
+    } else if constexpr (q.mk == 2) {
+      if constexpr (q.kc == 0) {
+        if constexpr (q.mb > 0) {
+          // block mb-1 is complete: its accumulators feed the epilogue, and
+          // its layer-3 weights are fetched a group before they are used
+          st.p0 = st.c0;
+          st.p1 = st.c1;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) st.w3r[(q.mb - 1) & 1][j] = lds[OFF_W3 + ((q.mb - 1) * 2 + st.g) * 8 + j];
+        }
+        st.c1 = mfma(a, st.H1[0][0], st.bias);
+        st.c0 = mfma(a, st.H0[0][0], st.bias);
+      } else {
+        st.c0 = mfma(a, st.H0[q.kc >> 1][q.kc & 1], st.c0);
+        st.c1 = mfma(a, st.H1[q.kc >> 1][q.kc & 1], st.c1);
+      }
+      if constexpr (q.kc == 4 && q.mb + 1 < MB)
+        st.bias = *(const f32x16 *)(lds + OFF_B2 + ((q.mb + 1) * 2 + st.g) * 16);
+      if constexpr (q.kc == 7 && q.mb == MB - 1) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) st.w3r[q.mb & 1][j] = lds[OFF_W3 + (q.mb * 2 + st.g) * 8 + j];
+      }
+    }
+    fence();
+    if constexpr (q.vk == kPackV) {
+      pack_part(st.a1[q.vb & 1][0], st.a1[q.vb & 1][1], st.H0[q.vb], st.H1[q.vb], 4 * q.vj, 4 * q.vj + 4);
+    } else if constexpr (q.vk == kEpiV) {
+#pragma unroll
+      for (int j = q.vj; j < q.vj + q.vn; ++j) epi_pair(st, q.vb & 1, j);
+      // an empty use pins the slice here; otherwise the dot chain, whose
+      // result is only needed at the end, is sunk below every MFMA
+      asm volatile("" ::"v"(st.zacc[0]), "v"(st.zacc[1]), "v"(st.zacc[2]), "v"(st.zacc[3]));
+    }
+    fence();
+  }
+
+  template <int... I>
+  __device__ static __forceinline__ void groups(S4 &st, const uint32_t *lds, std::integer_sequence<int, I...>) {
+    (group<I>(st, lds), ...);
+  }
+
+  __device__ static __forceinline__ float mlp4(const float (&x)[IN], const uint32_t *lds) {
+    S4 st;
+    st.lane = threadIdx.x & 63;
+    st.g = st.lane >> 5;
+    uint32_t P[IN / 2];
+#pragma unroll
+    for (int c = 0; c < IN / 2; ++c) P[c] = pack_bf16(x[2 * c], x[2 * c + 1]);
+#pragma unroll
+    for (int kc = 0; kc < KC1; ++kc) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        uint32_t lo = P[8 * kc + q], hi = P[8 * kc + 4 + q];
+        swap32(lo, hi);
+        st.XB[0][kc][q] = lo;
+        st.XB[1][kc][q] = hi;
+      }
+    }
+    st.lb = lds + st.lane * 4;
+    st.frag[0] = frag_of<0>(st.lb);
+    st.frag[1] = frag_of<1>(st.lb);
+    st.bias = *(const f32x16 *)(lds + OFF_B2 + st.g * 16);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) st.zacc[j] = 0.0f;
+    fence();
+    groups(st, lds, std::make_integer_sequence<int, kNG>{});
+    // block 3's epilogue
+    st.p0 = st.c0;
+    st.p1 = st.c1;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) epi_pair(st, 1, j);
+    // lanes l and l ^ 32 hold the two halves of the same record's dot
+    // product; after the swap lane l < 32 adds block 0's halves of record
+    // l and lane l >= 32 block 1's halves of record l.
+    uint32_t u0 = __builtin_bit_cast(uint32_t, st.zacc[0] + st.zacc[1]);
+    uint32_t u1 = __builtin_bit_cast(uint32_t, st.zacc[2] + st.zacc[3]);
+    swap32(u0, u1);
+    return __builtin_bit_cast(float, u0) + __builtin_bit_cast(float, u1) +
+           __builtin_bit_cast(float, lds[OFF_B3]);
+  }
+
   // z of the lane's own record; x: that record's features (fp32).
   //
   // A SIMD's VALU and matrix core only overlap when VALU work is issued in
@@ -498,6 +663,8 @@ struct HeadBF16 {
     static_assert((MB >= 2 && 8 % KC2 == 0) || MB > 4, "the pipelined head splits 8 register pairs over the chunks");
     if constexpr (MB > 4) {
       return mlp_loop(x, lds);
+    } else if constexpr (MB == 4) {
+      return mlp4(x, lds);
     } else {
       const int lane = threadIdx.x & 63, g = lane >> 5;
       // features -> bf16 pairs; the swap turns "own record" into the B
