@@ -231,6 +231,20 @@ __global__ void k_spec_prep(const ks_spec *__restrict__ specs, int32_t n_specs, 
   out[s] = c;
 }
 
+// Spec constants through the scalar cache: they are read-only during the
+// evaluation kernel and the index is wave-uniform, so the load goes through
+// the constant address space.
+// (The host pass of this file only parses device functions; it has no
+// constant address space.)
+__device__ __forceinline__ SpecC spec_at(const SpecC *base, int i) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  typedef const __attribute__((address_space(4))) SpecC *SpecCPtr;
+  return ((SpecCPtr)base)[__builtin_amdgcn_readfirstlane(i)];
+#else
+  return base[i];
+#endif
+}
+
 // spec-independent per-record quantities
 struct RowC {
   uint64_t B;
@@ -607,10 +621,9 @@ struct HeadBF16 {
     (group<I>(st, lds), ...);
   }
 
-  __device__ static __forceinline__ float mlp4(const float (&x)[IN], const uint32_t *lds) {
-    S4 st;
-    st.lane = threadIdx.x & 63;
-    st.g = st.lane >> 5;
+  // x -> bf16 pairs; the swap turns "own record" into the B layout of the
+  // two 32-record column blocks
+  __device__ static __forceinline__ void pack_x(const float (&x)[IN], u32x4 (&XB)[2][KC1]) {
     uint32_t P[IN / 2];
 #pragma unroll
     for (int c = 0; c < IN / 2; ++c) P[c] = pack_bf16(x[2 * c], x[2 * c + 1]);
@@ -620,9 +633,20 @@ struct HeadBF16 {
       for (int q = 0; q < 4; ++q) {
         uint32_t lo = P[8 * kc + q], hi = P[8 * kc + 4 + q];
         swap32(lo, hi);
-        st.XB[0][kc][q] = lo;
-        st.XB[1][kc][q] = hi;
+        XB[0][kc][q] = lo;
+        XB[1][kc][q] = hi;
       }
+    }
+  }
+
+  __device__ static __forceinline__ float mlp4(const u32x4 (&XB)[2][KC1], const uint32_t *lds) {
+    S4 st;
+    st.lane = threadIdx.x & 63;
+    st.g = st.lane >> 5;
+#pragma unroll
+    for (int kc = 0; kc < KC1; ++kc) {
+      st.XB[0][kc] = XB[0][kc];
+      st.XB[1][kc] = XB[1][kc];
     }
     st.lb = lds + st.lane * 4;
     st.frag[0] = frag_of<0>(st.lb);
@@ -664,7 +688,9 @@ struct HeadBF16 {
     if constexpr (MB > 4) {
       return mlp_loop(x, lds);
     } else if constexpr (MB == 4) {
-      return mlp4(x, lds);
+      u32x4 XB[2][KC1];
+      pack_x(x, XB);
+      return mlp4(XB, lds);
     } else {
       const int lane = threadIdx.x & 63, g = lane >> 5;
       // features -> bf16 pairs; the swap turns "own record" into the B
@@ -1081,10 +1107,10 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
       }
     }
 
-    SpecC sc_next = p.spec_c[0];
+    SpecC sc_next = spec_at(p.spec_c, 0);
     for (int s = 0; s < p.n_specs; ++s) {
       const SpecC sc = sc_next;
-      sc_next = p.spec_c[s + 1 < p.n_specs ? s + 1 : s];   // in flight during this spec
+      sc_next = spec_at(p.spec_c, s + 1 < p.n_specs ? s + 1 : s);   // in flight during this spec
       const Roof o = small ? roofline<true>(rc, sc) : roofline<false>(rc, sc);
       float eta = 1.0f;
       if constexpr (H::kMlp) {
