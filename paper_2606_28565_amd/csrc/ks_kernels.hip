@@ -202,6 +202,91 @@ __device__ __forceinline__ Cnt record_counts(int fam, uint32_t m32, uint32_t n32
   return c;
 }
 
+// The same counts with F and Bt rounded to fp32 as they are formed (each a
+// few roundings, within 1e-6 relative of the exact values) and B exact.
+// The eta = 1 stream uses it when no per-record count is written: it avoids
+// the 64-bit products and 64-bit to float conversions of the exact path.
+struct CntF {
+  float F, Bt;
+  uint64_t B;
+};
+
+__device__ __forceinline__ float u64_to_f32(uint64_t v) { return (float)v; }
+
+__device__ __forceinline__ CntF record_counts_f(int fam, uint32_t m32, uint32_t n32, uint32_t k32,
+                                                uint32_t a32, uint32_t b32, uint32_t step,
+                                                const EvalParams &p, uint32_t &bad) {
+  const float dt = (float)p.elem_bytes, M = (float)m32, N = (float)n32, K = (float)k32, A = (float)a32;
+  CntF c{0.0f, 0.0f, 0};
+  switch (fam) {
+    case KS_GEMM:
+    case KS_LM_HEAD:
+      c.F = (M * N) * (2.0f * K);
+      c.Bt = dt * (M * K + K * N + M * N);
+      c.B = (uint64_t)(((m32 + 127u) >> 7) * ((n32 + 127u) >> 7));
+      break;
+    case KS_GROUPED_GEMM: {
+      uint32_t ms = 0, act = 0, tiles = 0;
+      if ((uint64_t)b32 + a32 <= (uint64_t)p.n_expert_rows && a32 <= 1024) {
+        for (uint32_t e = 0; e < a32; ++e) {
+          const uint32_t me = p.expert_rows[b32 + e];
+          ms += me;
+          act += me > 0;
+          tiles += (me + 127u) >> 7;
+        }
+      } else {
+        bad |= kErrExpert;
+      }
+      const float Ms = (float)ms;
+      c.F = (Ms * N) * (2.0f * K);
+      c.Bt = dt * (Ms * K + (float)act * (K * N) + Ms * N);
+      c.B = (uint64_t)tiles * ((n32 + 127u) >> 7);
+      break;
+    }
+    case KS_ATTN_PREFILL:
+    case KS_ATTN_DECODE: {
+      uint64_t Q = 0, KV = 0, P = 0, T = 0;
+      if ((int64_t)step < p.n_steps) {
+        Q = p.agg[step];
+        KV = p.agg[p.n_steps + step];
+        P = p.agg[2 * p.n_steps + step];
+        T = p.agg[3 * p.n_steps + step];
+      }
+      const float NK = N * K;   // exact: N, K < 2^12
+      c.F = (4.0f * NK) * u64_to_f32(P);
+      c.Bt = dt * (2.0f * NK * u64_to_f32(Q) + (2.0f * A * K) * u64_to_f32(KV));
+      c.B = (uint64_t)n32 * T;
+      break;
+    }
+    case KS_RMSNORM:
+      c.F = 4.0f * (M * N);
+      c.Bt = dt * (2.0f * (M * N) + N);
+      c.B = m32;
+      break;
+    case KS_ROPE:
+      c.F = 3.0f * ((M * N) * K);
+      c.Bt = dt * (2.0f * ((M * N) * K) + M * K);
+      c.B = m32;
+      break;
+    case KS_SILU_MUL:
+      c.F = 5.0f * (M * N);
+      c.Bt = 3.0f * dt * (M * N);
+      c.B = ((uint64_t)m32 * n32 + 1023u) >> 10;
+      break;
+    case KS_KV_WRITE:
+      c.F = 0.0f;
+      c.Bt = 4.0f * dt * ((M * N) * K);
+      c.B = m32;
+      break;
+    default:  // KS_EMBED
+      c.F = 0.0f;
+      c.Bt = 2.0f * dt * (M * N) + 4.0f * M;
+      c.B = m32;
+      break;
+  }
+  return c;
+}
+
 // ------------------------------------------------------------ spec constants
 __global__ void k_spec_prep(const ks_spec *__restrict__ specs, int32_t n_specs, SpecC *__restrict__ out,
                             uint32_t *err) {
@@ -941,18 +1026,23 @@ __device__ __forceinline__ float dpp(float x) {
   return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, ROW, BANK, true));
 }
 
-__device__ __forceinline__ void seg_factors(uint32_t key, int lane, float (&f)[7]) {
-  const int c = lane & 15, row = lane >> 4;
-  const uint32_t k1 = __shfl(key, lane - 1), k2 = __shfl(key, lane - 2), k3 = __shfl(key, lane - 3);
-  const uint32_t k4 = __shfl(key, lane - 4), k8 = __shfl(key, lane - 8);
-  const uint32_t k15 = __shfl(key, row * 16 - 1), k31 = __shfl(key, 31);
-  f[0] = (c >= 1 && k1 == key) ? 1.0f : 0.0f;
-  f[1] = (c >= 2 && k2 == key) ? 1.0f : 0.0f;
-  f[2] = (c >= 3 && k3 == key) ? 1.0f : 0.0f;
-  f[3] = (c >= 4 && k4 == key) ? 1.0f : 0.0f;
-  f[4] = (c >= 8 && k8 == key) ? 1.0f : 0.0f;
-  f[5] = ((row & 1) && k15 == key) ? 1.0f : 0.0f;
-  f[6] = (row >= 2 && k31 == key) ? 1.0f : 0.0f;
+// key of the DPP source lane, or a value unequal to key where the pattern
+// has no source (bound_ctrl off: such lanes keep `old`)
+template <int CTRL, int ROW, int BANK>
+__device__ __forceinline__ uint32_t dpp_key(uint32_t key) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)(key ^ 1u), (int)key, CTRL, ROW, BANK, false);
+}
+
+// Factor of each seg_scan step: 1 where that step's DPP source lane holds
+// the same key (keys are sorted, so the lanes in between do too).
+__device__ __forceinline__ void seg_factors(uint32_t key, float (&f)[7]) {
+  f[0] = dpp_key<0x111, 0xf, 0xf>(key) == key ? 1.0f : 0.0f;
+  f[1] = dpp_key<0x112, 0xf, 0xf>(key) == key ? 1.0f : 0.0f;
+  f[2] = dpp_key<0x113, 0xf, 0xf>(key) == key ? 1.0f : 0.0f;
+  f[3] = dpp_key<0x114, 0xf, 0xe>(key) == key ? 1.0f : 0.0f;
+  f[4] = dpp_key<0x118, 0xf, 0xc>(key) == key ? 1.0f : 0.0f;
+  f[5] = dpp_key<0x142, 0xa, 0xf>(key) == key ? 1.0f : 0.0f;
+  f[6] = dpp_key<0x143, 0xc, 0xf>(key) == key ? 1.0f : 0.0f;
 }
 
 __device__ __forceinline__ float seg_scan(float v0, const float (&f)[7]) {
@@ -985,9 +1075,10 @@ struct Tile {
   int64_t row0, fam_lo, fam_hi;
 };
 
-__device__ __forceinline__ Tile locate(const EvalParams &p, int wt, int wave) {
+// fam0: a family at or before the tile's (workgroups walk tiles in order)
+__device__ __forceinline__ Tile locate(const EvalParams &p, int wt, int wave, int fam0) {
   Tile t;
-  int fam = 0;
+  int fam = fam0;
   while (wt >= p.wgt_off[fam + 1]) ++fam;
   t.fam = fam;
   t.tile_in_fam = (wt - p.wgt_off[fam]) * kWgWaves + wave;
@@ -1008,16 +1099,19 @@ struct Fields {
 __device__ __forceinline__ Fields load_fields(const EvalParams &p, const Tile &t, int lane) {
   Fields f = {0, 0, 0, 0, 0, 0, kNoKey, kNoKey};
   if (t.nvalid == 0) return f;
-  const int64_t row = t.row0 + (lane < t.nvalid ? lane : 0);
+  // wave-uniform bases plus a 32-bit lane offset (no per-lane 64-bit
+  // address arithmetic)
+  const uint32_t off = (uint32_t)(lane < t.nvalid ? lane : 0);
+  const int64_t r0 = t.row0;
   const int fam = t.fam;
   const bool grouped = fam == KS_GROUPED_GEMM;
   const bool attn = fam == KS_ATTN_PREFILL || fam == KS_ATTN_DECODE;
-  f.st = p.step[row];
-  f.n = p.n[row];
-  if (!grouped && !attn) f.m = p.m[row];
-  if (fam != KS_RMSNORM && fam != KS_SILU_MUL && fam != KS_EMBED) f.k = p.k[row];
-  if (grouped || attn) f.a = p.a[row];
-  if (grouped) f.b = p.b[row];
+  f.st = (p.step + r0)[off];
+  f.n = (p.n + r0)[off];
+  if (!grouped && !attn) f.m = (p.m + r0)[off];
+  if (fam != KS_RMSNORM && fam != KS_SILU_MUL && fam != KS_EMBED) f.k = (p.k + r0)[off];
+  if (grouped || attn) f.a = (p.a + r0)[off];
+  if (grouped) f.b = (p.b + r0)[off];
   if (t.row0 > t.fam_lo) f.prev = p.step[t.row0 - 1];
   if (t.row0 + kTileRows < t.fam_hi) f.next = p.step[t.row0 + kTileRows];
   return f;
@@ -1028,21 +1122,21 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
   using H = typename KindOf<KIND>::H;
   constexpr int IN = KindOf<KIND>::IN;
   __shared__ uint32_t lds[H::LDS_DW];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int n_wgt = p.wgt_off[KS_NFAM];
   int staged = -1;
   // the next tile's fields are loaded while the current one is evaluated
   Tile tn = {};
   Fields fn = {0, 0, 0, 0, 0, 0, kNoKey, kNoKey};
   if ((int)blockIdx.x < n_wgt) {
-    tn = locate(p, blockIdx.x, wave);
+    tn = locate(p, blockIdx.x, wave, 0);
     fn = load_fields(p, tn, lane);
   }
   for (int wt = blockIdx.x; wt < n_wgt; wt += gridDim.x) {
     const Tile tc = tn;
     const Fields fc = fn;
     if (wt + (int)gridDim.x < n_wgt) {
-      tn = locate(p, wt + gridDim.x, wave);
+      tn = locate(p, wt + gridDim.x, wave, tc.fam);
       fn = load_fields(p, tn, lane);
     }
     const int fam = tc.fam;
@@ -1061,30 +1155,38 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
 
     uint32_t bad = 0;
     if ((int64_t)fc.st >= p.n_steps) bad |= kErrStep;
-    const Cnt c = record_counts(fam, fc.m, fc.n, fc.k, fc.a, fc.b, fc.st, p, bad);
+    RowC rc;
+    if (!H::kMlp && !p.o_flops && !p.o_bytes && !p.o_blocks) {
+      const CntF cf = record_counts_f(fam, fc.m, fc.n, fc.k, fc.a, fc.b, fc.st, p, bad);
+      rc.B = cf.B;
+      rc.Ff = cf.F;
+      rc.Btf = cf.Bt;
+      rc.Bf = (float)cf.B;
+      rc.rcp_b = rcpf(fmaxf(rc.Bf, 1.0f));
+    } else {
+      const Cnt c = record_counts(fam, fc.m, fc.n, fc.k, fc.a, fc.b, fc.st, p, bad);
+      if (valid) {
+        if (p.o_flops) p.o_flops[row] = c.F;
+        if (p.o_bytes) p.o_bytes[row] = c.Bt;
+        if (p.o_blocks) p.o_blocks[row] = c.B;
+      }
+      rc = row_consts(c, fc.n, fc.k);
+    }
     if (valid && bad) atomicOr(p.err, bad);
     const bool live = valid && !(bad & kErrStep);
-    if (valid) {
-      if (p.o_flops) p.o_flops[row] = c.F;
-      if (p.o_bytes) p.o_bytes[row] = c.Bt;
-      if (p.o_blocks) p.o_blocks[row] = c.B;
-    }
-    const RowC rc = row_consts(c, fc.n, fc.k);
-    // wave-uniform; the eta = 1 stream keeps the float64 path, which measured
-    // faster there (the head kinds spend their time in the spec loop)
-    const bool small = H::kMlp && __ballot(c.B >= kSmallB) == 0;
+    const bool small = __ballot(rc.B >= kSmallB) == 0;   // wave-uniform
 
     // segment structure of this tile (spec-independent): keys are sorted
     const uint32_t key = live ? fc.st : kNoKey;
-    const uint32_t key_dn = __shfl_down(key, 1);
-    const bool is_tail = live && (lane == 63 || key_dn != key);
-    const uint32_t key0 = __shfl(key, 0);
+    const uint32_t key_dn = dpp_key<0x130, 0xf, 0xf>(key);   // wave_shl:1, lane 63: unequal
+    const bool is_tail = live && key_dn != key;
+    const uint32_t key0 = __builtin_amdgcn_readfirstlane(key);
     const bool to_carry = is_tail && key == key0 && fc.prev == key0;
     const int tile_id = p.tile_off[fam] + tc.tile_in_fam;
     if (p.range) {
       // the (family, step) record range, written where its global first
       // and last records are
-      const uint32_t key_up = __shfl_up(key, 1);
+      const uint32_t key_up = dpp_key<0x138, 0xf, 0xf>(key);   // wave_shr:1
       const bool head = live && (lane == 0 ? fc.prev != key : key_up != key);
       const bool tail = live && (lane == nvalid - 1 ? fc.next != key : key_dn != key);
       if (head) p.range[2 * ((size_t)fam * p.n_steps + key)] = (uint32_t)row;
@@ -1094,7 +1196,7 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
     // slot if the segment continues from the previous tile, else into the
     // (spec, family, step) partial.
     float fac[7];
-    seg_factors(key, lane, fac);
+    seg_factors(key, fac);
     double *dst = nullptr;
     size_t dst_stride = 0;
     if (p.partial && is_tail) {
@@ -1107,10 +1209,8 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
       }
     }
 
-    SpecC sc_next = spec_at(p.spec_c, 0);
     for (int s = 0; s < p.n_specs; ++s) {
-      const SpecC sc = sc_next;
-      sc_next = spec_at(p.spec_c, s + 1 < p.n_specs ? s + 1 : s);   // in flight during this spec
+      const SpecC sc = spec_at(p.spec_c, s);
       const Roof o = small ? roofline<true>(rc, sc) : roofline<false>(rc, sc);
       float eta = 1.0f;
       if constexpr (H::kMlp) {

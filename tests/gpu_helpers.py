@@ -23,13 +23,16 @@ def eval_kernels(wl, eta_one=False, n_specs=None, counts=True):
     return out
 
 
-def eval_steps(wl, eta_one=False, n_specs=None, per_pair=True):
+def eval_steps(wl, eta_one=False, n_specs=None, per_pair=True, counts=True):
+    """counts=False asks for per-pair outputs without the per-record counts
+    (the eta = 1 stream then forms F and Bt in fp32)."""
     import torch
     di = abi.DeviceInputs(wl, n_specs=n_specs)
     heads = di.make_heads(wl.heads.precision, wl.heads.in_dim, wl.heads.hidden,
                           abi.KS_ETA_ONE if eta_one else abi.KS_ETA_MLP)
     so_t, so = abi.step_outputs(wl.desc.n_steps, di.n_specs)
-    ko_t, ko = abi.kernel_outputs(wl.desc.n_rows, di.n_specs) if per_pair else ({}, None)
+    ko_t, ko = (abi.kernel_outputs(wl.desc.n_rows, di.n_specs, counts=counts) if per_pair
+                else ({}, None))
     abi.ks_eval_steps(di.desc, di.steps, di.specs_ptr, di.n_specs, heads, di.host, so, ko,
                       di.ws_ptr, di.ws_bytes, abi.current_stream())
     torch.cuda.synchronize()

@@ -12,6 +12,7 @@ from oracle import ks_oracle as o
 from workload import gen
 from tests import gpu_helpers as g
 from tests.helpers import make_desc, spec, steprec
+from paper_2606_28565_amd import abi
 
 pytestmark = pytest.mark.gpu
 
@@ -64,9 +65,10 @@ def z_error_bound(wl, ref):
 
 def _check_kernels(wl, gpu, ref, bf16, eta_one=False, ztol=ZTOL):
     c = ref["counts"]
-    np.testing.assert_array_equal(gpu["flops"], c["F"])
-    np.testing.assert_array_equal(gpu["bytes"], c["Bt"])
-    np.testing.assert_array_equal(gpu["blocks"], c["B"])
+    if "flops" in gpu:
+        np.testing.assert_array_equal(gpu["flops"], c["F"])
+        np.testing.assert_array_equal(gpu["bytes"], c["Bt"])
+        np.testing.assert_array_equal(gpu["blocks"], c["B"])
     assert g.rel_err(gpu["t_roof"], ref["t_roof"]).max() <= REL
     if eta_one:
         assert (gpu["eta"] == 1.0).all()
@@ -290,3 +292,80 @@ def test_many_specs_single_step():
     sp = gen.specs_grid(n, 99)
     rows = [(gen.GEMM, 0, int(m), 4096, 4096, 0, 0) for m in rng.integers(1, 5000, 70)]
     _edge_check(_wl(make_desc(rows, [[(5, 9)]]), 1, specs=sp, heads=gen.make_heads(16, 128, "bf16")))
+
+
+# ---------------------------------------------- eta = 1 stream, wave count ----
+def _eta1_case(wl, counts):
+    ref = o.eval_kernels(wl.desc, wl.specs, eta_one=True)
+    gpu = g.eval_steps(wl, eta_one=True, counts=counts)
+    assert ("flops" in gpu) == counts
+    _check_kernels(wl, gpu, ref, bf16=False, eta_one=True)
+    rs = o.eval_steps(wl.desc, wl.steps, wl.specs, wl.host, eta_one=True, kern=ref)
+    _check_steps(wl, gpu, rs, bf16=False, n_specs=wl.n_specs)
+    steps_only = g.eval_steps(wl, eta_one=True, per_pair=False)
+    _check_steps(wl, steps_only, rs, bf16=False, n_specs=wl.n_specs)
+
+
+def test_eta_one_without_count_outputs():
+    """Without per-record count outputs the eta = 1 stream forms F and Bt in
+    fp32; t_roof, t and the step sums keep the 1e-5 bar."""
+    _eta1_case(gen.config1(0, 120), counts=False)
+    _eta1_case(gen.config3(0, 40), counts=False)
+
+
+def _multi_spec(n_cus):
+    n = len(n_cus)
+    rng = np.random.default_rng(11)
+    return {"peak_flops": rng.uniform(0.5e15, 5e15, n), "hbm_bw": rng.uniform(2e12, 1e13, n),
+            "t0": np.full(n, 2e-6), "l2_bytes": np.full(n, 64.0 * 2 ** 20),
+            "ar_alpha0": np.full(n, 8e-6), "ar_alpha_log2p": np.full(n, 2e-6),
+            "ar_beta": np.full(n, 300e9), "n_cu": np.asarray(n_cus, np.int64)}
+
+
+def _block_count_workload(heads=None):
+    """Block counts that are exact multiples of the CU counts, and one off,
+    in a first SiLU tile that stays below 2^23; then a SiLU tile that
+    crosses it (2^23 - 1, 2^23, 2^23 + 1, a multiple of 148 just above,
+    2^24 - 1 and about 2^32).  A SiLU record (T, I) has B = ceil(T I / 1024),
+    so (T, 1024) gives B = T."""
+    n_cus = [148, 132, 256, 97, 1, 65535]
+    rows = []
+    for n in n_cus[:4]:                      # GEMM: B = ceil(M/128) ceil(N/128)
+        for k in (1, 3, 7):
+            for d in (-1, 0, 1):
+                bb = k * n + d
+                rows.append((gen.GEMM, 0, 128 * bb, 128, 64, 0, 0))
+                rows.append((gen.GEMM, 0, 128 * bb - 5, 100, 64, 0, 0))
+    small = [148 * k + d for k in (1, 50, 5000, 56679) for d in (-1, 0, 1)]
+    small += [132 * k + d for k in (1, 63550) for d in (-1, 0, 1)]
+    small += [256 * k + d for k in (1, 32767) for d in (-1, 0, 1)]
+    small += [97 * k + d for k in (1, 86479) for d in (-1, 0, 1)]
+    small += [65535 * k + d for k in (1, 128) for d in (-1, 0, 1)]
+    assert max(small) < (1 << 23) and len(small) <= 64
+    rows += [(gen.SILU_MUL, 0, v, 1024, 0, 0, 0) for v in small]
+    rows += [(gen.SILU_MUL, 0, 3 * 1024 + 7, 1, 0, 0, 0)] * (64 - len(small))
+    big = [(1 << 23) - 1, 1 << 23, (1 << 23) + 1, 148 * 56680, (1 << 24) - 1]
+    rows += [(gen.SILU_MUL, 0, v, 1024, 0, 0, 0) for v in big]
+    rows += [(gen.SILU_MUL, 0, (1 << 24) - 1, (1 << 18) - 1, 0, 0, 0), (gen.SILU_MUL, 0, 5, 7, 0, 0, 0)]
+    d = make_desc(rows, [[(1, 1)]])
+    return _wl(d, 1, specs=_multi_spec(n_cus), heads=heads)
+
+
+def test_block_counts_around_the_fp32_wave_path():
+    wl = _block_count_workload()
+    b = o.kernel_counts(wl.desc)["B"]
+    assert (b >= (1 << 23)).any() and (b < (1 << 23)).any()
+    _eta1_case(wl, counts=True)
+    _eta1_case(wl, counts=False)
+
+
+def test_block_counts_around_the_fp32_wave_path_bf16_head():
+    _edge_check(_block_count_workload(heads=gen.make_heads(16, 128, "bf16")))
+
+
+def test_n_cu_above_limit_flagged():
+    sp = spec(n_cu=70000)
+    wl = _wl(make_desc([(gen.GEMM, 0, 77, 300, 129, 0, 0)], [[(1, 5)]]), 1, specs=sp)
+    with pytest.raises(abi.KsError) as e:
+        g.eval_kernels(wl, eta_one=True)
+    assert e.value.status == abi.KS_ERANGE
