@@ -415,6 +415,15 @@ __device__ __forceinline__ void features(const RowC &r, const SpecC &s, const Ro
   }
 }
 
+// MFMA group schedules of the bf16 heads (gen_sched.py writes them and
+// checks their dependencies): {MFMA kind (0 none, 1 layer 1, 2 layer 2),
+// block, chunk, VALU kind (0 none, 1 pack, 2 epilogue), block, pack half or
+// first epilogue pair, epilogue pairs}.
+struct SchedGrp {
+  int mk, mb, kc, vk, vb, vj, vn;
+};
+#include "ks_sched.inc"
+
 // ------------------------------------------------------------ bf16 MFMA head
 // Orientation: hidden units are the MFMA rows (A = weights), the 64 records
 // of a wave are the columns (B = activations, two 32-column blocks), so the
@@ -484,68 +493,6 @@ struct HeadBF16 {
     if (threadIdx.x == 0) lds[OFF_B3] = __builtin_bit_cast(uint32_t, bf16_to_f32(b3[0]));
   }
 
-  // The 256-unit heads: layer 2 one 32-unit block at a time in a loop, which
-  // keeps only that block's weight fragments and accumulators live.
-  __device__ static __forceinline__ float mlp_loop(const float (&x)[IN], const uint32_t *lds) {
-    const int lane = threadIdx.x & 63, g = lane >> 5;
-    uint32_t P[IN / 2];
-#pragma unroll
-    for (int c = 0; c < IN / 2; ++c) P[c] = pack_bf16(x[2 * c], x[2 * c + 1]);
-    u32x4 XB[2][KC1];
-#pragma unroll
-    for (int kc = 0; kc < KC1; ++kc) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        uint32_t lo = P[8 * kc + q], hi = P[8 * kc + 4 + q];
-        swap32(lo, hi);
-        XB[0][kc][q] = lo;
-        XB[1][kc][q] = hi;
-      }
-    }
-    u32x4 H0[MB][2], H1[MB][2];
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      f32x16 c0 = {}, c1 = {};
-#pragma unroll
-      for (int kc = 0; kc < KC1; ++kc) {
-        const u32x4 a = *(const u32x4 *)(lds + ((mb * KC1 + kc) * 64 + lane) * 4);
-        c0 = mfma(a, XB[0][kc], c0);
-        c1 = mfma(a, XB[1][kc], c1);
-      }
-      pack_h1(c0, c1, H0[mb], H1[mb]);
-    }
-    float z0 = 0.0f, z1 = 0.0f;
-#pragma unroll 1
-    for (int mb = 0; mb < MB; ++mb) {
-      f32x16 c0 = *(const f32x16 *)(lds + OFF_B2 + (mb * 2 + g) * 16), c1 = c0;
-#pragma unroll
-      for (int kc = 0; kc < KC2; ++kc) {
-        const u32x4 a = *(const u32x4 *)(lds + OFF_W2 + ((mb * KC2 + kc) * 64 + lane) * 4);
-        c0 = mfma(a, H0[kc >> 1][kc & 1], c0);
-        c1 = mfma(a, H1[kc >> 1][kc & 1], c1);
-      }
-      epilogue(c0, c1, lds + OFF_W3 + (mb * 2 + g) * 8, z0, z1);
-    }
-    uint32_t u0 = __builtin_bit_cast(uint32_t, z0), u1 = __builtin_bit_cast(uint32_t, z1);
-    swap32(u0, u1);
-    return __builtin_bit_cast(float, u0) + __builtin_bit_cast(float, u1) +
-           __builtin_bit_cast(float, lds[OFF_B3]);
-  }
-
-  // relu + bf16 rounding of a 32-unit block of layer 1 (both column blocks)
-  __device__ static __forceinline__ void pack_h1(const f32x16 &c0, const f32x16 &c1, u32x4 (&h0)[2],
-                                                 u32x4 (&h1)[2]) {
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int r = 8 * h + 2 * q;
-        h0[h][q] = relu_bf16x2(pack_bf16(c0[r], c0[r + 1]));
-        h1[h][q] = relu_bf16x2(pack_bf16(c1[r], c1[r + 1]));
-      }
-    }
-  }
-
   // layer 3 over one 32-unit block of layer 2: z += w3 . bf16(relu(h2))
   template <typename W3>
   __device__ static __forceinline__ void epilogue(const f32x16 &c0, const f32x16 &c1, const W3 &w3,
@@ -582,7 +529,7 @@ struct HeadBF16 {
     }
   }
 
-  // ---- hidden 128: a fixed schedule of MFMA groups
+  // ---- a fixed schedule of MFMA groups (hidden 128 and 256)
   // A group is one weight fragment times the two 32-record column blocks
   // (two MFMAs, 64 cycles of the matrix core), followed by a slice of VALU
   // work of another stage.  The table interleaves layer-1 blocks with the
@@ -592,34 +539,14 @@ struct HeadBF16 {
   // last MFMA (and finishes it within the next block), so no VALU op waits
   // on an MFMA that is still in flight behind it and the matrix core never
   // drains.
-  struct Grp {
-    int mk, mb, kc;       // MFMA: 0 none, 1 layer 1, 2 layer 2; block; chunk
-    int vk, vb, vj, vn;   // VALU: 0 none, 1 pack (vj = half), 2 epilogue (pairs vj .. vj + vn - 1)
-  };
+  using Grp = SchedGrp;
   static constexpr int kNoV = 0, kPackV = 1, kEpiV = 2;
-  static constexpr Grp kSched16[] = {
-      {1, 0, 0, 0, 0, 0, 0}, {1, 1, 0, 1, 0, 0, 0}, {2, 0, 0, 1, 0, 1, 0}, {1, 2, 0, 1, 1, 0, 0},
-      {2, 0, 1, 1, 1, 1, 0}, {1, 3, 0, 1, 2, 0, 0}, {2, 0, 2, 1, 2, 1, 0}, {2, 0, 3, 1, 3, 0, 0},
-      {2, 0, 4, 1, 3, 1, 0}, {2, 0, 5, 0, 0, 0, 0}, {2, 0, 6, 0, 0, 0, 0}, {2, 0, 7, 0, 0, 0, 0},
-      {2, 1, 0, 0, 0, 0, 0}, {2, 1, 1, 2, 0, 0, 2}, {2, 1, 2, 2, 0, 2, 1}, {2, 1, 3, 2, 0, 3, 1},
-      {2, 1, 4, 2, 0, 4, 1}, {2, 1, 5, 2, 0, 5, 1}, {2, 1, 6, 2, 0, 6, 1}, {2, 1, 7, 2, 0, 7, 1},
-      {2, 2, 0, 0, 0, 0, 0}, {2, 2, 1, 2, 1, 0, 2}, {2, 2, 2, 2, 1, 2, 1}, {2, 2, 3, 2, 1, 3, 1},
-      {2, 2, 4, 2, 1, 4, 1}, {2, 2, 5, 2, 1, 5, 1}, {2, 2, 6, 2, 1, 6, 1}, {2, 2, 7, 2, 1, 7, 1},
-      {2, 3, 0, 0, 0, 0, 0}, {2, 3, 1, 2, 2, 0, 2}, {2, 3, 2, 2, 2, 2, 1}, {2, 3, 3, 2, 2, 3, 1},
-      {2, 3, 4, 2, 2, 4, 1}, {2, 3, 5, 2, 2, 5, 1}, {2, 3, 6, 2, 2, 6, 1}, {2, 3, 7, 2, 2, 7, 1}};
-  static constexpr Grp kSched32[] = {
-      {1, 0, 0, 0, 0, 0, 0}, {1, 0, 1, 0, 0, 0, 0}, {1, 1, 0, 0, 0, 0, 0}, {1, 1, 1, 1, 0, 0, 0},
-      {2, 0, 0, 1, 0, 1, 0}, {1, 2, 0, 1, 1, 0, 0}, {2, 0, 1, 1, 1, 1, 0}, {1, 2, 1, 0, 0, 0, 0},
-      {1, 3, 0, 0, 0, 0, 0}, {2, 0, 2, 1, 2, 0, 0}, {1, 3, 1, 1, 2, 1, 0}, {2, 0, 3, 0, 0, 0, 0},
-      {2, 0, 4, 1, 3, 0, 0}, {2, 0, 5, 1, 3, 1, 0}, {2, 0, 6, 0, 0, 0, 0}, {2, 0, 7, 0, 0, 0, 0},
-      {2, 1, 0, 0, 0, 0, 0}, {2, 1, 1, 2, 0, 0, 2}, {2, 1, 2, 2, 0, 2, 1}, {2, 1, 3, 2, 0, 3, 1},
-      {2, 1, 4, 2, 0, 4, 1}, {2, 1, 5, 2, 0, 5, 1}, {2, 1, 6, 2, 0, 6, 1}, {2, 1, 7, 2, 0, 7, 1},
-      {2, 2, 0, 0, 0, 0, 0}, {2, 2, 1, 2, 1, 0, 2}, {2, 2, 2, 2, 1, 2, 1}, {2, 2, 3, 2, 1, 3, 1},
-      {2, 2, 4, 2, 1, 4, 1}, {2, 2, 5, 2, 1, 5, 1}, {2, 2, 6, 2, 1, 6, 1}, {2, 2, 7, 2, 1, 7, 1},
-      {2, 3, 0, 0, 0, 0, 0}, {2, 3, 1, 2, 2, 0, 2}, {2, 3, 2, 2, 2, 2, 1}, {2, 3, 3, 2, 2, 3, 1},
-      {2, 3, 4, 2, 2, 4, 1}, {2, 3, 5, 2, 2, 5, 1}, {2, 3, 6, 2, 2, 6, 1}, {2, 3, 7, 2, 2, 7, 1}};
-  static constexpr int kNG = KC1 == 1 ? 36 : 40;
-  __device__ static constexpr Grp sched(int i) { return KC1 == 1 ? kSched16[i] : kSched32[i]; }
+  __device__ static constexpr Grp sched(int i) {
+    if constexpr (MB == 4) return KC1 == 1 ? kSched_4_1[i] : kSched_4_2[i];
+    else return KC1 == 1 ? kSched_8_1[i] : kSched_8_2[i];
+  }
+  static constexpr int kNG = MB == 4 ? (KC1 == 1 ? sizeof(kSched_4_1) : sizeof(kSched_4_2)) / sizeof(Grp)
+                                     : (KC1 == 1 ? sizeof(kSched_8_1) : sizeof(kSched_8_2)) / sizeof(Grp);
 
   struct S4 {
     u32x4 XB[2][KC1];
@@ -629,17 +556,19 @@ struct HeadBF16 {
     f32x16 c0, c1, p0, p1, bias;
     uint32_t w3r[2][8];
     float zacc[4];
-    const uint32_t *lb;
+    uint32_t lo[3];   // the lane's fragment offset (dwords) from LDS 0, 64 KB and 128 KB
     int lane, g;
   };
 
   // weight fragment of group I, from the lane's base address in LDS plus a
   // constant offset
+  // (ds_read offsets are 16-bit byte offsets: fragments beyond 64 KB use a
+  // second or third lane base, 64 KB and 128 KB further on)
   template <int I>
-  __device__ static __forceinline__ u32x4 frag_of(const uint32_t *lb) {
+  __device__ static __forceinline__ u32x4 frag_of(const uint32_t *lds, const uint32_t (&lo)[3]) {
     constexpr Grp q = sched(I);
     constexpr int off = q.mk == 1 ? (q.mb * KC1 + q.kc) * 256 : OFF_W2 + (q.mb * KC2 + q.kc) * 256;
-    return *(const u32x4 *)(lb + off);
+    return *(const u32x4 *)(lds + lo[off >> 14] + (off & 16383));
   }
 
   // one dot product pair of the layer-3 epilogue of the block held in p0/p1
@@ -654,7 +583,7 @@ struct HeadBF16 {
   __device__ static __forceinline__ void group(S4 &st, const uint32_t *lds) {
     constexpr Grp q = sched(I);
     // weight fragment of the group two ahead
-    if constexpr (I + 2 < kNG) st.frag[(I + 2) % 3] = frag_of<I + 2>(st.lb);
+    if constexpr (I + 2 < kNG && sched(I + 2).mk != 0) st.frag[(I + 2) % 3] = frag_of<I + 2>(lds, st.lo);
     const u32x4 a = st.frag[I % 3];
     if constexpr (q.mk == 1) {
       f32x16 &x0 = st.a1[q.mb & 1][0], &x1 = st.a1[q.mb & 1][1];
@@ -681,9 +610,9 @@ struct HeadBF16 {
         st.c0 = mfma(a, st.H0[q.kc >> 1][q.kc & 1], st.c0);
         st.c1 = mfma(a, st.H1[q.kc >> 1][q.kc & 1], st.c1);
       }
-      if constexpr (q.kc == 4 && q.mb + 1 < MB)
+      if constexpr (q.kc == KC2 / 2 && q.mb + 1 < MB)
         st.bias = *(const f32x16 *)(lds + OFF_B2 + ((q.mb + 1) * 2 + st.g) * 16);
-      if constexpr (q.kc == 7 && q.mb == MB - 1) {
+      if constexpr (q.kc == KC2 - 1 && q.mb == MB - 1) {
 #pragma unroll
         for (int j = 0; j < 8; ++j) st.w3r[q.mb & 1][j] = lds[OFF_W3 + (q.mb * 2 + st.g) * 8 + j];
       }
@@ -733,9 +662,14 @@ struct HeadBF16 {
       st.XB[0][kc] = XB[0][kc];
       st.XB[1][kc] = XB[1][kc];
     }
-    st.lb = lds + st.lane * 4;
-    st.frag[0] = frag_of<0>(st.lb);
-    st.frag[1] = frag_of<1>(st.lb);
+    st.lo[0] = st.lane * 4;
+    st.lo[1] = st.lo[0] + 16384;
+    st.lo[2] = st.lo[0] + 32768;
+    // opaque to the compiler, so it keeps the bases rather than forming
+    // each address beyond 64 KB anew
+    asm volatile("" : "+v"(st.lo[1]), "+v"(st.lo[2]));
+    st.frag[0] = frag_of<0>(lds, st.lo);
+    st.frag[1] = frag_of<1>(lds, st.lo);
     st.bias = *(const f32x16 *)(lds + OFF_B2 + st.g * 16);
 #pragma unroll
     for (int j = 0; j < 4; ++j) st.zacc[j] = 0.0f;
@@ -769,10 +703,8 @@ struct HeadBF16 {
   //                            dot with w3)
   // Only the features, the last epilogue and the tail stay exposed.
   __device__ static __forceinline__ float mlp(const float (&x)[IN], const uint32_t *lds) {
-    static_assert((MB >= 2 && 8 % KC2 == 0) || MB > 4, "the pipelined head splits 8 register pairs over the chunks");
-    if constexpr (MB > 4) {
-      return mlp_loop(x, lds);
-    } else if constexpr (MB == 4) {
+    static_assert(MB == 2 || MB == 4 || MB == 8, "hidden 64, 128 or 256");
+    if constexpr (MB == 4 || MB == 8) {
       u32x4 XB[2][KC1];
       pack_x(x, XB);
       return mlp4(XB, lds);
