@@ -369,3 +369,100 @@ def test_n_cu_above_limit_flagged():
     with pytest.raises(abi.KsError) as e:
         g.eval_kernels(wl, eta_one=True)
     assert e.value.status == abi.KS_ERANGE
+
+
+# ------------------------------------------------------------ maximum size --
+def _max_batch(n_steps=88_640, seed=5):
+    """A 64M-record batch of the 70B shape (80 layers x 9 kernels + 2 per
+    step = 722 records per step, as one C5 batch), built vectorized: decode
+    steps of U{1..64} requests with Pareto-like histories up to 131072.
+    Same record count, families and shapes as the benchmark's C5 batch."""
+    rng = np.random.default_rng(seed)
+    S, L, D, F, V = n_steps, 80, 8192, 28672, 32000
+    nreq = rng.integers(1, 65, S)
+    req_off = np.zeros(S + 1, np.int64)
+    req_off[1:] = np.cumsum(nreq)
+    req_h = np.minimum(131072, (512 * rng.uniform(size=int(req_off[-1])) ** (-1 / 1.2))).astype(np.uint32)
+    T = nreq.astype(np.uint32)                      # one query token per request
+    st = np.arange(S, dtype=np.uint32)
+    fams = []
+
+    def fam(f, per_step, m_of_step, n, k=None, a=None):
+        cnt = len(n)
+        k = [0] * cnt if k is None else k
+        a = [0] * cnt if a is None else a
+        fams.append((f, np.repeat(st, cnt), np.repeat(m_of_step, cnt),
+                     np.tile(np.asarray(n, np.uint32), S), np.tile(np.asarray(k, np.uint32), S),
+                     np.tile(np.asarray(a, np.uint32), S)))
+        assert per_step == cnt
+    gemm_n = [(64 + 16) * 128, D, 2 * F, D] * L
+    gemm_k = [D, D, D, F] * L
+    fam(gen.GEMM, 4 * L, T, gemm_n, gemm_k)
+    fam(gen.LM_HEAD, 1, nreq.astype(np.uint32), [V], [D])
+    fam(gen.ATTN_DECODE, L, np.zeros(S, np.uint32), [64] * L, [128] * L, [8] * L)
+    fam(gen.RMSNORM, 2 * L, T, [D] * (2 * L))
+    fam(gen.ROPE, L, T, [72] * L, [128] * L)
+    fam(gen.SILU_MUL, L, T, [F] * L)
+    fam(gen.EMBED, 1, T, [D])
+    fam_off = np.zeros(gen.NFAM + 1, np.int64)
+    cols = [[] for _ in range(5)]
+    for f in range(gen.NFAM):
+        for (ff, *c) in fams:
+            if ff == f:
+                for dst, src in zip(cols, c):
+                    dst.append(src)
+                fam_off[f + 1] += len(c[0])
+    fam_off = np.cumsum(fam_off)
+    step, m, n, k, a = (np.concatenate(c) for c in cols)
+    desc = gen.Desc(fam_off, step, m, n, k, a, np.zeros_like(a), req_off.astype(np.uint32),
+                    np.ones(int(req_off[-1]), np.uint32), req_h, np.zeros(0, np.uint32))
+    return gen.Workload("max", desc, steprec(S, layers=L, hidden=D, n_launch=0), gen.specs_datasheet(),
+                        gen.make_heads(32, 256, "bf16"), gen.HostConsts())
+
+
+def _sub_desc(d, rows):
+    """The records `rows` (sorted) of d, with d's request lists: the oracle
+    then prices only those records."""
+    fam = d.family()[rows]
+    fam_off = np.zeros(gen.NFAM + 1, np.int64)
+    fam_off[1:] = np.cumsum(np.bincount(fam, minlength=gen.NFAM))
+    return gen.Desc(fam_off, d.step[rows], d.m[rows], d.n[rows], d.k[rows], d.a[rows], d.b[rows],
+                    d.req_off, d.req_q, d.req_h, d.expert_rows, d.elem_bytes)
+
+
+def test_max_size_batch_sampled():
+    """One 64M-record batch (the largest single call of the C5 workload), bf16
+    32-256 heads and eta = 1: sampled records and steps against the oracle."""
+    import torch
+    wl = _max_batch()
+    d = wl.desc
+    assert d.n_rows == 88_640 * 722
+    rng = np.random.default_rng(3)
+    steps = np.unique(np.concatenate([[0, d.n_steps - 1], rng.integers(0, d.n_steps, 5)]))
+    rows = np.nonzero(np.isin(d.step, steps))[0]
+    rows_t = torch.as_tensor(rows, device="cuda")
+    for eta_one in (False, True):
+        di = abi.DeviceInputs(wl)
+        heads = di.make_heads("bf16", 32, 256, abi.KS_ETA_ONE if eta_one else abi.KS_ETA_MLP)
+        so_t, so = abi.step_outputs(d.n_steps, di.n_specs)
+        ko_t, ko = abi.kernel_outputs(d.n_rows, di.n_specs, counts=False)
+        abi.ks_eval_steps(di.desc, di.steps, di.specs_ptr, di.n_specs, heads, di.host, so, ko,
+                          di.ws_ptr, di.ws_bytes, abi.current_stream())
+        torch.cuda.synchronize()
+        abi.ks_device_status(di.ws_ptr, di.ws_bytes, abi.current_stream())
+        gpu = {key: ko_t[key][:, rows_t].cpu().numpy() for key in ("t_roof", "eta", "t_kernel")}
+        body = so_t["t_body"].cpu().numpy()[:, steps]
+        del di, ko_t, so_t
+        torch.cuda.empty_cache()
+        ref = o.eval_kernels(_sub_desc(d, rows), wl.specs, None if eta_one else wl.heads, eta_one=eta_one)
+        assert g.rel_err(gpu["t_roof"], ref["t_roof"]).max() <= REL
+        if eta_one:
+            assert (gpu["eta"] == 1.0).all()
+            assert g.rel_err(gpu["t_kernel"], ref["t"]).max() <= REL
+        else:
+            assert g.rel_err(gpu["eta"], ref["eta"]).max() <= REL_BF16
+        t_ge = np.maximum(ref["t_roof"] * gpu["eta"], wl.specs["t0"][:, None])
+        assert g.rel_err(gpu["t_kernel"], t_ge).max() <= REL
+        for s in range(wl.n_specs):
+            ref_body = np.bincount(d.step[rows], weights=t_ge[s], minlength=d.n_steps)[steps]
+            assert g.rel_err(body[s], ref_body).max() <= REL
