@@ -278,6 +278,20 @@ def head_forward(x, w1, w2, b2, w3, b3, emulate_bf16=False):
     return r(h2) @ w3 + b3
 
 
+def bounded_eta(x16, W, g, a):
+    """The bounded analytical head (Sec. 5.3, "A diverse, low-capacity head
+    family", and the efficiency-factor figure): utilization gamma - alpha/W
+    rising with the wave count W toward its peak gamma, eta its reciprocal.
+    Reading: gamma(x) = sigma(g . x) and alpha(x) = gamma(x) sigma(a . x),
+    so 0 < alpha < gamma < 1 and the utilization lies in (0, 1) for W >= 1;
+    a record without blocks (W = 0) counts as one wave."""
+    x16 = np.asarray(x16, np.float64)
+    gamma = 1.0 / (1.0 + np.exp(-(x16 @ g)))
+    alpha = gamma / (1.0 + np.exp(-(x16 @ a)))
+    w = np.maximum(np.asarray(W, np.float64), 1.0)
+    return 1.0 / (gamma - alpha / w)
+
+
 def eta_from_z(z):
     """sigma = 1/(1 + e^-z) in (0, 1]; eta = 1/sigma = 1 + e^-z >= 1."""
     return 1.0 + np.exp(-z)
@@ -304,10 +318,12 @@ def spec_at(specs, s):
 
 
 def eval_kernels(desc, specs, heads=None, eta_one=False, emulate_bf16=None,
-                 spec_ids=None, rows=None, keep_features=False):
+                 spec_ids=None, rows=None, keep_features=False, bounded=None):
     """Per-kernel latency model for every (spec, record) pair.
 
     heads: a ``workload.gen.Heads``; eta_one forces eta = 1 (pure roofline).
+    bounded: a ``workload.gen.Bounded``; the families in its mask take eta
+    from the bounded analytical head instead (of the MLP or of eta = 1).
     emulate_bf16 defaults to True for bf16 heads.  spec_ids / rows restrict
     the evaluation to a subset (counts are still exact per record).
     keep_features also returns the feature vectors ("x").
@@ -328,6 +344,8 @@ def eval_kernels(desc, specs, heads=None, eta_one=False, emulate_bf16=None,
     for si, s in enumerate(spec_ids):
         sp = spec_at(specs, s)
         rf = roofline(sub["F"], sub["Bt"], sub["B"], sp)
+        mask = bounded.mask if bounded is not None else 0
+        on_b = ((mask >> fam) & 1).astype(bool)
         if eta_one:
             z = np.full(len(rows), np.inf)
             eta = np.ones(len(rows))
@@ -336,11 +354,17 @@ def eval_kernels(desc, specs, heads=None, eta_one=False, emulate_bf16=None,
             if keep_features:
                 out["x"][si] = x
             z = np.zeros(len(rows))
-            for f in np.unique(fam):
+            for f in np.unique(fam[~on_b]):
                 sel = fam == f
                 z[sel] = head_forward(x[sel], heads.w1[f], heads.w2[f], heads.b2[f],
                                       heads.w3[f], heads.b3[f], emulate_bf16)
             eta = eta_from_z(z)
+        if on_b.any():
+            x16 = features(sub, desc.n[rows], effective_k(desc, rows), rf, sp, 16)
+            for f in np.unique(fam[on_b]):
+                sel = fam == f
+                eta[sel] = bounded_eta(x16[sel], rf["W"][sel], bounded.g[f], bounded.a[f])
+                z[sel] = -np.log(eta[sel] - 1.0)
         out["t_roof"][si] = rf["t_roof"]
         out["t_comp"][si] = rf["t_comp"]
         out["t_mem"][si] = rf["t_mem"]
@@ -379,12 +403,12 @@ def step_assembly(t_gpu, n_launch, c_disp, ell, c_ovl, c_tail):
 
 
 def eval_steps(desc, steprec, specs, host, heads=None, eta_one=False,
-               emulate_bf16=None, spec_ids=None, kern=None):
+               emulate_bf16=None, spec_ids=None, kern=None, bounded=None):
     """Per (spec, step): t_body, t_comm, t_gpu, t_step.  Every step's records
     must be present in desc (the body sums them).  ``kern`` may pass a result
     of eval_kernels over all rows to reuse."""
     if kern is None:
-        kern = eval_kernels(desc, specs, heads, eta_one, emulate_bf16, spec_ids)
+        kern = eval_kernels(desc, specs, heads, eta_one, emulate_bf16, spec_ids, bounded=bounded)
     n_steps = desc.n_steps
     spec_ids = list(range(len(specs["peak_flops"]))) if spec_ids is None else list(spec_ids)
     tokens = attention_work(desc.req_off, desc.req_q, desc.req_h)["Q"].astype(np.float64)

@@ -331,3 +331,64 @@ def test_metrics_appendix():
     assert metrics.percentile_nearest_rank(e, 50) == 3      # k = ceil(2.5) = 3
     assert metrics.percentile_nearest_rank(e, 90) == 5      # k = ceil(4.5) = 5
     assert metrics.percentile_nearest_rank(e, 20) == 1      # k = 1
+
+
+# ---------------------------------------- bounded analytical head (Sec. 5.3) --
+def test_bounded_head_zero_weights_closed_form():
+    """g = a = 0: gamma = 1/2, alpha = 1/4, so eta = 1/(1/2 - 1/(4W)): 4 at
+    one wave, 8/3 at two, toward 2 (= 1/gamma) as the waves grow; a record
+    without blocks counts as one wave."""
+    x = np.random.default_rng(0).normal(size=(4, 16))
+    z = np.zeros(16)
+    eta = o.bounded_eta(x, np.array([1, 2, 4, 0]), z, z)
+    np.testing.assert_allclose(eta, [4.0, 8.0 / 3.0, 1.0 / (0.5 - 1.0 / 16), 4.0], rtol=1e-15)
+    assert abs(o.bounded_eta(x[:1], np.array([10 ** 12]), z, z)[0] - 2.0) < 1e-11
+
+
+def test_bounded_head_hand_example():
+    """Only the constant feature x15 = 1 and g15 = ln 3: gamma = 3/4; a = 0:
+    alpha = 3/8; at W = 3 the utilization is 3/4 - 1/8 = 5/8, eta = 1.6."""
+    x = np.zeros((1, 16))
+    x[0, 15] = 1.0
+    g = np.zeros(16)
+    g[15] = math.log(3.0)
+    eta = o.bounded_eta(x, np.array([3]), g, np.zeros(16))
+    assert abs(eta[0] - 1.6) < 1e-15
+
+
+def test_bounded_head_monotone_and_bounded():
+    """Random heads: eta >= 1 / gamma > 1, and eta falls as the wave count
+    grows (the monotone wave-quantization prior the form imposes)."""
+    rng = np.random.default_rng(5)
+    x = rng.normal(size=(200, 16))
+    g, a = rng.normal(size=16), rng.normal(size=16)
+    gamma = 1.0 / (1.0 + np.exp(-(x @ g)))
+    prev = None
+    for w in (1, 2, 3, 7, 100, 10 ** 6):
+        eta = o.bounded_eta(x, np.full(200, w), g, a)
+        assert (eta >= 1.0 / gamma - 1e-12).all() and (eta > 1.0).all()
+        if prev is not None:
+            assert (eta < prev).all()
+        prev = eta
+
+
+def test_bounded_mask_selects_per_family():
+    """Families in the mask take the bounded head, the others keep theirs
+    (the MLP, or eta = 1), bit for bit."""
+    wl = gen.config1(0, 30)
+    bd = gen.make_bounded(gen.BOUNDED_MIXED)
+    fam = wl.desc.family()
+    on = ((gen.BOUNDED_MIXED >> fam) & 1).astype(bool)
+    assert on.any() and (~on).any()
+    for eta_one in (False, True):
+        plain = o.eval_kernels(wl.desc, wl.specs, wl.heads, eta_one=eta_one)
+        mixed = o.eval_kernels(wl.desc, wl.specs, wl.heads, eta_one=eta_one, bounded=bd)
+        np.testing.assert_array_equal(mixed["eta"][:, ~on], plain["eta"][:, ~on])
+        np.testing.assert_array_equal(mixed["t_roof"], plain["t_roof"])
+        assert (mixed["eta"][:, on] > 1.0).all()
+        # zero-weight bounded heads on the same families: the closed form
+        zero = gen.Bounded(gen.BOUNDED_MIXED, np.zeros((gen.NFAM, 16)), np.zeros((gen.NFAM, 16)),
+                           np.zeros((gen.NFAM, 2, 16), np.float32))
+        z = o.eval_kernels(wl.desc, wl.specs, wl.heads, eta_one=eta_one, bounded=zero)
+        w = np.maximum(z["W"][:, on].astype(np.float64), 1.0)
+        np.testing.assert_allclose(z["eta"][:, on], 1.0 / (0.5 - 0.25 / w), rtol=1e-15)

@@ -490,6 +490,39 @@ def make_heads(in_dim: int, hidden: int, precision: str, seed: int = HEAD_SEED,
                  v["b3"], s)
 
 
+@dataclass
+class Bounded:
+    """Per-family bounded analytical heads (the form NeuSight uses, kept by
+    the paper as one admissible head): gamma and alpha are logistic-linear
+    in the 16 base features.  mask bit f: family f uses this head instead of
+    the MLP (or instead of eta = 1)."""
+    mask: int
+    g: np.ndarray              # float64 [NFAM, 16]  exact parameter values (fp32)
+    a: np.ndarray              # float64 [NFAM, 16]
+    storage: np.ndarray        # float32 [NFAM, 2, 16]: g then a
+
+
+BOUNDED_SEED = HEAD_SEED + 50
+
+
+def make_bounded(mask: int, seed: int = BOUNDED_SEED, std: float = 0.5) -> Bounded:
+    """Family f draws g then a (16 each) from PCG64(seed + f), N(0, std^2),
+    rounded to float32 (the rounded values are the parameters)."""
+    st = np.zeros((NFAM, 2, 16), np.float32)
+    for f in range(NFAM):
+        rng = np.random.Generator(np.random.PCG64(seed + f))
+        st[f, 0] = rng.normal(0.0, std, 16).astype(np.float32)
+        st[f, 1] = rng.normal(0.0, std, 16).astype(np.float32)
+    v = st.astype(np.float64)
+    return Bounded(int(mask), v[:, 0].copy(), v[:, 1].copy(), np.ascontiguousarray(st))
+
+
+# the families whose head the mixed configuration switches to the bounded
+# form: compute-bound GEMMs and the smooth memory-bound writes (Sec. 5.3)
+BOUNDED_MIXED = (1 << GEMM) | (1 << LM_HEAD) | (1 << GROUPED_GEMM) | (1 << KV_WRITE) | (1 << EMBED)
+BOUNDED_ALL = (1 << NFAM) - 1
+
+
 @dataclass(frozen=True)
 class HostConsts:
     """Host terms of the step assembly (synthetic calibration values)."""
