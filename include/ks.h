@@ -123,11 +123,25 @@ enum { KS_ETA_MLP = 0, KS_ETA_ONE = 1 };
  * Element type float for KS_F32, bfloat16 bits (uint16) for KS_BF16.
  * z = w3 . relu(W2 relu(W1 x) + b2) + b3;  eta = 1 + exp(-z).
  * Supported: in_dim 16 or 32; hidden 64 or 128 (KS_F32), 64, 128 or 256
- * (KS_BF16).  mode KS_ETA_ONE ignores every other field (eta = 1).
+ * (KS_BF16).  mode KS_ETA_ONE: eta = 1 (the MLP fields are ignored).
+ *
+ * Per-family head selection (Sec. 5.3 picks each family's head from a pool):
+ * the families whose bit is set in bounded_mask (bit f = family f) take
+ * the bounded analytical head of Sec. 5.3 and its efficiency-factor figure
+ * instead of the MLP (mode KS_ETA_MLP) or of eta = 1 (mode KS_ETA_ONE):
+ *   gamma = sigma(g . x), alpha = gamma sigma(a . x), W' = max(W, 1),
+ *   eta = 1 / (gamma - alpha / W'),
+ * over the 16 base features x and the record's wave count W.  bounded:
+ * device float array [KS_NFAM][2][16], g then a per family (rows of other
+ * families are not read); NULL if bounded_mask is 0.  The MLP weights may be
+ * NULL when every family is in bounded_mask.  Computed in fp32.
  */
 typedef struct ks_heads {
   int32_t in_dim, hidden, precision, mode;
   const void *w1, *w2, *b2, *w3, *b3;
+  uint32_t bounded_mask;   /* bits 0 .. KS_NFAM-1 */
+  uint32_t reserved;
+  const float *bounded;
 } ks_heads;
 
 /* Per-step model record, device arrays [n_steps]. */

@@ -40,7 +40,8 @@ class ks_spec(C.Structure):
 
 class ks_heads(C.Structure):
     _fields_ = [("in_dim", C.c_int32), ("hidden", C.c_int32), ("precision", C.c_int32),
-                ("mode", C.c_int32), ("w1", P), ("w2", P), ("b2", P), ("w3", P), ("b3", P)]
+                ("mode", C.c_int32), ("w1", P), ("w2", P), ("b2", P), ("w3", P), ("b3", P),
+                ("bounded_mask", C.c_uint32), ("reserved", C.c_uint32), ("bounded", P)]
 
 
 class ks_steps(C.Structure):
@@ -232,13 +233,21 @@ class DeviceInputs:
         off = (-self.ws.data_ptr()) % 256
         self.ws_ptr = self.ws.data_ptr() + off
 
-    def make_heads(self, precision, in_dim, hidden, mode) -> ks_heads:
+    def make_heads(self, precision, in_dim, hidden, mode, bounded=None) -> ks_heads:
+        """bounded: a ``workload.gen.Bounded`` (its mask and parameters), or
+        None for no bounded-head family."""
         hd = ks_heads()
         hd.in_dim, hd.hidden = in_dim, hidden
         hd.precision = KS_BF16 if precision == "bf16" else KS_F32
         hd.mode = mode
         for name in ("w1", "w2", "b2", "w3", "b3"):
             setattr(hd, name, _ptr(self.heads_t[name]))
+        if bounded is not None and bounded.mask:
+            import torch
+            self.t["bounded"] = torch.from_numpy(np.ascontiguousarray(bounded.storage, np.float32)
+                                                 .reshape(-1).copy()).to(self.t["step"].device)
+            hd.bounded_mask = bounded.mask
+            hd.bounded = _ptr(self.t["bounded"])
         return hd
 
     @property

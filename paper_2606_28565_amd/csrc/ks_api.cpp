@@ -107,11 +107,16 @@ ks_status check_desc(const ks_desc *d) {
 
 ks_status head_kind(const ks_heads *h, int *kind) {
   if (!h) return fail(KS_EINVAL, "heads is NULL");
-  if (h->mode == KS_ETA_ONE) {
-    *kind = ks::kEtaOne;
+  const uint32_t all = (1u << KS_NFAM) - 1;
+  if (h->bounded_mask & ~all) return fail(KS_EINVAL, "heads.bounded_mask 0x%x has bits beyond the families",
+                                          h->bounded_mask);
+  if (h->bounded_mask && !h->bounded) return fail(KS_EINVAL, "heads.bounded is NULL with a nonzero mask");
+  if (h->mode != KS_ETA_ONE && h->mode != KS_ETA_MLP) return fail(KS_EINVAL, "heads.mode %d unknown", h->mode);
+  // no family left for the MLP: the head-less kernel (bounded families and eta = 1)
+  if (h->mode == KS_ETA_ONE || h->bounded_mask == all) {
+    *kind = h->bounded_mask ? ks::kBoundedOnly : ks::kEtaOne;
     return KS_OK;
   }
-  if (h->mode != KS_ETA_MLP) return fail(KS_EINVAL, "heads.mode %d unknown", h->mode);
   if (!h->w1 || !h->w2 || !h->b2 || !h->w3 || !h->b3) return fail(KS_EINVAL, "a head parameter pointer is NULL");
   const int in = h->in_dim, hid = h->hidden;
   if (in != 16 && in != 32) return fail(KS_EINVAL, "heads.in_dim %d not 16 or 32", in);
@@ -168,6 +173,8 @@ void fill_eval(ks::EvalParams &p, const ks_desc *d, const ks_spec *specs, int32_
     p.wgt_off[f] = t.wgt_off[f];
   }
   p.n_tiles = t.tile_off[KS_NFAM];
+  p.bounded_mask = h->bounded_mask;
+  p.bounded = h->bounded_mask ? h->bounded : nullptr;
   if (h->mode == KS_ETA_MLP) {
     p.w1 = h->w1;
     p.w2 = h->w2;

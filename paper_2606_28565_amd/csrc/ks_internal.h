@@ -29,6 +29,7 @@ enum HeadKind : int {
   kEtaOne = 0,
   kF32_16_64, kF32_16_128, kF32_32_64, kF32_32_128,
   kBF16_16_64, kBF16_16_128, kBF16_16_256, kBF16_32_64, kBF16_32_128, kBF16_32_256,
+  kBoundedOnly,   // no MLP: bounded-head families, eta = 1 for the rest
   kNumKinds
 };
 
@@ -60,6 +61,8 @@ struct EvalParams {
   int32_t n_tiles;
   // heads
   const void *w1, *w2, *b2, *w3, *b3;
+  uint32_t bounded_mask;       // families that take the bounded analytical head
+  const float *bounded;        // [KS_NFAM][2][16]: g then a
   // per-record / per-pair outputs (nullable)
   uint64_t *o_flops, *o_bytes, *o_blocks;
   float *o_troof, *o_eta, *o_t;

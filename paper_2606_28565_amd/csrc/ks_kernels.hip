@@ -424,6 +424,24 @@ struct SchedGrp {
 };
 #include "ks_sched.inc"
 
+// ------------------------------------------------------------ bounded head
+// The bounded analytical head (Sec. 5.3 and its efficiency-factor figure):
+// eta = 1 / (gamma - alpha / W'), gamma = sigma(g . x), alpha = gamma sigma(a . x),
+// W' = max(W, 1).  Written as (1 + e^-zg) W' (1 + E) / ((W' - 1) + W' E),
+// E = e^-za: every term is positive, so nothing cancels when alpha nears
+// gamma.  prm: g (16) then a (16), in LDS.
+__device__ __forceinline__ float bounded_eta(const float (&x)[16], float W, const float *prm) {
+  float zg = 0.0f, za = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    zg = fmaf(prm[i], x[i], zg);
+    za = fmaf(prm[16 + i], x[i], za);
+  }
+  const float w = fmaxf(W, 1.0f);
+  const float eg = __expf(-zg), ea = __expf(-za);
+  return (1.0f + eg) * (w * (1.0f + ea)) * rcpf((w - 1.0f) + w * ea);
+}
+
 // ------------------------------------------------------------ bf16 MFMA head
 // Orientation: hidden units are the MFMA rows (A = weights), the 64 records
 // of a wave are the columns (B = activations, two 32-column blocks), so the
@@ -931,6 +949,7 @@ struct HeadOne {
 // per SIMD, at most 256 registers per lane).
 template <int KIND> struct KindOf;
 template <> struct KindOf<kEtaOne> { using H = HeadOne; static constexpr int IN = 16; };
+template <> struct KindOf<kBoundedOnly> { using H = HeadOne; static constexpr int IN = 16; };
 template <> struct KindOf<kF32_16_64> { using H = HeadF32<16, 64>; static constexpr int IN = 16; };
 template <> struct KindOf<kF32_16_128> { using H = HeadF32<16, 128>; static constexpr int IN = 16; };
 template <> struct KindOf<kF32_32_64> { using H = HeadF32<32, 64>; static constexpr int IN = 32; };
@@ -1054,6 +1073,7 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
   using H = typename KindOf<KIND>::H;
   constexpr int IN = KindOf<KIND>::IN;
   __shared__ uint32_t lds[H::LDS_DW];
+  __shared__ float bnd_lds[32];   // the bounded head of the staged family: g then a
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int n_wgt = p.wgt_off[KS_NFAM];
   int staged = -1;
@@ -1072,10 +1092,16 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
       fn = load_fields(p, tn, lane);
     }
     const int fam = tc.fam;
-    if constexpr (H::kMlp) {
+    // this family takes the bounded head (the plain eta = 1 stream has none)
+    const bool bnd = KIND != kEtaOne && ((p.bounded_mask >> fam) & 1u);
+    if (H::kMlp || (KIND != kEtaOne && p.bounded_mask)) {
       if (fam != staged) {
         __syncthreads();
-        H::stage(lds, fam, p);
+        if (bnd) {
+          if (threadIdx.x < 32) bnd_lds[threadIdx.x] = p.bounded[fam * 32 + threadIdx.x];
+        } else {
+          if constexpr (H::kMlp) H::stage(lds, fam, p);
+        }
         __syncthreads();
         staged = fam;
       }
@@ -1088,7 +1114,7 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
     uint32_t bad = 0;
     if ((int64_t)fc.st >= p.n_steps) bad |= kErrStep;
     RowC rc;
-    if (!H::kMlp && !p.o_flops && !p.o_bytes && !p.o_blocks) {
+    if (!H::kMlp && !bnd && !p.o_flops && !p.o_bytes && !p.o_blocks) {
       const CntF cf = record_counts_f(fam, fc.m, fc.n, fc.k, fc.a, fc.b, fc.st, p, bad);
       rc.B = cf.B;
       rc.Ff = cf.F;
@@ -1145,11 +1171,17 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
       const SpecC sc = spec_at(p.spec_c, s);
       const Roof o = small ? roofline<true>(rc, sc) : roofline<false>(rc, sc);
       float eta = 1.0f;
-      if constexpr (H::kMlp) {
-        float x[IN];
-        features<IN>(rc, sc, o, x);
-        const float z = H::mlp(x, lds);
-        eta = 1.0f + __expf(-z);
+      if (bnd) {
+        float x[16];
+        features<16>(rc, sc, o, x);
+        eta = bounded_eta(x, o.W, bnd_lds);
+      } else {
+        if constexpr (H::kMlp) {
+          float x[IN];
+          features<IN>(rc, sc, o, x);
+          const float z = H::mlp(x, lds);
+          eta = 1.0f + __expf(-z);
+        }
       }
       const float t = fmaxf(o.t_roof * eta, sc.t0);
       if (valid) {
@@ -1320,6 +1352,7 @@ hipError_t launch_eval(int kind, const EvalParams &p, hipStream_t s) {
   if (p.wgt_off[KS_NFAM] == 0) return hipSuccess;
   switch (kind) {
     case kEtaOne: return launch_kind<kEtaOne>(p, s);
+    case kBoundedOnly: return launch_kind<kBoundedOnly>(p, s);
     case kF32_16_64: return launch_kind<kF32_16_64>(p, s);
     case kF32_16_128: return launch_kind<kF32_16_128>(p, s);
     case kF32_32_64: return launch_kind<kF32_32_64>(p, s);

@@ -107,7 +107,12 @@ def test_bad_specs_heads_workspace_rejected_on_host():
                  abi.ks_heads(16, 96, abi.KS_BF16, abi.KS_ETA_MLP, 1, 1, 1, 1, 1),
                  abi.ks_heads(16, 64, 7, abi.KS_ETA_MLP, 1, 1, 1, 1, 1),
                  abi.ks_heads(16, 64, abi.KS_F32, abi.KS_ETA_MLP, 1, None, 1, 1, 1),
-                 abi.ks_heads(16, 64, abi.KS_F32, 5)]
+                 abi.ks_heads(16, 64, abi.KS_F32, 5),
+                 # bounded-head mask beyond the families, or without parameters
+                 abi.ks_heads(16, 64, abi.KS_F32, abi.KS_ETA_ONE, bounded_mask=1 << 10, bounded=0x1000),
+                 abi.ks_heads(16, 64, abi.KS_F32, abi.KS_ETA_ONE, bounded_mask=3, bounded=None),
+                 # MLP mode with a family left for the MLP but no MLP weights
+                 abi.ks_heads(16, 64, abi.KS_F32, abi.KS_ETA_MLP, bounded_mask=3, bounded=0x1000)]
     for h in bad_heads:
         assert _call_eval(d, heads=h) == abi.KS_EINVAL, abi.ks_last_error()
     assert abi.load().ks_eval_kernels(C.byref(d), 0x2000, 1, C.byref(abi.ks_heads(16, 64, 0, 1)),

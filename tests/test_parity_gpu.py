@@ -466,3 +466,54 @@ def test_max_size_batch_sampled():
         for s in range(wl.n_specs):
             ref_body = np.bincount(d.step[rows], weights=t_ge[s], minlength=d.n_steps)[steps]
             assert g.rel_err(body[s], ref_body).max() <= REL
+
+
+# -------------------------------------------------- bounded analytical head --
+def _bounded_case(wl, bd, eta_one=False, n_specs=None, null_mlp=False):
+    """Families in bd.mask: fp32 bounded head at 1e-5; the others keep the
+    MLP bar of their precision (or eta = 1 exactly)."""
+    n_specs = n_specs or wl.n_specs
+    heads = None if eta_one else wl.heads
+    ref = o.eval_kernels(wl.desc, wl.specs, heads, eta_one=eta_one, spec_ids=range(n_specs), bounded=bd)
+    gpu = g.eval_steps(wl, eta_one=eta_one, n_specs=n_specs, bounded=bd, null_mlp=null_mlp)
+    c = ref["counts"]
+    np.testing.assert_array_equal(gpu["flops"], c["F"])
+    assert g.rel_err(gpu["t_roof"], ref["t_roof"]).max() <= REL
+    on = ((bd.mask >> wl.desc.family()) & 1).astype(bool)
+    assert g.rel_err(gpu["eta"][:, on], ref["eta"][:, on]).max() <= REL
+    assert g.rel_err(gpu["t_kernel"][:, on], ref["t"][:, on]).max() <= REL
+    bf16 = not eta_one and wl.heads.precision == "bf16"
+    if (~on).any():
+        tol = REL_BF16 if bf16 else REL
+        assert g.rel_err(gpu["eta"][:, ~on], ref["eta"][:, ~on]).max() <= tol
+    t0 = wl.specs["t0"][:n_specs, None]
+    assert g.rel_err(gpu["t_kernel"], np.maximum(ref["t_roof"] * gpu["eta"].astype(np.float64), t0)).max() <= REL
+    rs = o.eval_steps(wl.desc, wl.steps, wl.specs, wl.host, heads, eta_one=eta_one,
+                      spec_ids=range(n_specs), kern=ref)
+    _check_steps(wl, gpu, rs, bf16=bf16 and (~on).any(), n_specs=n_specs)
+    _check_steps(wl, gpu, _steps_given_eta(wl, gpu, ref, n_specs), bf16=False, n_specs=n_specs)
+
+
+def test_bounded_mixed_with_bf16_mlp():
+    _bounded_case(gen.config4(n_specs=12, grid_steps=20, c1_steps=30), gen.make_bounded(gen.BOUNDED_MIXED))
+
+
+def test_bounded_mixed_with_fp32_mlp_and_moe():
+    _bounded_case(gen.config1(0, 60), gen.make_bounded(gen.BOUNDED_MIXED))
+    _bounded_case(gen.config3(0, 20), gen.make_bounded(gen.BOUNDED_MIXED | (1 << gen.ATTN_DECODE)))
+
+
+def test_bounded_only():
+    """Every family bounded: through eta = 1 mode, and through MLP mode with
+    NULL MLP weights (both run the head-less kernel)."""
+    wl = gen.config1(0, 60)
+    bd = gen.make_bounded(gen.BOUNDED_ALL)
+    _bounded_case(wl, bd, eta_one=True)
+    _bounded_case(wl, bd, null_mlp=True)
+    # some families bounded, the rest at eta = 1
+    _bounded_case(wl, gen.make_bounded(gen.BOUNDED_MIXED), eta_one=True)
+
+
+def test_bounded_with_block_counts_around_2_23():
+    wl = _block_count_workload(heads=gen.make_heads(32, 256, "bf16"))
+    _bounded_case(wl, gen.make_bounded(gen.BOUNDED_ALL ^ (1 << gen.GEMM)))
