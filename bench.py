@@ -114,7 +114,7 @@ def head_flops_per_pair(in_dim: int, hidden: int) -> int:
     return 2 * (in_dim * hidden + hidden * hidden + hidden)
 
 
-def cpu_baseline(wl, sample: dict, eta_one: bool, threads: int):
+def cpu_baseline(wl, sample: dict, eta_one: bool, threads: int, bounded=None):
     """The oracle as it stands, on a bounded sample of the same workload:
     the first sample["specs"] spec vectors and, if sample["steps"] is set,
     only the records of the first sample["steps"] steps."""
@@ -128,7 +128,7 @@ def cpu_baseline(wl, sample: dict, eta_one: bool, threads: int):
     with threadpool_limits(limits=threads):
         t = time.perf_counter()
         k = o.eval_kernels(wl.desc, wl.specs, None if eta_one else wl.heads, eta_one=eta_one,
-                           spec_ids=spec_ids, rows=rows)
+                           spec_ids=spec_ids, rows=rows, bounded=bounded)
         if rows is None:
             o.eval_steps(wl.desc, wl.steps, wl.specs, wl.host, spec_ids=spec_ids, kern=k)
         dt = time.perf_counter() - t
@@ -148,6 +148,9 @@ def main() -> int:
     ap.add_argument("--workload", default="c4", choices=["c4", "c1", "c5-batch"])
     ap.add_argument("--eta-one", action="store_true", help="eta = 1 (pure roofline) mode")
     ap.add_argument("--per-pair", action="store_true", help="also write per-pair t_roof/eta/t_kernel")
+    ap.add_argument("--bounded", default="none", choices=["none", "mixed", "all"],
+                    help="families on the bounded analytical head: none; the GEMMs, embedding and "
+                         "KV writes (mixed, the rest on the MLP or eta = 1); or all")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -175,9 +178,12 @@ def main() -> int:
 
     print(f"[bench] generating workload {args.workload}", file=sys.stderr, flush=True)
     wl, wdesc, sample = _workload(args.workload)
+    from workload import gen
+    bmask = {"none": 0, "mixed": gen.BOUNDED_MIXED, "all": gen.BOUNDED_ALL}[args.bounded]
+    bounded = gen.make_bounded(bmask) if bmask else None
     di = abi.DeviceInputs(wl)
     heads = di.make_heads(wl.heads.precision, wl.heads.in_dim, wl.heads.hidden,
-                          abi.KS_ETA_ONE if args.eta_one else abi.KS_ETA_MLP)
+                          abi.KS_ETA_ONE if args.eta_one else abi.KS_ETA_MLP, bounded)
     so_t, so = abi.step_outputs(wl.desc.n_steps, di.n_specs)
     if args.per_pair:
         ko_t, ko = abi.kernel_outputs(wl.desc.n_rows, di.n_specs, counts=False)
@@ -210,14 +216,17 @@ def main() -> int:
     pairs = wl.desc.n_rows * di.n_specs
     value = pairs / (ms * 1e-3)
     step_evals = wl.desc.n_steps * di.n_specs / (ms * 1e-3)
-    if args.eta_one:
+    # records on the MLP: the families outside the bounded mask
+    import numpy as np
+    on_mlp = ((bmask >> wl.desc.family()) & 1) == 0
+    if args.eta_one or bmask == gen.BOUNDED_ALL:
         alg = stream_bytes(wl, di.n_specs)
         bound, unit, peak = "hbm", "GB/s", PEAK["hbm"] / 1e9
         achieved = alg / (ms * 1e-3) / 1e9
         dtype = "f32"
     else:
         per_pair = head_flops_per_pair(wl.heads.in_dim, wl.heads.hidden)
-        alg = float(pairs) * per_pair
+        alg = float(int(np.count_nonzero(on_mlp)) * di.n_specs) * per_pair
         bf16 = wl.heads.precision == "bf16"
         bound, unit = "mfma", "TFLOP/s"
         peak = (PEAK["bf16"] if bf16 else PEAK["f32"]) / 1e12
@@ -232,12 +241,14 @@ def main() -> int:
         "config": {"workload": wdesc, "records": wl.desc.n_rows, "spec_vectors": di.n_specs,
                    "serving_steps": wl.desc.n_steps, "predictions_per_step": pairs,
                    "head": ("eta=1" if args.eta_one else
-                            f"{wl.heads.precision} {wl.heads.in_dim}-{wl.heads.hidden}-{wl.heads.hidden}-1"),
+                            f"{wl.heads.precision} {wl.heads.in_dim}-{wl.heads.hidden}-{wl.heads.hidden}-1")
+                           + ("" if not bmask else f"; bounded head on families 0x{bmask:03x}"),
                    "per_pair_outputs": bool(args.per_pair)},
         "step_evals_per_s": step_evals,
         "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
                      "frac": achieved / peak,
-                     "traffic": recorded_traffic(f"{args.workload}{'-eta1' if args.eta_one else ''}"),
+                     "traffic": (recorded_traffic(f"{args.workload}{'-eta1' if args.eta_one else ''}")
+                                 if not bmask else None),
                      "note": "achieved = algorithmic work of the evaluation kernel per call "
                              "(FLOPs of the head, or the bytes the model reads and writes) / HIP-event "
                              "time of the whole call (all of its kernels)"},
@@ -245,7 +256,7 @@ def main() -> int:
     if not args.no_cpu_baseline:
         threads = args.cpu_threads or min(16, os.cpu_count() or 1)
         print(f"[bench] cpu baseline: oracle on {sample}, {threads} threads", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(wl, sample, args.eta_one, threads)
+        out["cpu_baseline"] = cpu_baseline(wl, sample, args.eta_one, threads, bounded)
         try:
             model = subprocess.run(["lscpu"], capture_output=True, text=True).stdout
             model = [l.split(":", 1)[1].strip() for l in model.splitlines() if l.startswith("Model name")]
