@@ -19,6 +19,11 @@ What it computes, and where the paper states it (KernelSight-LM):
   "Per-family heads on dimensionless features"); its output is a
   utilization sigma in (0, 1] and the efficiency factor is eta = 1/sigma >= 1
   (Sec. 5.3, Fig. "efficiency factor" caption);
+* per family, instead of that head, the bounded analytical head
+  eta = 1/(gamma - alpha/W) (Sec. 5.3, the efficiency-factor figure);
+* Tier B (Sec. 5.5): eta interpolated over a grid of measured values in
+  three feature coordinates where the query lies in the measured region,
+  the family's other head elsewhere ("density-routed");
 * t = max(t_roof eta, t0), the launch floor applied after eta (Eq. 2);
 * per-step body: the sum of the step's kernels (Sec. 5.7), which with one
   record per dispatched kernel equals L t_layer + t_lm_head + t_embed;
@@ -292,6 +297,36 @@ def bounded_eta(x16, W, g, a):
     return 1.0 / (gamma - alpha / w)
 
 
+def grid_eta(x16, grid, f):
+    """Tier B (Sec. 5.5, "Tier B: Target-Measured Prediction"): eta
+    interpolated over a grid of measured values in feature coordinates.
+    Reading: a regular grid over three of the base features, multilinear
+    interpolation of eta in the cell holding the query.  The query is routed
+    to the grid only inside the grid's box and only if all eight corners of
+    its cell were measured (NaN marks a missing node): the "dense interior"
+    of the measured points.  Returns (eta, routed); where routed is False
+    the family's learned head applies."""
+    x16 = np.asarray(x16, np.float64)
+    lo, hi, n = np.asarray(grid.lo), np.asarray(grid.hi), np.asarray(grid.n)
+    c = x16[:, list(grid.axes)]
+    t = (c - lo) / (hi - lo) * (n - 1)                       # node coordinates
+    inside = np.all((t >= 0.0) & (t <= n - 1), axis=1)
+    i = np.clip(np.floor(t), 0, n - 2).astype(np.int64)
+    fr = t - i
+    v = grid.values[f].astype(np.float64)
+    eta = np.zeros(len(c))
+    known = np.ones(len(c), bool)
+    for corner in range(8):
+        b = [(corner >> d) & 1 for d in range(3)]
+        idx = tuple(np.clip(i[:, d] + b[d], 0, n[d] - 1) for d in range(3))
+        w = np.prod([fr[:, d] if b[d] else 1.0 - fr[:, d] for d in range(3)], axis=0)
+        val = v[idx]
+        known &= ~np.isnan(val)
+        eta += w * np.where(np.isnan(val), 0.0, val)
+    routed = inside & known
+    return np.where(routed, eta, np.nan), routed
+
+
 def eta_from_z(z):
     """sigma = 1/(1 + e^-z) in (0, 1]; eta = 1/sigma = 1 + e^-z >= 1."""
     return 1.0 + np.exp(-z)
@@ -318,12 +353,14 @@ def spec_at(specs, s):
 
 
 def eval_kernels(desc, specs, heads=None, eta_one=False, emulate_bf16=None,
-                 spec_ids=None, rows=None, keep_features=False, bounded=None):
+                 spec_ids=None, rows=None, keep_features=False, bounded=None, grid=None):
     """Per-kernel latency model for every (spec, record) pair.
 
     heads: a ``workload.gen.Heads``; eta_one forces eta = 1 (pure roofline).
     bounded: a ``workload.gen.Bounded``; the families in its mask take eta
     from the bounded analytical head instead (of the MLP or of eta = 1).
+    grid: a ``workload.gen.Grid`` (Tier B); for the families in its mask,
+    records routed to the grid take the interpolated eta ("routed" output).
     emulate_bf16 defaults to True for bf16 heads.  spec_ids / rows restrict
     the evaluation to a subset (counts are still exact per record).
     keep_features also returns the feature vectors ("x").
@@ -339,6 +376,7 @@ def eval_kernels(desc, specs, heads=None, eta_one=False, emulate_bf16=None,
     out = {key: np.zeros((len(spec_ids), len(rows))) for key in
            ("t_roof", "eta", "t", "z", "t_comp", "t_mem", "u")}
     out["W"] = np.zeros((len(spec_ids), len(rows)), U64)
+    out["routed"] = np.zeros((len(spec_ids), len(rows)), bool)
     if keep_features and not eta_one:
         out["x"] = np.zeros((len(spec_ids), len(rows), heads.in_dim))
     for si, s in enumerate(spec_ids):
@@ -365,6 +403,16 @@ def eval_kernels(desc, specs, heads=None, eta_one=False, emulate_bf16=None,
                 sel = fam == f
                 eta[sel] = bounded_eta(x16[sel], rf["W"][sel], bounded.g[f], bounded.a[f])
                 z[sel] = -np.log(eta[sel] - 1.0)
+        gmask = grid.mask if grid is not None else 0
+        on_g = ((gmask >> fam) & 1).astype(bool)
+        if on_g.any():
+            x16 = features(sub, desc.n[rows], effective_k(desc, rows), rf, sp, 16)
+            for f in np.unique(fam[on_g]):
+                sel = np.nonzero(fam == f)[0]
+                eg, routed = grid_eta(x16[sel], grid, f)
+                eta[sel[routed]] = eg[routed]
+                z[sel[routed]] = -np.log(np.maximum(eg[routed] - 1.0, 1e-300))
+                out["routed"][si, sel] = routed
         out["t_roof"][si] = rf["t_roof"]
         out["t_comp"][si] = rf["t_comp"]
         out["t_mem"][si] = rf["t_mem"]
@@ -403,12 +451,12 @@ def step_assembly(t_gpu, n_launch, c_disp, ell, c_ovl, c_tail):
 
 
 def eval_steps(desc, steprec, specs, host, heads=None, eta_one=False,
-               emulate_bf16=None, spec_ids=None, kern=None, bounded=None):
+               emulate_bf16=None, spec_ids=None, kern=None, bounded=None, grid=None):
     """Per (spec, step): t_body, t_comm, t_gpu, t_step.  Every step's records
     must be present in desc (the body sums them).  ``kern`` may pass a result
     of eval_kernels over all rows to reuse."""
     if kern is None:
-        kern = eval_kernels(desc, specs, heads, eta_one, emulate_bf16, spec_ids, bounded=bounded)
+        kern = eval_kernels(desc, specs, heads, eta_one, emulate_bf16, spec_ids, bounded=bounded, grid=grid)
     n_steps = desc.n_steps
     spec_ids = list(range(len(specs["peak_flops"]))) if spec_ids is None else list(spec_ids)
     tokens = attention_work(desc.req_off, desc.req_q, desc.req_h)["Q"].astype(np.float64)

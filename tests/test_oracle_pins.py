@@ -392,3 +392,134 @@ def test_bounded_mask_selects_per_family():
         z = o.eval_kernels(wl.desc, wl.specs, wl.heads, eta_one=eta_one, bounded=zero)
         w = np.maximum(z["W"][:, on].astype(np.float64), 1.0)
         np.testing.assert_allclose(z["eta"][:, on], 1.0 / (0.5 - 0.25 / w), rtol=1e-15)
+
+
+# ------------------------------------------ Tier B grid interpolation (Sec. 5.5) --
+def _grid(values, lo=(-1.0, 0.0, -0.5), hi=(0.5, 0.4, 0.7), axes=(1, 2, 6)):
+    v = np.asarray(values, np.float32)
+    full = np.broadcast_to(v, (gen.NFAM,) + v.shape).copy()
+    return gen.Grid(gen.GRID_ALL, axes, np.asarray(lo, np.float64), np.asarray(hi, np.float64),
+                    v.shape, full)
+
+
+def _coords_to_x16(c, axes=(1, 2, 6)):
+    x = np.random.default_rng(1).normal(size=(len(c), 16))
+    x[:, list(axes)] = c
+    return x
+
+
+def test_grid_reproduces_node_values():
+    """At a node every weight but one vanishes: the node's value."""
+    v = np.random.default_rng(2).uniform(1.0, 3.0, size=(4, 5, 3)).astype(np.float32)
+    gr = _grid(v)
+    idx = np.array(np.meshgrid(*[np.arange(s) for s in v.shape], indexing="ij")).reshape(3, -1).T
+    c = gr.lo + idx * (gr.hi - gr.lo) / (np.array(v.shape) - 1)
+    eta, routed = o.grid_eta(_coords_to_x16(c), gr, 0)
+    assert routed.all()
+    np.testing.assert_allclose(eta, v[tuple(idx.T)].astype(np.float64), rtol=1e-14)
+
+
+def test_grid_reproduces_multilinear_functions():
+    """Trilinear interpolation is exact for (a0 + b0 c0)(a1 + b1 c1)(a2 + b2 c2)
+    and for sums of such terms (here an affine function plus c0 c1 c2), at any
+    point of the box: a dropped weight or a swapped axis fails this."""
+    gr0 = _grid(np.zeros((6, 4, 5)))
+    n = np.array(gr0.n)
+    node = [np.linspace(gr0.lo[d], gr0.hi[d], n[d]) for d in range(3)]
+    C = np.meshgrid(*node, indexing="ij")
+
+    def f(c0, c1, c2):
+        return 1.5 + 0.7 * c0 - 0.3 * c1 + 0.2 * c2 + 0.9 * c0 * c1 * c2 + 0.4 * c0 * c2
+
+    vals = f(*C)
+    gr = gen.Grid(gen.GRID_ALL, gr0.axes, gr0.lo, gr0.hi, gr0.n,
+                  np.broadcast_to(vals, (gen.NFAM,) + vals.shape).copy())   # float64 nodes
+    rng = np.random.default_rng(3)
+    c = gr.lo + rng.uniform(size=(500, 3)) * (gr.hi - gr.lo)
+    eta, routed = o.grid_eta(_coords_to_x16(c), gr, 3)
+    assert routed.all()
+    np.testing.assert_allclose(eta, f(c[:, 0], c[:, 1], c[:, 2]), rtol=1e-13, atol=1e-13)
+
+
+def test_grid_matches_regular_grid_interpolator():
+    """Random node values with unmeasured (NaN) nodes against scipy's
+    RegularGridInterpolator: same values where routed, and routed exactly
+    where scipy's linear interpolation is not NaN (a NaN corner reaches the
+    result whatever its weight)."""
+    from scipy.interpolate import RegularGridInterpolator
+    rng = np.random.default_rng(4)
+    v = rng.uniform(1.0, 4.0, size=(7, 6, 8))
+    v[rng.uniform(size=v.shape) < 0.1] = np.nan
+    gr = gen.Grid(gen.GRID_ALL, (0, 3, 12), np.array([-0.6, 0.2, 0.1]), np.array([0.0, 1.0, 0.3]), v.shape,
+                  np.broadcast_to(v, (gen.NFAM,) + v.shape).copy())
+    node = [np.linspace(gr.lo[d], gr.hi[d], v.shape[d]) for d in range(3)]
+    ref = RegularGridInterpolator(node, v, method="linear", bounds_error=False, fill_value=np.nan)
+    c = gr.lo + rng.uniform(size=(4000, 3)) * (gr.hi - gr.lo)
+    eta, routed = o.grid_eta(_coords_to_x16(c, gr.axes), gr, 7)
+    r = ref(c)
+    np.testing.assert_array_equal(routed, ~np.isnan(r))
+    assert 0.2 < routed.mean() < 0.8
+    np.testing.assert_allclose(eta[routed], r[routed], rtol=1e-13)
+
+
+def test_grid_outside_box_or_unmeasured_falls_back():
+    """Outside the box, or in a cell with an unmeasured corner, nothing is
+    routed; one unmeasured node blocks exactly the (up to 8) cells around it."""
+    v = np.full((5, 5, 5), 2.0)
+    v[2, 2, 2] = np.nan
+    gr = _grid(v)
+    n = np.array(v.shape)
+    step = (gr.hi - gr.lo) / (n - 1)
+    # cell centres: blocked iff the cell touches node (2, 2, 2)
+    idx = np.array(np.meshgrid(*[np.arange(4)] * 3, indexing="ij")).reshape(3, -1).T
+    c = gr.lo + (idx + 0.5) * step
+    _, routed = o.grid_eta(_coords_to_x16(c), gr, 0)
+    blocked = np.all((idx == 1) | (idx == 2), axis=1)
+    np.testing.assert_array_equal(routed, ~blocked)
+    # just outside each face
+    for d in range(3):
+        for side in (-1, 1):
+            p = (gr.lo + gr.hi) / 2
+            p[d] = (gr.lo[d] if side < 0 else gr.hi[d]) + side * 1e-9
+            _, r = o.grid_eta(_coords_to_x16(p[None]), gr, 0)
+            assert not r[0]
+    # on the faces themselves: routed (the box is closed)
+    _, r = o.grid_eta(_coords_to_x16(np.array([gr.lo, gr.hi])), gr, 0)
+    assert r.all()
+
+
+def test_grid_routing_in_eval_kernels():
+    """Per family: routed records take the interpolated eta of their own
+    features, the rest keep the family's other head bit for bit (MLP, eta = 1
+    or the bounded head); routing does not depend on that other head; an
+    all-NaN grid routes nothing."""
+    wl = gen.config1(0, 30)
+    gr = gen.make_grid(gen.GRID_ALL ^ (1 << gen.GEMM))
+    fam = wl.desc.family()
+    res = []
+    for kw in ({}, {"eta_one": True}, {"bounded": gen.make_bounded(gen.BOUNDED_MIXED)}):
+        heads = None if kw.get("eta_one") else wl.heads
+        plain = o.eval_kernels(wl.desc, wl.specs, heads, **kw)
+        mixed = o.eval_kernels(wl.desc, wl.specs, heads, grid=gr, keep_features=not kw, **kw)
+        r = mixed["routed"]
+        assert r.any() and (~r).any() and not r[:, fam == gen.GEMM].any()
+        np.testing.assert_array_equal(mixed["eta"][~r], plain["eta"][~r])
+        np.testing.assert_array_equal(mixed["t_roof"], plain["t_roof"])
+        t0 = wl.specs["t0"][:, None]
+        np.testing.assert_array_equal(mixed["t"], np.maximum(mixed["t_roof"] * mixed["eta"], t0))
+        if not kw:
+            for s in range(wl.n_specs):
+                for f in np.unique(fam[r[s]]):
+                    sel = r[s] & (fam == f)
+                    e, rr = o.grid_eta(mixed["x"][s][sel][:, :16], gr, f)
+                    assert rr.all()
+                    np.testing.assert_array_equal(mixed["eta"][s, sel], e)
+        res.append(mixed)
+    for m in res[1:]:
+        np.testing.assert_array_equal(m["routed"], res[0]["routed"])
+        np.testing.assert_array_equal(m["eta"][m["routed"]], res[0]["eta"][m["routed"]])
+    empty = gen.Grid(gr.mask, gr.axes, gr.lo, gr.hi, gr.n, np.full_like(gr.values, np.nan))
+    a = o.eval_kernels(wl.desc, wl.specs, wl.heads, grid=empty)
+    b = o.eval_kernels(wl.desc, wl.specs, wl.heads)
+    assert not a["routed"].any()
+    np.testing.assert_array_equal(a["eta"], b["eta"])

@@ -523,6 +523,46 @@ BOUNDED_MIXED = (1 << GEMM) | (1 << LM_HEAD) | (1 << GROUPED_GEMM) | (1 << KV_WR
 BOUNDED_ALL = (1 << NFAM) - 1
 
 
+@dataclass
+class Grid:
+    """Tier-B measured efficiency grids (synthetic stand-ins): per family a
+    regular grid over three of the 16 base features, eta at each node, NaN
+    where the node was not measured.  mask bit f: family f has a grid."""
+    mask: int
+    axes: tuple                # three feature indices
+    lo: np.ndarray             # float64 [3]
+    hi: np.ndarray             # float64 [3]
+    n: tuple                   # nodes per axis
+    values: np.ndarray         # float32 [NFAM, n0, n1, n2]; the float32 values are the data
+
+
+GRID_SEED = HEAD_SEED + 60
+
+
+def make_grid(mask: int, axes=(1, 2, 6), lo=(-0.8, 0.0, -0.4), hi=(0.2, 0.4, 0.6), n=(8, 8, 8),
+              holes: float = 0.08, seed: int = GRID_SEED) -> Grid:
+    """A smooth efficiency surface over the grid's coordinates (c0, c1, c2),
+    eta = 1 + 0.6 sigma(3 c0 + 2) + 0.8 c1 + 0.3 cos(3 c2) + N(0, 0.02^2)
+    (kept >= 1), different per family by a seeded offset; a seeded fraction
+    `holes` of the nodes is left unmeasured (NaN)."""
+    lo, hi = np.asarray(lo, np.float64), np.asarray(hi, np.float64)
+    c = [np.linspace(lo[d], hi[d], n[d]) for d in range(3)]
+    C0, C1, C2 = np.meshgrid(*c, indexing="ij")
+    vals = np.zeros((NFAM,) + tuple(n), np.float32)
+    for f in range(NFAM):
+        rng = np.random.Generator(np.random.PCG64(seed + f))
+        off = rng.uniform(0.0, 0.5)
+        eta = (1.0 + off + 0.6 / (1.0 + np.exp(-(3.0 * C0 + 2.0))) + 0.8 * C1 + 0.3 * np.cos(3.0 * C2)
+               + rng.normal(0.0, 0.02, C0.shape))
+        eta = np.maximum(eta, 1.0)
+        eta[rng.uniform(size=C0.shape) < holes] = np.nan
+        vals[f] = eta.astype(np.float32)
+    return Grid(int(mask), tuple(axes), lo, hi, tuple(n), vals)
+
+
+GRID_ALL = (1 << NFAM) - 1
+
+
 @dataclass(frozen=True)
 class HostConsts:
     """Host terms of the step assembly (synthetic calibration values)."""
