@@ -135,13 +135,34 @@ enum { KS_ETA_MLP = 0, KS_ETA_ONE = 1 };
  * device float array [KS_NFAM][2][16], g then a per family (rows of other
  * families are not read); NULL if bounded_mask is 0.  The MLP weights may be
  * NULL when every family is in bounded_mask.  Computed in fp32.
+ *
+ * Tier B, density-routed measured grids (Sec. 5.5, "Tier B"): for the
+ * families whose bit is set in grid_mask, eta comes from a grid of measured
+ * values over three of the 16 base features, axis d taking feature
+ * grid_axis[d] (0 .. 14) on grid_n[d] >= 2 evenly spaced nodes from
+ * grid_lo[d] to grid_hi[d] (finite, lo < hi).  A query is routed to the
+ * grid when its coordinates lie in the closed box and the eight corners of
+ * its cell are all measured (not NaN); there eta is the trilinear
+ * interpolation of the corners.  Other queries of such a family take the
+ * family's other head (MLP, bounded head or eta = 1, as above).
+ * grid: device float array [KS_NFAM][n0][n1][n2], row-major, NaN for a node
+ * never measured (rows of families outside grid_mask are not read); NULL if
+ * grid_mask is 0.  n0 n1 n2 <= KS_GRID_MAX_NODES.  Computed in fp32: a query
+ * within rounding of a cell face next to an unmeasured node, or of the box,
+ * may be routed either way.
  */
+enum { KS_GRID_MAX_NODES = 2048 };
+
 typedef struct ks_heads {
   int32_t in_dim, hidden, precision, mode;
   const void *w1, *w2, *b2, *w3, *b3;
   uint32_t bounded_mask;   /* bits 0 .. KS_NFAM-1 */
-  uint32_t reserved;
+  uint32_t grid_mask;      /* bits 0 .. KS_NFAM-1 */
   const float *bounded;
+  int32_t grid_axis[3];
+  int32_t grid_n[3];
+  double grid_lo[3], grid_hi[3];
+  const float *grid;
 } ks_heads;
 
 /* Per-step model record, device arrays [n_steps]. */

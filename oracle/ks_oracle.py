@@ -360,7 +360,8 @@ def eval_kernels(desc, specs, heads=None, eta_one=False, emulate_bf16=None,
     bounded: a ``workload.gen.Bounded``; the families in its mask take eta
     from the bounded analytical head instead (of the MLP or of eta = 1).
     grid: a ``workload.gen.Grid`` (Tier B); for the families in its mask,
-    records routed to the grid take the interpolated eta ("routed" output).
+    records routed to the grid take the interpolated eta ("routed" output;
+    "x16": the base features of every pair when a grid is given).
     emulate_bf16 defaults to True for bf16 heads.  spec_ids / rows restrict
     the evaluation to a subset (counts are still exact per record).
     keep_features also returns the feature vectors ("x").
@@ -379,6 +380,8 @@ def eval_kernels(desc, specs, heads=None, eta_one=False, emulate_bf16=None,
     out["routed"] = np.zeros((len(spec_ids), len(rows)), bool)
     if keep_features and not eta_one:
         out["x"] = np.zeros((len(spec_ids), len(rows), heads.in_dim))
+    if grid is not None:
+        out["x16"] = np.zeros((len(spec_ids), len(rows), 16))
     for si, s in enumerate(spec_ids):
         sp = spec_at(specs, s)
         rf = roofline(sub["F"], sub["Bt"], sub["B"], sp)
@@ -405,8 +408,9 @@ def eval_kernels(desc, specs, heads=None, eta_one=False, emulate_bf16=None,
                 z[sel] = -np.log(eta[sel] - 1.0)
         gmask = grid.mask if grid is not None else 0
         on_g = ((gmask >> fam) & 1).astype(bool)
-        if on_g.any():
+        if grid is not None:
             x16 = features(sub, desc.n[rows], effective_k(desc, rows), rf, sp, 16)
+            out["x16"][si] = x16
             for f in np.unique(fam[on_g]):
                 sel = np.nonzero(fam == f)[0]
                 eg, routed = grid_eta(x16[sel], grid, f)

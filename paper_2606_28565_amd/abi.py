@@ -41,7 +41,9 @@ class ks_spec(C.Structure):
 class ks_heads(C.Structure):
     _fields_ = [("in_dim", C.c_int32), ("hidden", C.c_int32), ("precision", C.c_int32),
                 ("mode", C.c_int32), ("w1", P), ("w2", P), ("b2", P), ("w3", P), ("b3", P),
-                ("bounded_mask", C.c_uint32), ("reserved", C.c_uint32), ("bounded", P)]
+                ("bounded_mask", C.c_uint32), ("grid_mask", C.c_uint32), ("bounded", P),
+                ("grid_axis", C.c_int32 * 3), ("grid_n", C.c_int32 * 3),
+                ("grid_lo", C.c_double * 3), ("grid_hi", C.c_double * 3), ("grid", P)]
 
 
 class ks_steps(C.Structure):
@@ -233,9 +235,10 @@ class DeviceInputs:
         off = (-self.ws.data_ptr()) % 256
         self.ws_ptr = self.ws.data_ptr() + off
 
-    def make_heads(self, precision, in_dim, hidden, mode, bounded=None) -> ks_heads:
+    def make_heads(self, precision, in_dim, hidden, mode, bounded=None, grid=None) -> ks_heads:
         """bounded: a ``workload.gen.Bounded`` (its mask and parameters), or
-        None for no bounded-head family."""
+        None for no bounded-head family.  grid: a ``workload.gen.Grid``
+        (Tier B measured grids), or None."""
         hd = ks_heads()
         hd.in_dim, hd.hidden = in_dim, hidden
         hd.precision = KS_BF16 if precision == "bf16" else KS_F32
@@ -248,6 +251,17 @@ class DeviceInputs:
                                                  .reshape(-1).copy()).to(self.t["step"].device)
             hd.bounded_mask = bounded.mask
             hd.bounded = _ptr(self.t["bounded"])
+        if grid is not None and grid.mask:
+            import torch
+            self.t["grid"] = torch.from_numpy(np.ascontiguousarray(grid.values, np.float32)
+                                              .reshape(-1).copy()).to(self.t["step"].device)
+            hd.grid_mask = grid.mask
+            hd.grid = _ptr(self.t["grid"])
+            for d in range(3):
+                hd.grid_axis[d] = int(grid.axes[d])
+                hd.grid_n[d] = int(grid.n[d])
+                hd.grid_lo[d] = float(grid.lo[d])
+                hd.grid_hi[d] = float(grid.hi[d])
         return hd
 
     @property

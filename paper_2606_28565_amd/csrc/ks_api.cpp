@@ -2,6 +2,7 @@
 // workspace layout, the launch sequence and error reporting.
 #include <hip/hip_runtime_api.h>
 
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -112,9 +113,28 @@ ks_status head_kind(const ks_heads *h, int *kind) {
                                           h->bounded_mask);
   if (h->bounded_mask && !h->bounded) return fail(KS_EINVAL, "heads.bounded is NULL with a nonzero mask");
   if (h->mode != KS_ETA_ONE && h->mode != KS_ETA_MLP) return fail(KS_EINVAL, "heads.mode %d unknown", h->mode);
-  // no family left for the MLP: the head-less kernel (bounded families and eta = 1)
+  if (h->grid_mask & ~all) return fail(KS_EINVAL, "heads.grid_mask 0x%x has bits beyond the families", h->grid_mask);
+  if (h->grid_mask) {
+    if (!h->grid) return fail(KS_EINVAL, "heads.grid is NULL with a nonzero mask");
+    int64_t nodes = 1;
+    for (int d = 0; d < 3; ++d) {
+      if (h->grid_axis[d] < 0 || h->grid_axis[d] > 14)
+        return fail(KS_EINVAL, "heads.grid_axis[%d] = %d not a feature 0 .. 14", d, h->grid_axis[d]);
+      if (h->grid_n[d] < 2 || h->grid_n[d] > KS_GRID_MAX_NODES)
+        return fail(KS_EINVAL, "heads.grid_n[%d] = %d below 2 or above %d", d, h->grid_n[d], (int)KS_GRID_MAX_NODES);
+      nodes *= h->grid_n[d];
+      const double lo = h->grid_lo[d], hi = h->grid_hi[d];
+      const float scale = (float)((h->grid_n[d] - 1) / (hi - lo));
+      if (!std::isfinite((float)lo) || !std::isfinite((float)hi) || !(lo < hi) || !std::isfinite(scale))
+        return fail(KS_EINVAL, "heads.grid_lo/hi[%d] = %g, %g not finite with lo < hi", d, lo, hi);
+    }
+    if (nodes > KS_GRID_MAX_NODES)
+      return fail(KS_EINVAL, "heads grid of %lld nodes above %d", (long long)nodes, (int)KS_GRID_MAX_NODES);
+  }
+  // no family left for the MLP: the head-less kernel (bounded and grid
+  // families, eta = 1 for the rest)
   if (h->mode == KS_ETA_ONE || h->bounded_mask == all) {
-    *kind = h->bounded_mask ? ks::kBoundedOnly : ks::kEtaOne;
+    *kind = (h->bounded_mask | h->grid_mask) ? ks::kBoundedOnly : ks::kEtaOne;
     return KS_OK;
   }
   if (!h->w1 || !h->w2 || !h->b2 || !h->w3 || !h->b3) return fail(KS_EINVAL, "a head parameter pointer is NULL");
@@ -175,6 +195,16 @@ void fill_eval(ks::EvalParams &p, const ks_desc *d, const ks_spec *specs, int32_
   p.n_tiles = t.tile_off[KS_NFAM];
   p.bounded_mask = h->bounded_mask;
   p.bounded = h->bounded_mask ? h->bounded : nullptr;
+  p.grid_mask = h->grid_mask;
+  p.grid = h->grid_mask ? h->grid : nullptr;
+  p.grid_nodes = 0;
+  for (int a = 0; a < 3; ++a) {
+    p.grid_axis[a] = h->grid_mask ? h->grid_axis[a] : 0;
+    p.grid_n[a] = h->grid_mask ? h->grid_n[a] : 2;
+    p.grid_lo[a] = h->grid_mask ? (float)h->grid_lo[a] : 0.0f;
+    p.grid_scale[a] = h->grid_mask ? (float)((h->grid_n[a] - 1) / (h->grid_hi[a] - h->grid_lo[a])) : 0.0f;
+  }
+  if (h->grid_mask) p.grid_nodes = p.grid_n[0] * p.grid_n[1] * p.grid_n[2];
   if (h->mode == KS_ETA_MLP) {
     p.w1 = h->w1;
     p.w2 = h->w2;

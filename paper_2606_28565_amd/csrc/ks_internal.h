@@ -29,7 +29,7 @@ enum HeadKind : int {
   kEtaOne = 0,
   kF32_16_64, kF32_16_128, kF32_32_64, kF32_32_128,
   kBF16_16_64, kBF16_16_128, kBF16_16_256, kBF16_32_64, kBF16_32_128, kBF16_32_256,
-  kBoundedOnly,   // no MLP: bounded-head families, eta = 1 for the rest
+  kBoundedOnly,   // no MLP: bounded-head and grid families, eta = 1 for the rest
   kNumKinds
 };
 
@@ -63,6 +63,10 @@ struct EvalParams {
   const void *w1, *w2, *b2, *w3, *b3;
   uint32_t bounded_mask;       // families that take the bounded analytical head
   const float *bounded;        // [KS_NFAM][2][16]: g then a
+  uint32_t grid_mask;          // families with a measured eta grid (Tier B)
+  int32_t grid_axis[3], grid_n[3], grid_nodes;
+  float grid_lo[3], grid_scale[3];   // node coordinate (c - lo) * scale
+  const float *grid;           // [KS_NFAM][grid_nodes]
   // per-record / per-pair outputs (nullable)
   uint64_t *o_flops, *o_bytes, *o_blocks;
   float *o_troof, *o_eta, *o_t;

@@ -395,20 +395,34 @@ __device__ __forceinline__ Roof roofline(const RowC &r, const SpecC &s) {
 // the 16 dimensionless features (x[16 + i] = x[i]^2 for 32 inputs);
 // x1 = log2(AI / ridge) = log2(AI) + log2(BW / P), and the last-wave
 // occupancy B / (W N) is 1 / u
+__device__ __forceinline__ float feature(int i, const RowC &r, const SpecC &s, const Roof &o) {
+  switch (i) {
+    case 0: return r.x0;
+    case 1: return fmaxf(r.la + s.lr, -20.0f) * (1.0f / 16);
+    case 2: return log2f_fast(fmaf(r.Bf, s.rcp_n, 1.0f)) * (1.0f / 16);
+    case 3: return rcpf(o.u);
+    case 4: return log2f_fast(1.0f + o.W) * (1.0f / 16);
+    case 5: return fminf(1.0f, s.l2 * r.rcp_bt1);
+    case 6: return log2f_fast(fmaxf(o.t_roof * s.rcp_t0, 0x1p-20f)) * (1.0f / 16);
+    case 7: {
+      const float den = o.t_comp + o.t_mem;
+      return den > 0.0f ? o.t_comp * rcpf(den) : 0.0f;
+    }
+    case 8: return r.xs[0];
+    case 9: return r.xs[1];
+    case 10: return r.xs[2];
+    case 11: return r.xs[3];
+    case 12: return r.xs[4];
+    case 13: return r.xs[5];
+    case 14: return r.xs[6];
+    default: return 1.0f;
+  }
+}
+
 template <int IN>
 __device__ __forceinline__ void features(const RowC &r, const SpecC &s, const Roof &o, float (&x)[IN]) {
-  x[0] = r.x0;
-  x[1] = fmaxf(r.la + s.lr, -20.0f) * (1.0f / 16);
-  x[2] = log2f_fast(fmaf(r.Bf, s.rcp_n, 1.0f)) * (1.0f / 16);
-  x[3] = rcpf(o.u);
-  x[4] = log2f_fast(1.0f + o.W) * (1.0f / 16);
-  x[5] = fminf(1.0f, s.l2 * r.rcp_bt1);
-  x[6] = log2f_fast(fmaxf(o.t_roof * s.rcp_t0, 0x1p-20f)) * (1.0f / 16);
-  const float den = o.t_comp + o.t_mem;
-  x[7] = den > 0.0f ? o.t_comp * rcpf(den) : 0.0f;
 #pragma unroll
-  for (int i = 0; i < 7; ++i) x[8 + i] = r.xs[i];
-  x[15] = 1.0f;
+  for (int i = 0; i < 16; ++i) x[i] = feature(i, r, s, o);
   if constexpr (IN == 32) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) x[16 + i] = x[i] * x[i];
@@ -440,6 +454,43 @@ __device__ __forceinline__ float bounded_eta(const float (&x)[16], float W, cons
   const float w = fmaxf(W, 1.0f);
   const float eg = __expf(-zg), ea = __expf(-za);
   return (1.0f + eg) * (w * (1.0f + ea)) * rcpf((w - 1.0f) + w * ea);
+}
+
+// ------------------------------------------------------------ Tier B grid
+// The measured efficiency grid of Sec. 5.5 (Tier B), density-routed: the
+// query's three coordinates (features grid_axis[d]) are mapped to node
+// units t_d = (c_d - lo_d) (n_d - 1) / (hi_d - lo_d); inside the closed box,
+// with all eight corners of the cell measured (not NaN), eta is their
+// trilinear interpolation and `routed` is set; elsewhere the caller keeps
+// the family's other head.  g: the family's nodes, row-major [n0][n1][n2],
+// in LDS.  Every read stays in the family's nodes: the cell index is clamped
+// to 0 .. n_d - 2 (a NaN coordinate clamps to 0 and is never routed).
+__device__ __forceinline__ float grid_eta(const RowC &r, const SpecC &s, const Roof &o, const EvalParams &p,
+                                          const float *g, bool &routed) {
+  float fr[3];
+  int idx[3];
+  bool in = true;
+#pragma unroll
+  for (int d = 0; d < 3; ++d) {
+    const float t = (feature(p.grid_axis[d], r, s, o) - p.grid_lo[d]) * p.grid_scale[d];
+    const float top = (float)(p.grid_n[d] - 1);
+    in = in && t >= 0.0f && t <= top;
+    const float tc = fminf(fmaxf(t, 0.0f), top);
+    idx[d] = min((int)tc, p.grid_n[d] - 2);
+    fr[d] = tc - (float)idx[d];
+  }
+  const int s2 = p.grid_n[2], s1 = p.grid_n[1] * s2;
+  const float *c = g + (idx[0] * s1 + idx[1] * s2 + idx[2]);
+  const float v000 = c[0], v001 = c[1], v010 = c[s2], v011 = c[s2 + 1];
+  const float v100 = c[s1], v101 = c[s1 + 1], v110 = c[s1 + s2], v111 = c[s1 + s2 + 1];
+  const bool known = !__builtin_isnan(v000) && !__builtin_isnan(v001) && !__builtin_isnan(v010) &&
+                     !__builtin_isnan(v011) && !__builtin_isnan(v100) && !__builtin_isnan(v101) &&
+                     !__builtin_isnan(v110) && !__builtin_isnan(v111);
+  routed = in && known;
+  const float a00 = fmaf(fr[2], v001 - v000, v000), a01 = fmaf(fr[2], v011 - v010, v010);
+  const float a10 = fmaf(fr[2], v101 - v100, v100), a11 = fmaf(fr[2], v111 - v110, v110);
+  const float b0 = fmaf(fr[1], a01 - a00, a00), b1 = fmaf(fr[1], a11 - a10, a10);
+  return fmaf(fr[0], b1 - b0, b0);
 }
 
 // ------------------------------------------------------------ bf16 MFMA head
@@ -1068,12 +1119,15 @@ __device__ __forceinline__ Fields load_fields(const EvalParams &p, const Tile &t
   return f;
 }
 
-template <int KIND>
+// GRID: compiled with Tier B routing (a separate instantiation, so the
+// kernels without a grid keep their registers)
+template <int KIND, bool GRID>
 __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalParams p) {
   using H = typename KindOf<KIND>::H;
   constexpr int IN = KindOf<KIND>::IN;
   __shared__ uint32_t lds[H::LDS_DW];
   __shared__ float bnd_lds[32];   // the bounded head of the staged family: g then a
+  __shared__ float grid_lds[KS_GRID_MAX_NODES];   // the staged family's measured grid
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int n_wgt = p.wgt_off[KS_NFAM];
   int staged = -1;
@@ -1094,13 +1148,19 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
     const int fam = tc.fam;
     // this family takes the bounded head (the plain eta = 1 stream has none)
     const bool bnd = KIND != kEtaOne && ((p.bounded_mask >> fam) & 1u);
-    if (H::kMlp || (KIND != kEtaOne && p.bounded_mask)) {
+    // ... and a measured grid that routes some of its records
+    const bool grd = GRID && ((p.grid_mask >> fam) & 1u);
+    if (H::kMlp || (KIND != kEtaOne && (p.bounded_mask || GRID))) {
       if (fam != staged) {
         __syncthreads();
         if (bnd) {
           if (threadIdx.x < 32) bnd_lds[threadIdx.x] = p.bounded[fam * 32 + threadIdx.x];
         } else {
           if constexpr (H::kMlp) H::stage(lds, fam, p);
+        }
+        if (grd) {
+          const float *src = p.grid + (size_t)fam * p.grid_nodes;
+          for (int i = threadIdx.x; i < p.grid_nodes; i += kWgThreads) grid_lds[i] = src[i];
         }
         __syncthreads();
         staged = fam;
@@ -1114,7 +1174,7 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
     uint32_t bad = 0;
     if ((int64_t)fc.st >= p.n_steps) bad |= kErrStep;
     RowC rc;
-    if (!H::kMlp && !bnd && !p.o_flops && !p.o_bytes && !p.o_blocks) {
+    if (!H::kMlp && !bnd && !grd && !p.o_flops && !p.o_bytes && !p.o_blocks) {
       const CntF cf = record_counts_f(fam, fc.m, fc.n, fc.k, fc.a, fc.b, fc.st, p, bad);
       rc.B = cf.B;
       rc.Ff = cf.F;
@@ -1171,18 +1231,29 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
       const SpecC sc = spec_at(p.spec_c, s);
       const Roof o = small ? roofline<true>(rc, sc) : roofline<false>(rc, sc);
       float eta = 1.0f;
+      // Tier B first: the family's other head runs only if some record of
+      // the wave is not routed to the grid
+      bool routed = false;
+      float eta_g = 0.0f;
+      if (grd) eta_g = grid_eta(rc, sc, o, p, grid_lds, routed);
+      const bool other = !grd || __ballot(valid && !routed) != 0;
       if (bnd) {
-        float x[16];
-        features<16>(rc, sc, o, x);
-        eta = bounded_eta(x, o.W, bnd_lds);
+        if (other) {
+          float x[16];
+          features<16>(rc, sc, o, x);
+          eta = bounded_eta(x, o.W, bnd_lds);
+        }
       } else {
         if constexpr (H::kMlp) {
-          float x[IN];
-          features<IN>(rc, sc, o, x);
-          const float z = H::mlp(x, lds);
-          eta = 1.0f + __expf(-z);
+          if (other) {
+            float x[IN];
+            features<IN>(rc, sc, o, x);
+            const float z = H::mlp(x, lds);
+            eta = 1.0f + __expf(-z);
+          }
         }
       }
+      if (routed) eta = eta_g;
       const float t = fmaxf(o.t_roof * eta, sc.t0);
       if (valid) {
         const size_t i = (size_t)s * (size_t)p.fam_off[KS_NFAM] + (size_t)row;
@@ -1310,20 +1381,20 @@ hipError_t launch_spec_prep(const ks_spec *specs, int32_t n_specs, SpecC *out, u
 // The persistent grid: as many workgroups as are resident at once (the
 // occupancy the compiled kernel's registers and LDS allow, times the CU
 // count), so no workgroup of the head kinds waits for another to finish.
-// Cached per device and kind.
+// Cached per device and kernel.
 constexpr int kMaxDevices = 64;
-static std::atomic<int> g_resident[kMaxDevices][kNumKinds];
+static std::atomic<int> g_resident[kMaxDevices][kNumKinds][2];
 
-template <int KIND>
+template <int KIND, bool GRID>
 static hipError_t resident_wgs(int *out) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
-  std::atomic<int> *slot = dev < kMaxDevices ? &g_resident[dev][KIND] : nullptr;
+  std::atomic<int> *slot = dev < kMaxDevices ? &g_resident[dev][KIND][GRID] : nullptr;
   int r = slot ? slot->load(std::memory_order_relaxed) : 0;
   if (r == 0) {
     int per_cu = 0, n_cu = 0;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_eval<KIND>, kWgThreads, 0);
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_eval<KIND, GRID>, kWgThreads, 0);
     if (e != hipSuccess) return e;
     e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
@@ -1337,15 +1408,26 @@ static hipError_t resident_wgs(int *out) {
   return hipSuccess;
 }
 
-template <int KIND>
-static hipError_t launch_kind(const EvalParams &p, hipStream_t s) {
+template <int KIND, bool GRID>
+static hipError_t launch_grid(const EvalParams &p, hipStream_t s) {
   int cap = 0;
-  const hipError_t e = resident_wgs<KIND>(&cap);
+  const hipError_t e = resident_wgs<KIND, GRID>(&cap);
   if (e != hipSuccess) return e;
   const int n_wgt = p.wgt_off[KS_NFAM];
   const int grid = n_wgt < cap ? n_wgt : cap;
-  hipLaunchKernelGGL(k_eval<KIND>, dim3(grid), dim3(kWgThreads), 0, s, p);
+  hipLaunchKernelGGL((k_eval<KIND, GRID>), dim3(grid), dim3(kWgThreads), 0, s, p);
   return hipGetLastError();
+}
+
+// the eta = 1 stream has no Tier B instantiation (a grid selects the
+// head-less kind)
+template <int KIND>
+static hipError_t launch_kind(const EvalParams &p, hipStream_t s) {
+  if constexpr (KIND == kEtaOne) {
+    return p.grid_mask ? hipErrorInvalidValue : launch_grid<KIND, false>(p, s);
+  } else {
+    return p.grid_mask ? launch_grid<KIND, true>(p, s) : launch_grid<KIND, false>(p, s);
+  }
 }
 
 hipError_t launch_eval(int kind, const EvalParams &p, hipStream_t s) {

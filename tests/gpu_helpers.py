@@ -6,11 +6,11 @@ import numpy as np
 from paper_2606_28565_amd import abi
 
 
-def eval_kernels(wl, eta_one=False, n_specs=None, counts=True, bounded=None):
+def eval_kernels(wl, eta_one=False, n_specs=None, counts=True, bounded=None, grid=None):
     import torch
     di = abi.DeviceInputs(wl, n_specs=n_specs)
     heads = di.make_heads(wl.heads.precision, wl.heads.in_dim, wl.heads.hidden,
-                          abi.KS_ETA_ONE if eta_one else abi.KS_ETA_MLP, bounded)
+                          abi.KS_ETA_ONE if eta_one else abi.KS_ETA_MLP, bounded, grid)
     o, so = abi.kernel_outputs(wl.desc.n_rows, di.n_specs, counts=counts)
     abi.ks_eval_kernels(di.desc, di.specs_ptr, di.n_specs, heads, so, di.ws_ptr, di.ws_bytes,
                         abi.current_stream())
@@ -24,14 +24,15 @@ def eval_kernels(wl, eta_one=False, n_specs=None, counts=True, bounded=None):
 
 
 def eval_steps(wl, eta_one=False, n_specs=None, per_pair=True, counts=True, bounded=None,
-               null_mlp=False):
+               null_mlp=False, grid=None):
     """counts=False asks for per-pair outputs without the per-record counts
     (the eta = 1 stream then forms F and Bt in fp32).  bounded: a
-    ``workload.gen.Bounded``; null_mlp passes NULL MLP weights."""
+    ``workload.gen.Bounded``; grid: a ``workload.gen.Grid``; null_mlp
+    passes NULL MLP weights."""
     import torch
     di = abi.DeviceInputs(wl, n_specs=n_specs)
     heads = di.make_heads(wl.heads.precision, wl.heads.in_dim, wl.heads.hidden,
-                          abi.KS_ETA_ONE if eta_one else abi.KS_ETA_MLP, bounded)
+                          abi.KS_ETA_ONE if eta_one else abi.KS_ETA_MLP, bounded, grid)
     if null_mlp:
         heads.w1 = heads.w2 = heads.b2 = heads.w3 = heads.b3 = None
     so_t, so = abi.step_outputs(wl.desc.n_steps, di.n_specs)

@@ -115,6 +115,21 @@ def test_bad_specs_heads_workspace_rejected_on_host():
                  abi.ks_heads(16, 64, abi.KS_F32, abi.KS_ETA_MLP, bounded_mask=3, bounded=0x1000)]
     for h in bad_heads:
         assert _call_eval(d, heads=h) == abi.KS_EINVAL, abi.ks_last_error()
+    # Tier B grids: each field outside its documented range
+    good = dict(grid_mask=3, grid=0x1000, grid_axis=(1, 2, 6), grid_n=(4, 4, 4),
+                grid_lo=(0.0, 0.0, 0.0), grid_hi=(1.0, 1.0, 1.0))
+    for key, val, needle in (("grid_mask", 1 << 10, "grid_mask"), ("grid", None, "grid is NULL"),
+                             ("grid_axis", (1, 15, 6), "grid_axis[1]"), ("grid_axis", (-1, 2, 6), "grid_axis[0]"),
+                             ("grid_n", (4, 1, 4), "grid_n[1]"), ("grid_n", (16, 16, 16), "nodes"),
+                             ("grid_hi", (1.0, 1.0, 0.0), "grid_lo/hi[2]"),
+                             ("grid_lo", (float("nan"), 0.0, 0.0), "grid_lo/hi[0]"),
+                             ("grid_hi", (1e39, 1.0, 1.0), "grid_lo/hi[0]"),
+                             ("grid_hi", (1e-40, 1.0, 1.0), "grid_lo/hi[0]")):
+        for mode in (abi.KS_ETA_ONE, abi.KS_ETA_MLP):
+            kw = dict(good, **{key: val})
+            h = abi.ks_heads(16, 64, abi.KS_F32, mode, 1, 1, 1, 1, 1, **kw)
+            assert _call_eval(d, heads=h) == abi.KS_EINVAL, (key, val)
+            assert needle in abi.ks_last_error(), (needle, abi.ks_last_error())
     assert abi.load().ks_eval_kernels(C.byref(d), 0x2000, 1, C.byref(abi.ks_heads(16, 64, 0, 1)),
                                       None, 0x100000, 1 << 30, None) == abi.KS_EINVAL
 

@@ -517,3 +517,117 @@ def test_bounded_only():
 def test_bounded_with_block_counts_around_2_23():
     wl = _block_count_workload(heads=gen.make_heads(32, 256, "bf16"))
     _bounded_case(wl, gen.make_bounded(gen.BOUNDED_ALL ^ (1 << gen.GEMM)))
+
+
+# ------------------------------------------- Tier B measured grids (Sec. 5.5) --
+GRID_EPS = 1e-5   # node units: fp32 coordinates may sit on either side of a face this close
+
+
+def _grid_eta_check(wl, gr, ref, plain, gpu_eta, n_specs, fallback_tol):
+    """Pairs with every coordinate farther than GRID_EPS from a cell face are
+    routed as the oracle routes them and match its eta (REL when routed, the
+    fallback head's bar otherwise).  Pairs that close to a face match the
+    fallback or the grid at one of the nearby points on either side."""
+    fam = wl.desc.family()
+    on = ((gr.mask >> fam) & 1).astype(bool)
+    ax = list(gr.axes)
+    n = np.asarray(gr.n, np.float64)
+    step = (gr.hi - gr.lo) / (n - 1)
+    n_amb = 0
+    for s in range(n_specs):
+        x = ref["x16"][s]
+        t = (x[:, ax] - gr.lo) / step
+        amb = on & (np.abs(t - np.round(t)) < GRID_EPS).any(axis=1)
+        n_amb += int(amb.sum())
+        routed = ref["routed"][s] & ~amb
+        rest = ~routed & ~amb
+        assert g.rel_err(gpu_eta[s, routed], ref["eta"][s, routed]).max(initial=0) <= REL
+        assert g.rel_err(gpu_eta[s, rest], ref["eta"][s, rest]).max(initial=0) <= fallback_tol
+        for r in np.nonzero(amb)[0]:
+            cands = [plain["eta"][s, r]]
+            for sg in np.array(np.meshgrid(*[[-2, 0, 2]] * 3)).reshape(3, -1).T:
+                xn = x[r].copy()
+                xn[ax] += sg * GRID_EPS * step
+                e, rr = o.grid_eta(xn[None], gr, fam[r])
+                if rr[0]:
+                    cands.append(e[0])
+            tol = max(REL * 4, fallback_tol)
+            assert min(g.rel_err(gpu_eta[s, r], c) for c in cands) <= tol, (s, r, gpu_eta[s, r], cands)
+    assert n_amb <= 0.01 * on.sum() * n_specs
+
+
+def _grid_case(wl, gr, eta_one=False, bounded=None, null_mlp=False, n_specs=None, expect_routed=True):
+    n_specs = n_specs or wl.n_specs
+    heads = None if eta_one else wl.heads
+    kw = dict(eta_one=eta_one, spec_ids=range(n_specs), bounded=bounded)
+    ref = o.eval_kernels(wl.desc, wl.specs, heads, grid=gr, **kw)
+    plain = o.eval_kernels(wl.desc, wl.specs, heads, **kw)
+    gpu = g.eval_steps(wl, eta_one=eta_one, n_specs=n_specs, bounded=bounded, grid=gr, null_mlp=null_mlp)
+    if expect_routed:
+        assert ref["routed"].any() and (~ref["routed"]).any()
+    np.testing.assert_array_equal(gpu["flops"], ref["counts"]["F"])
+    assert g.rel_err(gpu["t_roof"], ref["t_roof"]).max() <= REL
+    bf16 = not eta_one and wl.heads.precision == "bf16"
+    fam = wl.desc.family()
+    on_b = ((bounded.mask if bounded is not None else 0) >> fam) & 1
+    mlp_fallback = bf16 and not (on_b.astype(bool)).all()
+    _grid_eta_check(wl, gr, ref, plain, gpu["eta"], n_specs, REL_BF16 if mlp_fallback else REL)
+    t0 = wl.specs["t0"][:n_specs, None]
+    assert g.rel_err(gpu["t_kernel"], np.maximum(ref["t_roof"] * gpu["eta"].astype(np.float64), t0)).max() <= REL
+    _check_steps(wl, gpu, _steps_given_eta(wl, gpu, ref, n_specs), bf16=False, n_specs=n_specs)
+    return ref, gpu
+
+
+def _quantile_grid(wl, mask, axes, q=(0.1, 0.9), n=(6, 5, 7), holes=0.08, seed=gen.GRID_SEED):
+    """A grid over the central quantiles of the workload's own features
+    (taken from the oracle), so part of the records fall inside."""
+    x = o.eval_kernels(wl.desc, wl.specs, None, eta_one=True,
+                       grid=gen.make_grid(0, axes=axes))["x16"].reshape(-1, 16)[:, list(axes)]
+    lo, hi = np.quantile(x, q[0], axis=0), np.quantile(x, q[1], axis=0)
+    hi = np.maximum(hi, lo + 1e-3)
+    # off the features' recurring exact values (x4 = 1/16 at one wave, ...)
+    w = hi - lo
+    lo, hi = lo - 0.0137 * w, hi + 0.0191 * w
+    return gen.make_grid(mask, axes=axes, lo=lo, hi=hi, n=n, holes=holes, seed=seed)
+
+
+def test_grid_with_fp32_mlp():
+    wl = gen.config1(0, 60)
+    _grid_case(wl, gen.make_grid(gen.GRID_ALL ^ (1 << gen.GEMM)))
+
+
+def test_grid_with_bf16_mlp():
+    """bf16 MLP fallback; the head is skipped for waves with every record on
+    the grid."""
+    wl = gen.config4(n_specs=12, grid_steps=20, c1_steps=30)
+    _grid_case(wl, _quantile_grid(wl, gen.GRID_ALL, (1, 2, 6)))
+
+
+def test_grid_eta_one_and_bounded_fallbacks():
+    wl = gen.config1(0, 60)
+    gr = gen.make_grid(gen.GRID_ALL)
+    _grid_case(wl, gr, eta_one=True)
+    bd = gen.make_bounded(gen.BOUNDED_MIXED)
+    _grid_case(wl, gr, bounded=bd)
+    _grid_case(wl, gr, eta_one=True, bounded=bd)
+    _grid_case(wl, gr, bounded=gen.make_bounded(gen.BOUNDED_ALL), null_mlp=True)
+
+
+@pytest.mark.parametrize("axes", [(0, 3, 4), (5, 7, 8), (9, 10, 11), (12, 13, 14), (2, 1, 6)])
+def test_grid_every_feature_axis(axes):
+    wl = gen.config3(0, 20)
+    _grid_case(wl, _quantile_grid(wl, gen.GRID_ALL, axes), expect_routed=False)
+
+
+def test_grid_sizes_and_degenerate_grids():
+    """The largest grid (2048 nodes), the smallest (2 x 2 x 2), a grid with
+    no holes, one with no measured node (routes nothing: the plain result)."""
+    wl = gen.config1(0, 40)
+    _grid_case(wl, _quantile_grid(wl, gen.GRID_ALL, (1, 2, 6), n=(16, 16, 8)))
+    _grid_case(wl, _quantile_grid(wl, gen.GRID_ALL, (1, 2, 6), n=(2, 2, 2), holes=0.0))
+    _grid_case(wl, _quantile_grid(wl, gen.GRID_ALL, (1, 2, 6), n=(9, 3, 4), holes=0.0))
+    ref, gpu = _grid_case(wl, gen.make_grid(gen.GRID_ALL, holes=1.0), expect_routed=False)
+    assert not ref["routed"].any()
+    plain = g.eval_steps(wl)
+    np.testing.assert_array_equal(gpu["eta"], plain["eta"])
+    np.testing.assert_array_equal(gpu["t_step"], plain["t_step"])
