@@ -433,9 +433,12 @@ def eval_kernels(desc, specs, heads=None, eta_one=False, emulate_bf16=None,
 # --------------------------------------------------------------------------
 # step terms (Sec. 5.6, Eq. 3; Sec. 5.7, Eq. 4)
 # --------------------------------------------------------------------------
-def step_body(t, step, n_steps):
-    """Sum of the latencies of each step's kernels (Sec. 5.7)."""
-    return np.bincount(np.asarray(step, np.int64), weights=t, minlength=n_steps)
+def step_body(t, step, n_steps, mult=None):
+    """Sum of the latencies of each step's kernels (Sec. 5.7); a record of
+    multiplicity m stands for m dispatches of the same kernel (the L
+    homogeneous layers of t_gpu = L t_layer + ...) and adds m t."""
+    w = t if mult is None else t * np.asarray(mult, np.float64)
+    return np.bincount(np.asarray(step, np.int64), weights=w, minlength=n_steps)
 
 
 def allreduce_time(P, S, alpha0, alpha_log2p, beta):
@@ -469,7 +472,8 @@ def eval_steps(desc, steprec, specs, host, heads=None, eta_one=False,
     out = {key: np.zeros((len(spec_ids), n_steps)) for key in ("t_body", "t_comm", "t_gpu", "t_step")}
     for si, s in enumerate(spec_ids):
         sp = spec_at(specs, s)
-        body = step_body(kern["t"][si], desc.step[kern["rows"]], n_steps)
+        mult = None if getattr(desc, "mult", None) is None else desc.mult[kern["rows"]]
+        body = step_body(kern["t"][si], desc.step[kern["rows"]], n_steps, mult)
         t_ar = allreduce_time(steprec.tp, S, sp["ar_alpha0"], sp["ar_alpha_log2p"], sp["ar_beta"])
         comm = 2.0 * L * t_ar                       # two all-reduces per layer
         gpu = host.body_scale * body + comm

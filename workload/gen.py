@@ -273,6 +273,7 @@ class Desc:
     req_h: np.ndarray          # uint32 [n_req]
     expert_rows: np.ndarray    # uint32 [n_expert_rows]
     elem_bytes: int = 2
+    mult: np.ndarray | None = None   # uint32 [n_rows]: dispatches per record (None: 1)
 
     @property
     def n_rows(self) -> int:
