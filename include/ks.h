@@ -93,6 +93,12 @@ typedef struct ks_desc {
   int64_t n_expert_rows;
   uint32_t elem_bytes;                   /* dt, bytes per element (2 = bf16) */
   uint32_t reserved;
+  /* device [n_rows] or NULL: the number of dispatches each record stands
+   * for (Sec. 5.7: decoder layers are homogeneous, so a kernel that is the
+   * same in every layer may be one record of multiplicity L).  The step body
+   * adds mult * t for the record; per-pair outputs stay per dispatch.  NULL:
+   * every record is one dispatch.  Limit: mult < 2^24. */
+  const uint32_t *mult;
 } ks_desc;
 
 /*
@@ -191,6 +197,93 @@ typedef struct ks_step_out {
   double *t_body, *t_gpu, *t_step;
 } ks_step_out;
 
+/*
+ * Batch expansion (Sec. 4.1: the scheduler's batch descriptor of each step;
+ * Sec. 5.7: one embedding and one LM head per step around L homogeneous
+ * layers; Sec. 5.8: the dense GEMMs, norms and activations run over the
+ * step's T = sum q_r tokens, attention over its requests).  ks_expand writes
+ * the records (and the per-step model record) of every kernel the steps of
+ * one batch dispatch, on the device, in the layout ks_eval_steps reads.
+ *
+ * Per layer, in dispatch order (per-GPU shard sizes under TP P: H = Hq/P,
+ * Hkv = ceil(Hkv/P), I = ffn/P, I_e = expert_ffn/P, V/P):
+ *   GEMM QKV (m T, n (H + 2 Hkv) d, k D); ROPE (T, H + Hkv, d);
+ *   KV_WRITE (T, Hkv, d) if kv_write; attention (n H, k d, a Hkv) in
+ *   ATTN_PREFILL if the step's prefill flag is set, else ATTN_DECODE;
+ *   GEMM O (T, D, H d); RMSNORM (T, D) twice; then dense: GEMM gate/up
+ *   (T, 2I, D), SILU_MUL (T, I), GEMM down (T, D, I); or experts > 0: GEMM
+ *   router (T, E, D), GROUPED_GEMM gate/up (n 2 I_e, k D, a E,
+ *   b (j L + l) E), SILU_MUL (top_k T, I_e), GROUPED_GEMM down (n D, k I_e,
+ *   a E, b (j L + l) E).
+ * Per step j: EMBED (T, D) and LM_HEAD (m R requests, n V/P, k D).
+ * Unused fields are written as 0.  Records are family-major; within a
+ * family by step, then layer, then dispatch order.  Grouped records point
+ * at the routed row counts M_e of (step j, layer l): the caller passes its
+ * [n_steps][L][E] routing array as ks_desc.expert_rows (n_expert_rows =
+ * n_steps L E).  Per-step record: layers L, hidden D, tp P, n_launch = L for
+ * a step with a prefill chunk (eager, one launch charge per layer) else 0.
+ *
+ * KS_EXPAND_HOMOGENEOUS: every kernel that is the same in all L layers of
+ * a step (all but the grouped GEMMs) is one record of multiplicity L, in
+ * dispatch order within its family; the grouped GEMMs stay per layer.
+ * KS_EXPAND_PER_LAYER: one record per dispatched kernel (multiplicity 1).
+ */
+typedef struct ks_model {
+  uint32_t hidden;       /* D, >= 1                                       */
+  uint32_t layers;       /* L, >= 1                                       */
+  uint32_t q_heads;      /* Hq (whole model), divisible by tp             */
+  uint32_t kv_heads;     /* Hkv (whole model), >= 1                       */
+  uint32_t head_dim;     /* d                                             */
+  uint32_t ffn;          /* dense MLP width, divisible by tp (unused for experts > 0) */
+  uint32_t vocab;        /* V, divisible by tp                            */
+  uint32_t tp;           /* P, >= 1                                       */
+  uint32_t experts;      /* E: 0 = dense MLP, else 1 .. 1024 experts      */
+  uint32_t top_k;        /* routed copies per token, 1 .. E (experts > 0) */
+  uint32_t expert_ffn;   /* per-expert width, divisible by tp (experts > 0) */
+  uint32_t kv_write;     /* 1: a KV-cache write kernel per layer, else 0  */
+} ks_model;
+
+/* One batch of consecutive steps (device arrays unless noted). */
+typedef struct ks_batch {
+  int64_t n_steps;
+  const uint32_t *req_off;   /* [n_steps + 1], req_off[0] = 0, non-decreasing */
+  const uint32_t *req_q;     /* [n_req] query tokens of each request          */
+  int64_t n_req;
+  const uint8_t *prefill;    /* [n_steps] nonzero: the step has a prefill chunk */
+  int64_t n_prefill;         /* host value: how many prefill flags are nonzero */
+} ks_batch;
+
+enum { KS_EXPAND_PER_LAYER = 0, KS_EXPAND_HOMOGENEOUS = 1 };
+
+/* Outputs of ks_expand (device, caller-owned).  Record arrays hold
+ * fam_off[KS_NFAM] entries (fam_off from ks_expand_layout); mult may be NULL
+ * in KS_EXPAND_PER_LAYER mode.  layers, hidden, tp, n_launch: [n_steps],
+ * the ks_steps arrays of the batch. */
+typedef struct ks_records {
+  uint32_t *step, *m, *n, *k, *a, *b, *mult;
+  uint32_t *layers, *hidden, *tp, *n_launch;
+} ks_records;
+
+/* Host only: the family offsets of the expansion of n_steps steps of which
+ * n_prefill carry a prefill chunk (fam_off[0] = 0, fam_off[KS_NFAM] = record
+ * count).  Checks the model (KS_EINVAL / KS_ERANGE: sizes not divisible by
+ * tp, record fields beyond the ks_desc limits, more than 2^32 - 1 records
+ * or routed-row offsets). */
+ks_status ks_expand_layout(const ks_model* model, int64_t n_steps, int64_t n_prefill, int32_t mode,
+                           int64_t fam_off[KS_NFAM + 1]);
+
+/* Bytes of device workspace ks_expand needs for n_steps steps. */
+size_t ks_expand_workspace_bytes(int64_t n_steps);
+
+/* Writes the records of the batch (asynchronous on `stream`).  Host checks
+ * as ks_expand_layout plus null pointers and the workspace.  Device data
+ * that disagrees with the call (request offsets out of order or beyond
+ * n_req, a step's T or top_k T at or above 2^24, a prefill flag count other
+ * than n_prefill) raises a flag that ks_device_status(ws) reports; the
+ * kernels then still write only inside the record arrays. */
+ks_status ks_expand(const ks_model* model, const ks_batch* batch, int32_t mode, const ks_records* out,
+                    void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Bytes of device workspace ks_eval_kernels / ks_eval_steps / ks_validate
  * need for this record set and spec count (256-byte aligned).  0 on bad
  * arguments. */
@@ -218,9 +311,9 @@ ks_status ks_validate(const ks_desc* desc, const ks_steps* steps,
                       const ks_spec* specs, int32_t n_specs,
                       void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* Synchronizes the stream and reports the flag the evaluation kernels raise
- * when they skipped a record on bad data since the workspace's last
- * evaluation call started (KS_OK if none). */
+/* Synchronizes the stream and reports the flag the evaluation (or
+ * expansion) kernels raise when they skipped a record on bad data since the
+ * workspace's last evaluation (or expansion) call started (KS_OK if none). */
 ks_status ks_device_status(const void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Message of the last non-OK status returned on this thread. */

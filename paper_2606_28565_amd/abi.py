@@ -28,7 +28,7 @@ class ks_desc(C.Structure):
                 ("step", P), ("m", P), ("n", P), ("k", P), ("a", P), ("b", P),
                 ("n_steps", C.c_int64), ("req_off", P), ("req_q", P), ("req_h", P),
                 ("n_req", C.c_int64), ("expert_rows", P), ("n_expert_rows", C.c_int64),
-                ("elem_bytes", C.c_uint32), ("reserved", C.c_uint32)]
+                ("elem_bytes", C.c_uint32), ("reserved", C.c_uint32), ("mult", P)]
 
 
 class ks_spec(C.Structure):
@@ -62,6 +62,27 @@ class ks_kernel_out(C.Structure):
 
 class ks_step_out(C.Structure):
     _fields_ = [("t_body", P), ("t_gpu", P), ("t_step", P)]
+
+
+MODEL_FIELDS = ("hidden", "layers", "q_heads", "kv_heads", "head_dim", "ffn", "vocab", "tp",
+                "experts", "top_k", "expert_ffn", "kv_write")
+
+
+class ks_model(C.Structure):
+    _fields_ = [(name, C.c_uint32) for name in MODEL_FIELDS]
+
+
+class ks_batch(C.Structure):
+    _fields_ = [("n_steps", C.c_int64), ("req_off", P), ("req_q", P), ("n_req", C.c_int64),
+                ("prefill", P), ("n_prefill", C.c_int64)]
+
+
+class ks_records(C.Structure):
+    _fields_ = [(name, P) for name in ("step", "m", "n", "k", "a", "b", "mult",
+                                       "layers", "hidden", "tp", "n_launch")]
+
+
+KS_EXPAND_PER_LAYER, KS_EXPAND_HOMOGENEOUS = 0, 1
 
 
 assert C.sizeof(ks_spec) == 64
@@ -98,6 +119,14 @@ def load(path: str = LIB_PATH) -> C.CDLL:
     lib.ks_validate.restype = C.c_int
     lib.ks_device_status.argtypes = [P, C.c_size_t, P]
     lib.ks_device_status.restype = C.c_int
+    lib.ks_expand_layout.argtypes = [C.POINTER(ks_model), C.c_int64, C.c_int64, C.c_int32,
+                                     C.POINTER(C.c_int64)]
+    lib.ks_expand_layout.restype = C.c_int
+    lib.ks_expand_workspace_bytes.argtypes = [C.c_int64]
+    lib.ks_expand_workspace_bytes.restype = C.c_size_t
+    lib.ks_expand.argtypes = [C.POINTER(ks_model), C.POINTER(ks_batch), C.c_int32,
+                              C.POINTER(ks_records), P, C.c_size_t, P]
+    lib.ks_expand.restype = C.c_int
     lib.ks_last_error.argtypes = []
     lib.ks_last_error.restype = C.c_char_p
     lib.ks_version.argtypes = []
@@ -143,6 +172,24 @@ def ks_validate(desc, steps, specs_ptr, n_specs, ws_ptr, ws_bytes, stream, check
 
 def ks_device_status(ws_ptr, ws_bytes, stream, check=True):
     st = load().ks_device_status(ws_ptr, ws_bytes, stream)
+    return _check(st) if check else st
+
+
+def ks_expand_layout(model: ks_model, n_steps: int, n_prefill: int, mode: int, check=True):
+    """Returns (status, fam_off as a list of NFAM + 1 ints)."""
+    arr = (C.c_int64 * (NFAM + 1))()
+    st = load().ks_expand_layout(C.byref(model), n_steps, n_prefill, mode, arr)
+    if check:
+        _check(st)
+    return st, list(arr)
+
+
+def ks_expand_workspace_bytes(n_steps: int) -> int:
+    return load().ks_expand_workspace_bytes(n_steps)
+
+
+def ks_expand(model, batch, mode, out, ws_ptr, ws_bytes, stream, check=True):
+    st = load().ks_expand(C.byref(model), C.byref(batch), mode, C.byref(out), ws_ptr, ws_bytes, stream)
     return _check(st) if check else st
 
 
@@ -218,6 +265,9 @@ class DeviceInputs:
         self.desc.expert_rows = _ptr(self.t["expert_rows"]) if len(d.expert_rows) else None
         self.desc.n_expert_rows = len(d.expert_rows)
         self.desc.elem_bytes = d.elem_bytes
+        if getattr(d, "mult", None) is not None:
+            self.t["mult"] = u32(d.mult)
+            self.desc.mult = _ptr(self.t["mult"]) if self.t["mult"].numel() else None
 
         self.steps = ks_steps()
         self.steps.n_steps = d.n_steps
@@ -299,3 +349,74 @@ def step_outputs(n_steps: int, n_specs: int, device="cuda"):
 def current_stream() -> int:
     import torch
     return torch.cuda.current_stream().cuda_stream
+
+
+# --------------------------------------------------------------------------
+# batch expansion: batch descriptors on the device -> records on the device
+# --------------------------------------------------------------------------
+def model_of(shape) -> ks_model:
+    """A decoder shape (any object with the ks_model field names, e.g.
+    ``workload.gen.ModelShape``) -> ks_model."""
+    return ks_model(*(int(getattr(shape, name)) for name in MODEL_FIELDS))
+
+
+class DeviceBatch:
+    """One batch of steps (request lists, prefill flags and, for a mixture of
+    experts, the [steps][layers][experts] routing counts) resident on the
+    device, the record arrays ks_expand writes, and a ks_desc / ks_steps
+    pair over them for the evaluation entry points."""
+
+    def __init__(self, trace, mode=KS_EXPAND_PER_LAYER, device="cuda", elem_bytes=2):
+        import torch
+        dev = torch.device(device)
+
+        def u32(x):
+            return torch.from_numpy(np.ascontiguousarray(x, np.uint32).view(np.int32)).to(dev)
+
+        self.mode = mode
+        self.model = model_of(trace.shape)
+        S = int(trace.n_steps)
+        n_pre = int(np.count_nonzero(trace.prefill))
+        self.t = {"req_off": u32(trace.req_off), "req_q": u32(trace.req_q), "req_h": u32(trace.req_h),
+                  "prefill": torch.from_numpy(np.ascontiguousarray(trace.prefill, np.uint8)).to(dev)}
+        route = trace.experts if trace.experts is not None else np.zeros(0, np.uint32)
+        self.t["route"] = u32(np.asarray(route).reshape(-1))
+        self.batch = ks_batch(S, _ptr(self.t["req_off"]),
+                              _ptr(self.t["req_q"]) if self.t["req_q"].numel() else None,
+                              int(len(trace.req_q)), _ptr(self.t["prefill"]) if S else None, n_pre)
+        _, fam_off = ks_expand_layout(self.model, S, n_pre, mode)
+        self.fam_off = fam_off
+        n = fam_off[-1]
+        for name in ("step", "m", "n", "k", "a", "b", "mult"):
+            self.t[name] = torch.empty(n, dtype=torch.int32, device=dev)
+        for name in ("layers", "hidden", "tp", "n_launch"):
+            self.t["s_" + name] = torch.empty(S, dtype=torch.int32, device=dev)
+        self.out = ks_records(*(_ptr(self.t[name]) if n else None
+                                for name in ("step", "m", "n", "k", "a", "b", "mult")),
+                              *(_ptr(self.t["s_" + name]) if S else None
+                                for name in ("layers", "hidden", "tp", "n_launch")))
+        self.ws_bytes = ks_expand_workspace_bytes(S)
+        self.ws = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=dev)
+        self.ws_ptr = self.ws.data_ptr() + (-self.ws.data_ptr()) % 256
+
+        self.desc = ks_desc()
+        self.desc.n_rows = n
+        for f in range(NFAM + 1):
+            self.desc.fam_off[f] = fam_off[f]
+        for name in ("step", "m", "n", "k", "a", "b"):
+            setattr(self.desc, name, _ptr(self.t[name]) if n else None)
+        self.desc.mult = _ptr(self.t["mult"]) if n and mode == KS_EXPAND_HOMOGENEOUS else None
+        self.desc.n_steps = S
+        self.desc.req_off = _ptr(self.t["req_off"])
+        self.desc.req_q = self.batch.req_q
+        self.desc.req_h = _ptr(self.t["req_h"]) if self.t["req_h"].numel() else None
+        self.desc.n_req = self.batch.n_req
+        self.desc.expert_rows = _ptr(self.t["route"]) if self.t["route"].numel() else None
+        self.desc.n_expert_rows = int(self.t["route"].numel())
+        self.desc.elem_bytes = elem_bytes
+        self.steps = ks_steps(S, *(_ptr(self.t["s_" + name]) if S else None
+                                   for name in ("layers", "hidden", "tp", "n_launch")))
+
+    def expand(self, stream, check=True):
+        return ks_expand(self.model, self.batch, self.mode, self.out, self.ws_ptr, self.ws_bytes,
+                         stream, check)

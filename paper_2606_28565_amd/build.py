@@ -43,10 +43,12 @@ def build(verbose: bool = False) -> str:
     kern = os.path.join(tmp, "ks_kernels.o")
     api = os.path.join(tmp, "ks_api.o")
     common = ["-I", INCLUDE, "-I", CSRC]
+    expand = os.path.join(tmp, "ks_expand.o")
     _run([HIPCC, *DEVICE_FLAGS, *common, "-c", os.path.join(CSRC, "ks_kernels.hip"), "-o", kern])
+    _run([HIPCC, *DEVICE_FLAGS, *common, "-c", os.path.join(CSRC, "ks_expand.hip"), "-o", expand])
     _run([HIPCC, *HOST_FLAGS, *common, "-D__HIP_PLATFORM_AMD__", "-c",
           os.path.join(CSRC, "ks_api.cpp"), "-o", api])
-    objs = [kern, api]
+    objs = [kern, expand, api]
     tmp_lib = LIB + ".tmp"
     _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp_lib])
     os.replace(tmp_lib, LIB)

@@ -181,6 +181,7 @@ void fill_eval(ks::EvalParams &p, const ks_desc *d, const ks_spec *specs, int32_
   p.b = d->b;
   p.expert_rows = d->expert_rows;
   p.n_expert_rows = d->expert_rows ? d->n_expert_rows : 0;
+  p.mult = d->n_rows > 0 ? d->mult : nullptr;
   p.agg = reinterpret_cast<const uint64_t *>(ws + L.agg);
   p.n_steps = d->n_steps;
   p.elem_bytes = d->elem_bytes;
@@ -237,6 +238,115 @@ ks_status prologue(const ks_desc *d, const ks_spec *specs, int32_t n_specs, char
   return KS_OK;
 }
 
+// ---- batch expansion: the per-family record templates of a model (the
+// per-layer kernel list in dispatch order, and the per-step embedding and
+// LM head), the item space and the record counts
+struct Plan {
+  uint32_t n_tpl[KS_NFAM];          // templates per layer (or per step)
+  ks::ExpandTpl tpl[KS_NFAM][ks::kExpandTpl];
+  bool per_layer[KS_NFAM];          // dispatched once per layer (else once per step)
+  uint32_t per_step[KS_NFAM], mult[KS_NFAM];
+  int64_t count[KS_NFAM];
+};
+
+ks_status model_plan(const ks_model *md, int64_t n_steps, int64_t n_prefill, int32_t mode, Plan *pl) {
+  if (!md) return fail(KS_EINVAL, "model is NULL");
+  if (mode != KS_EXPAND_PER_LAYER && mode != KS_EXPAND_HOMOGENEOUS) return fail(KS_EINVAL, "mode %d unknown", mode);
+  if (n_steps < 0 || n_steps >= (int64_t(1) << 32) - 1)
+    return fail(KS_ERANGE, "n_steps %lld outside [0, 2^32-1)", (long long)n_steps);
+  if (n_prefill < 0 || n_prefill > n_steps)
+    return fail(KS_EINVAL, "n_prefill %lld outside [0, n_steps]", (long long)n_prefill);
+  const uint32_t P = md->tp;
+  if (md->layers < 1 || md->hidden < 1 || md->head_dim < 1 || md->kv_heads < 1 || P < 1)
+    return fail(KS_EINVAL, "model: layers, hidden, head_dim, kv_heads and tp must be >= 1");
+  if (md->q_heads < P || md->q_heads % P) return fail(KS_EINVAL, "model: q_heads %u not a positive multiple of tp %u",
+                                                      md->q_heads, P);
+  if (md->vocab % P) return fail(KS_EINVAL, "model: vocab %u not divisible by tp %u", md->vocab, P);
+  if (md->kv_write > 1) return fail(KS_EINVAL, "model: kv_write %u not 0 or 1", md->kv_write);
+  const bool moe = md->experts > 0;
+  if (moe) {
+    if (md->experts > 1024) return fail(KS_ERANGE, "model: experts %u above 1024", md->experts);
+    if (md->top_k < 1 || md->top_k > md->experts)
+      return fail(KS_EINVAL, "model: top_k %u outside 1 .. experts", md->top_k);
+    if (md->expert_ffn % P) return fail(KS_EINVAL, "model: expert_ffn %u not divisible by tp %u", md->expert_ffn, P);
+  } else if (md->ffn % P) {
+    return fail(KS_EINVAL, "model: ffn %u not divisible by tp %u", md->ffn, P);
+  }
+  const uint64_t D = md->hidden, L = md->layers, d = md->head_dim;
+  const uint64_t H = md->q_heads / P, Hkv = (md->kv_heads + P - 1) / P;
+  const uint64_t I = moe ? 0 : md->ffn / P, Ie = moe ? md->expert_ffn / P : 0, V = md->vocab / P;
+  const uint64_t E = md->experts;
+  if (H >= 4096 || d >= 4096 || Hkv >= 4096) return fail(KS_ERANGE, "model: attention H, d or Hkv at or above 2^12");
+  std::memset(pl, 0, sizeof *pl);
+  auto add = [&](int f, uint32_t msrc, uint64_t n, uint64_t k, uint64_t a, bool grouped) {
+    pl->tpl[f][pl->n_tpl[f]++] = ks::ExpandTpl{(uint32_t)n, (uint32_t)k, (uint32_t)a, msrc, grouped ? 1u : 0u};
+    return n < (1u << 18) && k < (1u << 18);
+  };
+  bool ok = true;
+  // per layer, dispatch order within each family
+  ok &= add(KS_GEMM, ks::kMTok, (H + 2 * Hkv) * d, D, 0, false);   // QKV projection
+  ok &= add(KS_ROPE, ks::kMTok, H + Hkv, d, 0, false);
+  if (md->kv_write) ok &= add(KS_KV_WRITE, ks::kMTok, Hkv, d, 0, false);
+  ok &= add(KS_ATTN_PREFILL, ks::kMZero, H, d, Hkv, false);        // either attention family
+  ok &= add(KS_GEMM, ks::kMTok, D, H * d, 0, false);                // O projection
+  ok &= add(KS_RMSNORM, ks::kMTok, D, 0, 0, false);
+  ok &= add(KS_RMSNORM, ks::kMTok, D, 0, 0, false);
+  if (!moe) {
+    ok &= add(KS_GEMM, ks::kMTok, 2 * I, D, 0, false);              // gate/up
+    ok &= add(KS_SILU_MUL, ks::kMTok, I, 0, 0, false);
+    ok &= add(KS_GEMM, ks::kMTok, D, I, 0, false);                  // down
+  } else {
+    ok &= add(KS_GEMM, ks::kMTok, E, D, 0, false);                  // router
+    ok &= add(KS_GROUPED_GEMM, ks::kMZero, 2 * Ie, D, E, true);     // gate/up
+    ok &= add(KS_SILU_MUL, ks::kMTopk, Ie, 0, 0, false);
+    ok &= add(KS_GROUPED_GEMM, ks::kMZero, D, Ie, E, true);         // down
+  }
+  for (int f = 0; f < KS_NFAM; ++f) pl->per_layer[f] = pl->n_tpl[f] > 0;
+  // per step
+  ok &= add(KS_EMBED, ks::kMTok, D, 0, 0, false);
+  ok &= add(KS_LM_HEAD, ks::kMReq, V, D, 0, false);
+  if (!ok) return fail(KS_ERANGE, "model: a record's n or k at or above 2^18");
+  int64_t total = 0, items = 0;
+  for (int f = 0; f < KS_NFAM; ++f) {
+    const bool collapse = mode == KS_EXPAND_HOMOGENEOUS && f != KS_GROUPED_GEMM;
+    const uint64_t reps = pl->per_layer[f] && !collapse ? L : 1;
+    pl->per_step[f] = (uint32_t)(reps * pl->n_tpl[f]);
+    pl->mult[f] = pl->per_layer[f] && collapse ? (uint32_t)L : 1u;
+    const int64_t steps = f == KS_ATTN_PREFILL ? n_prefill : (f == KS_ATTN_DECODE ? n_steps - n_prefill : n_steps);
+    const int64_t per = f == KS_ATTN_DECODE ? pl->per_step[KS_ATTN_PREFILL] : pl->per_step[f];
+    if (per > 0 && steps > ((int64_t(1) << 40) / per)) return fail(KS_ERANGE, "expansion beyond 2^32 records");
+    pl->count[f] = per * steps;
+    total += pl->count[f];
+    items += (int64_t)pl->per_step[f] * n_steps;
+  }
+  if (total >= (int64_t(1) << 32) - 1 || items >= (int64_t(1) << 32))
+    return fail(KS_ERANGE, "expansion of %lld records at or above 2^32 - 1", (long long)total);
+  if (moe && (uint64_t)n_steps * L * E >= (uint64_t(1) << 32))
+    return fail(KS_ERANGE, "routed-row offsets n_steps L E at or above 2^32");
+  if (pl->mult[KS_GEMM] >= (1u << 24)) return fail(KS_ERANGE, "layers at or above 2^24");
+  return KS_OK;
+}
+
+struct ExpandLayout {
+  size_t tok, rank, blk, total;
+  int64_t n_blk;
+};
+
+ExpandLayout expand_layout_of(int64_t n_steps) {
+  ExpandLayout L;
+  const size_t S = (size_t)(n_steps < 0 ? 0 : n_steps);
+  L.n_blk = (int64_t)((S + ks::kExpandBlk - 1) / ks::kExpandBlk);
+  size_t off = 256;
+  L.tok = off;
+  off += align256(S * sizeof(uint32_t));
+  L.rank = off;
+  off += align256(S * sizeof(uint32_t));
+  L.blk = off;
+  off += align256((size_t)L.n_blk * sizeof(uint32_t));
+  L.total = off;
+  return L;
+}
+
 const char *flag_text(uint32_t f) {
   if (f & ks::kErrStep) return "a record's step index is >= n_steps";
   if (f & ks::kErrOrder) return "record steps decrease within a family";
@@ -244,12 +354,14 @@ const char *flag_text(uint32_t f) {
   if (f & ks::kErrExpert) return "grouped-GEMM expert offsets beyond n_expert_rows (or E > 1024)";
   if (f & ks::kErrRange) return "a shape or count outside the documented limits";
   if (f & ks::kErrSpec) return "a spec vector is not usable (non-positive peak, bandwidth or n_cu)";
+  if (f & ks::kErrPrefill) return "the batch's prefill flags disagree with n_prefill";
   return "unknown";
 }
 
 ks_status flag_status(uint32_t f) {
   if (!f) return KS_OK;
-  const bool range = (f & (ks::kErrRange | ks::kErrSpec)) && !(f & (ks::kErrStep | ks::kErrOrder | ks::kErrReq | ks::kErrExpert));
+  const bool range = (f & (ks::kErrRange | ks::kErrSpec)) &&
+                     !(f & (ks::kErrStep | ks::kErrOrder | ks::kErrReq | ks::kErrExpert | ks::kErrPrefill));
   return fail(range ? KS_ERANGE : KS_EINVAL, "device check: %s (flags 0x%x)", flag_text(f), f);
 }
 
@@ -357,6 +469,7 @@ ks_status ks_validate(const ks_desc *desc, const ks_steps *steps, const ks_spec 
   v.k = desc->k;
   v.a = desc->a;
   v.b = desc->b;
+  v.mult = desc->mult;
   v.expert_rows = desc->expert_rows;
   v.n_expert_rows = desc->expert_rows ? desc->n_expert_rows : 0;
   v.n_rows = desc->n_rows;
@@ -384,6 +497,96 @@ ks_status ks_device_status(const void *ws, size_t ws_bytes, hipStream_t stream) 
   e = hipStreamSynchronize(stream);
   if (e != hipSuccess) return hip_fail(e, "stream synchronize");
   return flag_status(flag);
+}
+
+ks_status ks_expand_layout(const ks_model *model, int64_t n_steps, int64_t n_prefill, int32_t mode,
+                           int64_t fam_off[KS_NFAM + 1]) {
+  if (!fam_off) return fail(KS_EINVAL, "fam_off is NULL");
+  Plan pl;
+  const ks_status st = model_plan(model, n_steps, n_prefill, mode, &pl);
+  if (st != KS_OK) return st;
+  fam_off[0] = 0;
+  for (int f = 0; f < KS_NFAM; ++f) fam_off[f + 1] = fam_off[f] + pl.count[f];
+  return KS_OK;
+}
+
+size_t ks_expand_workspace_bytes(int64_t n_steps) {
+  if (n_steps < 0 || n_steps >= (int64_t(1) << 32) - 1) return 0;
+  return expand_layout_of(n_steps).total;
+}
+
+ks_status ks_expand(const ks_model *model, const ks_batch *batch, int32_t mode, const ks_records *out, void *ws,
+                    size_t ws_bytes, hipStream_t stream) {
+  if (!batch) return fail(KS_EINVAL, "batch is NULL");
+  Plan pl;
+  ks_status st = model_plan(model, batch->n_steps, batch->n_prefill, mode, &pl);
+  if (st != KS_OK) return st;
+  const int64_t S = batch->n_steps;
+  if (batch->n_req < 0 || batch->n_req >= (int64_t(1) << 32))
+    return fail(KS_ERANGE, "n_req %lld outside [0, 2^32)", (long long)batch->n_req);
+  if (!batch->req_off) return fail(KS_EINVAL, "batch.req_off is NULL");
+  if (batch->n_req > 0 && !batch->req_q) return fail(KS_EINVAL, "batch.req_q is NULL");
+  if (S > 0 && !batch->prefill) return fail(KS_EINVAL, "batch.prefill is NULL");
+  if (!out) return fail(KS_EINVAL, "out is NULL");
+  int64_t total = 0;
+  for (int f = 0; f < KS_NFAM; ++f) total += pl.count[f];
+  if (total > 0 && (!out->step || !out->m || !out->n || !out->k || !out->a || !out->b))
+    return fail(KS_EINVAL, "a record output array is NULL");
+  if (mode == KS_EXPAND_HOMOGENEOUS && total > 0 && !out->mult)
+    return fail(KS_EINVAL, "out.mult is NULL in the homogeneous mode");
+  if (S > 0 && (!out->layers || !out->hidden || !out->tp || !out->n_launch))
+    return fail(KS_EINVAL, "a per-step output array is NULL");
+  const ExpandLayout L = expand_layout_of(S);
+  if (!ws) return fail(KS_EWORKSPACE, "workspace is NULL");
+  if (ws_bytes < L.total) return fail(KS_EWORKSPACE, "workspace %zu bytes < %zu required", ws_bytes, L.total);
+  if (reinterpret_cast<uintptr_t>(ws) % 256) return fail(KS_EWORKSPACE, "workspace not 256-byte aligned");
+  char *w = static_cast<char *>(ws);
+
+  ks::ExpandParams p;
+  std::memset(&p, 0, sizeof p);
+  p.req_off = batch->req_off;
+  p.req_q = batch->req_q;
+  p.n_req = batch->n_req;
+  p.prefill = batch->prefill;
+  p.n_steps = S;
+  p.n_prefill = batch->n_prefill;
+  p.L = model->layers;
+  p.E = model->experts;
+  p.top_k = model->experts ? model->top_k : 0;
+  p.D = model->hidden;
+  p.P = model->tp;
+  p.item_off[0] = 0;
+  p.fam_off[0] = 0;
+  for (int f = 0; f < KS_NFAM; ++f) {
+    // the attention items of every step live under ATTN_PREFILL
+    p.per_step[f] = f == KS_ATTN_DECODE ? 0 : pl.per_step[f];
+    p.n_tpl[f] = pl.n_tpl[f] ? pl.n_tpl[f] : 1;
+    p.mult[f] = pl.mult[f];
+    for (int t = 0; t < ks::kExpandTpl; ++t) p.tpl[f][t] = pl.tpl[f][t];
+    p.item_off[f + 1] = p.item_off[f] + (int64_t)p.per_step[f] * S;
+    p.fam_off[f + 1] = p.fam_off[f] + pl.count[f];
+  }
+  p.tok = reinterpret_cast<uint32_t *>(w + L.tok);
+  p.rank = reinterpret_cast<uint32_t *>(w + L.rank);
+  p.blk = reinterpret_cast<uint32_t *>(w + L.blk);
+  p.n_blk = L.n_blk;
+  p.err = reinterpret_cast<uint32_t *>(w);
+  p.o_step = out->step;
+  p.o_m = out->m;
+  p.o_n = out->n;
+  p.o_k = out->k;
+  p.o_a = out->a;
+  p.o_b = out->b;
+  p.o_mult = out->mult;
+  p.o_layers = out->layers;
+  p.o_hidden = out->hidden;
+  p.o_tp = out->tp;
+  p.o_nlaunch = out->n_launch;
+  hipError_t e = ks::launch_clear(p.err, nullptr, 0, stream);
+  if (e != hipSuccess) return hip_fail(e, "clear launch");
+  e = ks::launch_expand(p, stream);
+  if (e != hipSuccess) return hip_fail(e, "expansion launch");
+  return KS_OK;
 }
 
 const char *ks_last_error(void) { return g_err.c_str(); }

@@ -1,0 +1,192 @@
+// Batch expansion on gfx950: the batch descriptors of consecutive steps
+// (request lists, prefill flags) -> the records of every kernel each step
+// dispatches, family-major, in the layout the evaluation kernel streams
+// (Sec. 4.1: the scheduler's batch descriptor; Sec. 5.7: one embedding and
+// one LM head per step around L homogeneous layers; Sec. 5.8: GEMMs, norms
+// and activations over the step's T tokens, attention over its requests).
+//
+//   k_expand_steps    per step: T = sum q_r (16 lanes per step), the
+//                     per-step model record (L, D, P, launches)
+//   k_expand_rank     per block of 1024 steps: each step's count of earlier
+//                     prefill steps in the block, and the block's total
+//   k_expand_scan     one workgroup: exclusive prefix of the block totals
+//                     (and their sum checked against n_prefill)
+//   k_expand_records  one thread per record: step and slot from the item
+//                     index, fields from the family's templates, stores to
+//                     the record arrays (HBM write stream)
+#include <hip/hip_runtime.h>
+
+#include "ks_internal.h"
+
+namespace ks {
+
+constexpr int kTokLanes = 16;
+
+__global__ __launch_bounds__(256) void k_expand_steps(ExpandParams p) {
+  const int sub = threadIdx.x & (kTokLanes - 1);
+  const int64_t groups = ((int64_t)gridDim.x * blockDim.x) / kTokLanes;
+  uint32_t bad = 0;
+  for (int64_t j = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kTokLanes; j < p.n_steps; j += groups) {
+    uint32_t r0 = p.req_off[j], r1 = p.req_off[j + 1];
+    if (r0 > r1 || (int64_t)r1 > p.n_req || (j == 0 && r0 != 0)) {
+      bad |= kErrReq;
+      r0 = r1 = 0;
+    }
+    uint64_t T = 0;
+    for (uint32_t r = r0 + sub; r < r1; r += kTokLanes) T += p.req_q[r];
+#pragma unroll
+    for (int off = kTokLanes / 2; off > 0; off >>= 1) T += __shfl_xor(T, off);
+    if (sub == 0) {
+      // T and top_k T feed record m fields (limit 2^24)
+      const uint64_t k = p.top_k > 1 ? p.top_k : 1;
+      if (T * k >= (1ull << 24)) bad |= kErrRange;
+      p.tok[j] = T >= (1ull << 32) ? 0xFFFFFFFFu : (uint32_t)T;
+      const bool pre = p.prefill[j] != 0;
+      p.o_layers[j] = p.L;
+      p.o_hidden[j] = p.D;
+      p.o_tp[j] = p.P;
+      p.o_nlaunch[j] = pre ? p.L : 0u;
+    }
+  }
+  if (bad) atomicOr(p.err, bad);
+}
+
+// In-block exclusive prefix of the prefill flags: thread t of block b owns
+// steps b 1024 + 4 t .. + 3.
+__global__ __launch_bounds__(256) void k_expand_rank(ExpandParams p) {
+  __shared__ uint32_t wsum[4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t j0 = (int64_t)blockIdx.x * kExpandBlk + 4 * tid;
+  uint32_t fl[4], cnt = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    fl[i] = (j0 + i < p.n_steps && p.prefill[j0 + i] != 0) ? 1u : 0u;
+    cnt += fl[i];
+  }
+  uint32_t incl = cnt;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t v = __shfl_up(incl, off);
+    if (lane >= off) incl += v;
+  }
+  if (lane == 63) wsum[wave] = incl;
+  __syncthreads();
+  uint32_t base = 0;
+  for (int w = 0; w < wave; ++w) base += wsum[w];
+  uint32_t excl = base + incl - cnt;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if (j0 + i < p.n_steps) p.rank[j0 + i] = excl;
+    excl += fl[i];
+  }
+  if (tid == 255) p.blk[blockIdx.x] = excl;
+}
+
+// Exclusive prefix of the block totals in place, 256 at a time; the grand
+// total must equal the batch's n_prefill.
+__global__ __launch_bounds__(256) void k_expand_scan(ExpandParams p) {
+  __shared__ uint32_t wsum[4];
+  __shared__ uint64_t carry_s;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  uint64_t carry = 0;
+  for (int64_t c0 = 0; c0 < p.n_blk; c0 += 256) {
+    const int64_t i = c0 + tid;
+    const uint32_t v = i < p.n_blk ? p.blk[i] : 0u;
+    uint32_t incl = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const uint32_t u = __shfl_up(incl, off);
+      if (lane >= off) incl += u;
+    }
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    uint32_t base = 0;
+    for (int w = 0; w < wave; ++w) base += wsum[w];
+    if (i < p.n_blk) p.blk[i] = (uint32_t)(carry + base + incl - v);
+    if (tid == 255) carry_s = carry + base + incl;
+    __syncthreads();
+    carry = carry_s;
+    __syncthreads();
+  }
+  if (tid == 0 && (int64_t)carry != p.n_prefill) atomicOr(p.err, kErrPrefill);
+}
+
+// One record per item.  Attention items are the (step, layer) pairs of all
+// steps: a prefill step's go to ATTN_PREFILL at its rank among prefill
+// steps, the others to ATTN_DECODE at their rank among the rest (an item
+// whose rank is beyond the family's records, when the flags disagree with
+// n_prefill, is not written).
+__global__ __launch_bounds__(256) void k_expand_records(ExpandParams p) {
+  const int64_t total = p.item_off[KS_NFAM];
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t n_pre = p.n_prefill, n_dec = p.n_steps - p.n_prefill;
+  uint32_t bad = 0;
+  int f = 0;
+  for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < total; g += stride) {
+    while (g >= p.item_off[f + 1]) ++f;
+    const uint32_t idx = (uint32_t)(g - p.item_off[f]);
+    const uint32_t ps = p.per_step[f];
+    const uint32_t j = idx / ps;
+    const uint32_t slot = idx - j * ps;
+    const uint32_t nt = p.n_tpl[f];
+    const uint32_t layer = slot / nt;
+    const ExpandTpl t = p.tpl[f][slot - layer * nt];
+    int64_t dst;
+    if (f == KS_ATTN_PREFILL) {
+      const int64_t r = (int64_t)p.blk[j / kExpandBlk] + p.rank[j];
+      if (p.prefill[j] != 0) {
+        dst = r < n_pre ? p.fam_off[KS_ATTN_PREFILL] + r * ps + slot : -1;
+      } else {
+        const int64_t rd = (int64_t)j - r;
+        dst = (rd >= 0 && rd < n_dec) ? p.fam_off[KS_ATTN_DECODE] + rd * ps + slot : -1;
+      }
+      if (dst < 0) {
+        bad |= kErrPrefill;
+        continue;
+      }
+    } else {
+      dst = p.fam_off[f] + idx;
+    }
+    uint32_t m = 0;
+    if (t.msrc == kMTok) {
+      m = p.tok[j];
+    } else if (t.msrc == kMTopk) {
+      m = p.tok[j] * p.top_k;
+    } else if (t.msrc == kMReq) {
+      const uint32_t r0 = p.req_off[j], r1 = p.req_off[j + 1];
+      m = r1 >= r0 ? r1 - r0 : 0u;
+    }
+    p.o_step[dst] = j;
+    p.o_m[dst] = m;
+    p.o_n[dst] = t.n;
+    p.o_k[dst] = t.k;
+    p.o_a[dst] = t.a;
+    p.o_b[dst] = t.grouped ? (j * p.L + layer) * p.E : 0u;
+    if (p.o_mult) p.o_mult[dst] = p.mult[f];
+  }
+  if (bad) atomicOr(p.err, bad);
+}
+
+static int grid_cap(int64_t n, int block, int cap) {
+  int64_t g = (n + block - 1) / block;
+  if (g < 1) g = 1;
+  return (int)(g < cap ? g : cap);
+}
+
+hipError_t launch_expand(const ExpandParams &p, hipStream_t s) {
+  if (p.n_steps == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_expand_steps, dim3(grid_cap(p.n_steps * kTokLanes, 256, 16384)), dim3(256), 0, s, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_expand_rank, dim3((unsigned)p.n_blk), dim3(256), 0, s, p);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_expand_scan, dim3(1), dim3(256), 0, s, p);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (p.item_off[KS_NFAM] == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_expand_records, dim3(grid_cap(p.item_off[KS_NFAM], 256, 8192)), dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
+}  // namespace ks

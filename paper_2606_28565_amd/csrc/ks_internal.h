@@ -22,6 +22,7 @@ enum : uint32_t {
   kErrRange = 8u,     // a shape or count outside the documented limits
   kErrOrder = 16u,    // steps decrease within a family
   kErrSpec = 32u,     // spec vector not usable
+  kErrPrefill = 64u,  // prefill flags disagree with the batch's n_prefill
 };
 
 // head kinds compiled into the evaluation kernel
@@ -50,6 +51,7 @@ struct EvalParams {
   const uint32_t *step, *m, *n, *k, *a, *b;
   const uint32_t *expert_rows;
   int64_t n_expert_rows;
+  const uint32_t *mult;        // [n_rows] dispatches per record, or NULL (1)
   const uint64_t *agg;         // [4][n_steps]: Q, KV, PAIRS, TILES
   int64_t n_steps;
   uint32_t elem_bytes;
@@ -95,6 +97,7 @@ struct FinishParams {
 
 struct ValidateParams {
   const uint32_t *step, *m, *n, *k, *a, *b;
+  const uint32_t *mult;                // nullable
   const uint32_t *expert_rows;
   int64_t n_expert_rows;
   int64_t n_rows;
@@ -108,6 +111,45 @@ struct ValidateParams {
   int32_t n_specs;
   uint32_t *err;
 };
+
+// ---- batch expansion
+// m of a record template: 0, the step's tokens T, top_k T, or its requests R
+enum : uint32_t { kMZero = 0, kMTok = 1, kMTopk = 2, kMReq = 3 };
+struct ExpandTpl {
+  uint32_t n, k, a, msrc, grouped;
+};
+constexpr int kExpandTpl = 4;         // templates per family and layer, at most
+constexpr int kExpandBlk = 1024;      // steps per block of the prefill-rank scan
+
+// Item space: family f (KS_ATTN_PREFILL stands for both attention families,
+// KS_ATTN_DECODE has no items) owns items [item_off[f], item_off[f+1]),
+// per_step[f] per step; item i of the family is step i / per_step[f] and
+// slot i % per_step[f], whose template is slot % n_tpl[f] and whose layer is
+// slot / n_tpl[f].
+struct ExpandParams {
+  const uint32_t *req_off, *req_q;
+  int64_t n_req;
+  const uint8_t *prefill;
+  int64_t n_steps, n_prefill;
+  uint32_t L, E, top_k, D, P;
+  int64_t item_off[KS_NFAM + 1];
+  uint32_t per_step[KS_NFAM];
+  uint32_t n_tpl[KS_NFAM];
+  uint32_t mult[KS_NFAM];
+  ExpandTpl tpl[KS_NFAM][kExpandTpl];
+  int64_t fam_off[KS_NFAM + 1];
+  // workspace
+  uint32_t *tok;     // [n_steps] T of each step
+  uint32_t *rank;    // [n_steps] prefill steps before it within its block
+  uint32_t *blk;     // [n_blk] prefill steps per block, then their exclusive prefix
+  int64_t n_blk;
+  uint32_t *err;
+  // outputs
+  uint32_t *o_step, *o_m, *o_n, *o_k, *o_a, *o_b, *o_mult;
+  uint32_t *o_layers, *o_hidden, *o_tp, *o_nlaunch;
+};
+
+hipError_t launch_expand(const ExpandParams &p, hipStream_t s);
 
 hipError_t launch_clear(uint32_t *err, uint32_t *range, int64_t n_range, hipStream_t s);
 hipError_t launch_spec_prep(const ks_spec *specs, int32_t n_specs, SpecC *out, uint32_t *err, hipStream_t s);

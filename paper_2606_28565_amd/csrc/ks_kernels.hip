@@ -1096,10 +1096,11 @@ __device__ __forceinline__ Tile locate(const EvalParams &p, int wt, int wave, in
 // the steps just before and after the tile within its family.
 struct Fields {
   uint32_t st, m, n, k, a, b, prev, next;
+  float mult;   // dispatches the record stands for (1 without a multiplicity array)
 };
 
 __device__ __forceinline__ Fields load_fields(const EvalParams &p, const Tile &t, int lane) {
-  Fields f = {0, 0, 0, 0, 0, 0, kNoKey, kNoKey};
+  Fields f = {0, 0, 0, 0, 0, 0, kNoKey, kNoKey, 1.0f};
   if (t.nvalid == 0) return f;
   // wave-uniform bases plus a 32-bit lane offset (no per-lane 64-bit
   // address arithmetic)
@@ -1114,6 +1115,7 @@ __device__ __forceinline__ Fields load_fields(const EvalParams &p, const Tile &t
   if (fam != KS_RMSNORM && fam != KS_SILU_MUL && fam != KS_EMBED) f.k = (p.k + r0)[off];
   if (grouped || attn) f.a = (p.a + r0)[off];
   if (grouped) f.b = (p.b + r0)[off];
+  if (p.mult) f.mult = (float)(p.mult + r0)[off];   // exact below 2^24
   if (t.row0 > t.fam_lo) f.prev = p.step[t.row0 - 1];
   if (t.row0 + kTileRows < t.fam_hi) f.next = p.step[t.row0 + kTileRows];
   return f;
@@ -1133,7 +1135,7 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
   int staged = -1;
   // the next tile's fields are loaded while the current one is evaluated
   Tile tn = {};
-  Fields fn = {0, 0, 0, 0, 0, 0, kNoKey, kNoKey};
+  Fields fn = {0, 0, 0, 0, 0, 0, kNoKey, kNoKey, 1.0f};
   if ((int)blockIdx.x < n_wgt) {
     tn = locate(p, blockIdx.x, wave, 0);
     fn = load_fields(p, tn, lane);
@@ -1262,7 +1264,9 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
         if (p.o_t) p.o_t[i] = t;
       }
       if (p.partial) {
-        const float v = seg_scan(live ? t : 0.0f, fac);
+        // a record of multiplicity m adds m t (the product is exact to fp32
+        // rounding; m is 1 without a multiplicity array)
+        const float v = seg_scan(live ? t * fc.mult : 0.0f, fac);
         if (dst) dst[(size_t)s * dst_stride] = (double)v;
       }
     }
@@ -1322,6 +1326,7 @@ __global__ void k_validate(ValidateParams p) {
     if (i > p.fam_off[f] && p.step[i - 1] > st) bad |= kErrOrder;
     const uint32_t m = p.m[i], n = p.n[i], k = p.k[i], a = p.a[i], b = p.b[i];
     if (m >= (1u << 24) || n >= (1u << 18) || k >= (1u << 18)) bad |= kErrRange;
+    if (p.mult && p.mult[i] >= (1u << 24)) bad |= kErrRange;
     if ((f == KS_ATTN_PREFILL || f == KS_ATTN_DECODE) && (n >= 4096u || k >= 4096u || a >= 4096u))
       bad |= kErrRange;
     if (f == KS_GROUPED_GEMM) {

@@ -24,7 +24,8 @@ def test_library_exports_every_declared_symbol():
     lib = abi.load()
     names = _declared_functions()
     assert {"ks_eval_kernels", "ks_eval_steps", "ks_workspace_bytes", "ks_validate",
-            "ks_device_status", "ks_last_error", "ks_version"} <= set(names)
+            "ks_device_status", "ks_last_error", "ks_version", "ks_expand", "ks_expand_layout",
+            "ks_expand_workspace_bytes"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
     assert abi.ks_version().startswith("ks ")
@@ -35,7 +36,8 @@ def test_struct_layout_matches_header(tmp_path):
     with the ctypes mirrors."""
     structs = {"ks_desc": abi.ks_desc, "ks_spec": abi.ks_spec, "ks_heads": abi.ks_heads,
                "ks_steps": abi.ks_steps, "ks_host": abi.ks_host,
-               "ks_kernel_out": abi.ks_kernel_out, "ks_step_out": abi.ks_step_out}
+               "ks_kernel_out": abi.ks_kernel_out, "ks_step_out": abi.ks_step_out,
+               "ks_model": abi.ks_model, "ks_batch": abi.ks_batch, "ks_records": abi.ks_records}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "ks.h"', "int main(void){"]
     for s, cls in structs.items():
         lines.append(f'printf("{s} size %zu\\n", sizeof({s}));')
@@ -165,3 +167,85 @@ def test_missing_library_fails_loudly(tmp_path):
             abi.load(str(tmp_path / "nope.so"))
         finally:
             abi._lib = saved
+
+
+# ---- batch expansion (host side only)
+def _model(**kw):
+    from workload import gen
+    base = dict(hidden=4096, layers=32, q_heads=32, kv_heads=8, head_dim=128, ffn=11008, vocab=32000,
+                tp=1, experts=0, top_k=0, expert_ffn=0, kv_write=0)
+    base.update(kw)
+    return abi.ks_model(*(base[n] for n in abi.MODEL_FIELDS))
+
+
+def test_expand_layout_closed_form_counts():
+    """Record counts per family for a dense and an MoE model, both modes,
+    against the oracle's closed form (host arithmetic only)."""
+    from types import SimpleNamespace
+    from oracle import ks_expand as ox
+    cases = [dict(), dict(kv_write=1, tp=4), dict(experts=8, top_k=2, expert_ffn=14336, ffn=0),
+             dict(kv_heads=2, tp=8, q_heads=64, ffn=28672, layers=80, hidden=8192)]
+    for kw in cases:
+        md = _model(**kw)
+        shape = SimpleNamespace(**{n: getattr(md, n) for n in abi.MODEL_FIELDS})
+        for mode in (abi.KS_EXPAND_PER_LAYER, abi.KS_EXPAND_HOMOGENEOUS):
+            for S, npre in ((0, 0), (1, 1), (1000, 297), (88_640, 26_000)):
+                _, fo = abi.ks_expand_layout(md, S, npre, mode)
+                want = ox.family_counts(shape, S, npre, mode == abi.KS_EXPAND_HOMOGENEOUS)
+                assert [fo[f + 1] - fo[f] for f in range(abi.NFAM)] == list(want), (kw, mode, S)
+
+
+@pytest.mark.parametrize("kw,status,needle", [
+    (dict(tp=3), abi.KS_EINVAL, "q_heads"),
+    (dict(vocab=32001, tp=2, q_heads=32), abi.KS_EINVAL, "vocab"),
+    (dict(ffn=11007, tp=2), abi.KS_EINVAL, "ffn"),
+    (dict(layers=0), abi.KS_EINVAL, "layers"),
+    (dict(experts=2000, top_k=2, expert_ffn=64), abi.KS_ERANGE, "experts"),
+    (dict(experts=8, top_k=9, expert_ffn=64), abi.KS_EINVAL, "top_k"),
+    (dict(ffn=300000), abi.KS_ERANGE, "2^18"),
+    (dict(head_dim=4096), abi.KS_ERANGE, "2^12"),
+    (dict(kv_write=2), abi.KS_EINVAL, "kv_write"),
+])
+def test_expand_layout_rejects_bad_models(kw, status, needle):
+    st, _ = abi.ks_expand_layout(_model(**kw), 10, 2, 0, check=False)
+    assert st == status and needle in abi.ks_last_error()
+
+
+def test_expand_layout_rejects_bad_counts():
+    md = _model()
+    assert abi.ks_expand_layout(md, 10, 11, 0, check=False)[0] == abi.KS_EINVAL
+    assert abi.ks_expand_layout(md, -1, 0, 0, check=False)[0] == abi.KS_ERANGE
+    assert abi.ks_expand_layout(md, 10, 2, 7, check=False)[0] == abi.KS_EINVAL
+    # more records than the u32 record index allows
+    assert abi.ks_expand_layout(md, 20_000_000, 0, 0, check=False)[0] == abi.KS_ERANGE
+    # MoE routed-row offsets must fit u32
+    moe = _model(experts=1024, top_k=2, expert_ffn=1024, ffn=0, layers=80)
+    assert abi.ks_expand_layout(moe, 60_000, 0, 1, check=False)[0] == abi.KS_ERANGE
+    assert abi.ks_expand_workspace_bytes(-1) == 0
+    assert abi.ks_expand_workspace_bytes(5000) >= 256 + 2 * 4 * 5000
+
+
+def test_expand_host_checks():
+    md = _model()
+    out = abi.ks_records()
+    ws = C.create_string_buffer(1 << 16)
+    wsp = (C.addressof(ws) + 255) & ~255
+    b = abi.ks_batch(4, None, None, 0, None, 1)
+    assert abi.ks_expand(md, b, 0, out, wsp, 1 << 15, None, check=False) == abi.KS_EINVAL
+    assert "req_off" in abi.ks_last_error()
+    b.req_off = 16
+    assert abi.ks_expand(md, b, 0, out, wsp, 1 << 15, None, check=False) == abi.KS_EINVAL
+    assert "prefill" in abi.ks_last_error()
+    b.prefill = 16
+    assert abi.ks_expand(md, b, 0, out, wsp, 1 << 15, None, check=False) == abi.KS_EINVAL
+    assert "record output" in abi.ks_last_error()
+    for name in ("step", "m", "n", "k", "a", "b"):
+        setattr(out, name, 16)
+    assert abi.ks_expand(md, b, 1, out, wsp, 1 << 15, None, check=False) == abi.KS_EINVAL
+    assert "mult" in abi.ks_last_error()
+    assert abi.ks_expand(md, b, 0, out, wsp, 1 << 15, None, check=False) == abi.KS_EINVAL
+    assert "per-step" in abi.ks_last_error()
+    for name in ("layers", "hidden", "tp", "n_launch"):
+        setattr(out, name, 16)
+    assert abi.ks_expand(md, b, 0, out, wsp, 8, None, check=False) == abi.KS_EWORKSPACE
+    assert abi.ks_expand(md, b, 0, out, wsp + 8, 1 << 15, None, check=False) == abi.KS_EWORKSPACE
