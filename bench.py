@@ -36,19 +36,30 @@ C5_BATCH_STEPS = 88_640      # 88,640 steps x 722 kernels = 64.0 M records
 
 
 def _workload(name: str):
-    """(workload, description, oracle sample) for each benchmark workload.
-    The oracle sample bounds the CPU baseline to ~10-30 s of work."""
+    """(workload, description, oracle sample, batch traces) for each benchmark
+    workload.  The oracle sample bounds the CPU baseline to ~10-30 s of
+    work; the traces are the batch descriptors the records come from."""
     from workload import gen
     if name == "c4":
         return (gen.config4(), "c4-capacity-grid: llama-7b c1 trace + S2 trace prefix, 256 specs",
-                {"specs": 16, "steps": None})
+                {"specs": 16, "steps": None},
+                [gen.trace_c1(), gen.trace_c2(1).slice(0, gen.C4_GRID_STEPS)])
     if name == "c1":
-        return gen.config1(), "c1-llama7b: 1000 steps, 2 datasheet specs, fp32 heads", {"specs": 2, "steps": None}
+        return (gen.config1(), "c1-llama7b: 1000 steps, 2 datasheet specs, fp32 heads", {"specs": 2, "steps": None},
+                [gen.trace_c1()])
     if name == "c5-batch":
         wl = gen.config5(0, C5_BATCH_STEPS)
         return (wl, f"c5-70b-prefix: one 64M-record batch (steps 0..{C5_BATCH_STEPS}), 2 datasheet specs, "
-                    "bf16 32-256-256 heads", {"specs": 2, "steps": 300})
+                    "bf16 32-256-256 heads", {"specs": 2, "steps": 300},
+                [gen.trace_c5().slice(0, C5_BATCH_STEPS)])
     raise SystemExit(f"unknown workload {name}")
+
+
+def expand_bytes(n_records: int, n_steps: int, with_mult: bool) -> float:
+    """Algorithmic HBM bytes of the expansion's record writer: six u32 fields
+    per record (seven with the multiplicity) written, and per step the token
+    count, the prefill flag and the request offset it reads."""
+    return n_records * 4.0 * (7 if with_mult else 6) + n_steps * 9.0
 
 
 def kernel_source_hash() -> str:
@@ -140,6 +151,26 @@ def cpu_baseline(wl, sample: dict, eta_one: bool, threads: int, bounded=None):
                       f"({pairs} predictions, {dt:.1f} s, fp64 numpy, {threads} BLAS threads)"}
 
 
+def _print_expand_only(args, wl, wdesc, db, ms, k_ms) -> int:
+    hom = args.expand == "homogeneous"
+    eb = expand_bytes(db.fam_off[-1], db.desc.n_steps, hom)
+    out = {
+        "metric": "kernel records expanded/s", "value": db.fam_off[-1] / (ms * 1e-3), "unit": "records/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u32", "data": "synthetic",
+        "config": {"workload": wdesc + " (batch expansion only, "
+                               + ("homogeneous" if hom else "per-layer") + " records)",
+                   "records": db.fam_off[-1], "serving_steps": db.desc.n_steps},
+        "roofline": {"bound": "hbm", "achieved": eb / (k_ms * 1e-3) / 1e9, "peak": PEAK["hbm"] / 1e9,
+                     "unit": "GB/s", "frac": eb / (k_ms * 1e-3) / PEAK["hbm"], "traffic": None,
+                     "kernel_ms": k_ms,
+                     "note": "achieved = record bytes written (+ per-step inputs read) by the record "
+                             "writer / its mean HIP-event duration"},
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -151,6 +182,12 @@ def main() -> int:
     ap.add_argument("--bounded", default="none", choices=["none", "mixed", "all"],
                     help="families on the bounded analytical head: none; the GEMMs, embedding and "
                          "KV writes (mixed, the rest on the MLP or eta = 1); or all")
+    ap.add_argument("--expand", default="none", choices=["none", "per-layer", "homogeneous"],
+                    help="start from the batch descriptors: each step runs ks_expand (one record "
+                         "per dispatched kernel, or layer-identical kernels as one record of "
+                         "multiplicity L) and then ks_eval_steps on its records")
+    ap.add_argument("--expand-only", action="store_true",
+                    help="time ks_expand alone (the records are not evaluated)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -177,7 +214,7 @@ def main() -> int:
         return 0
 
     print(f"[bench] generating workload {args.workload}", file=sys.stderr, flush=True)
-    wl, wdesc, sample = _workload(args.workload)
+    wl, wdesc, sample, traces = _workload(args.workload)
     from workload import gen
     bmask = {"none": 0, "mixed": gen.BOUNDED_MIXED, "all": gen.BOUNDED_ALL}[args.bounded]
     bounded = gen.make_bounded(bmask) if bmask else None
@@ -190,10 +227,65 @@ def main() -> int:
     else:
         ko = None
     stream = abi.current_stream()
+    db = None
+    if args.expand != "none" or args.expand_only:
+        if len(traces) != 1:
+            raise SystemExit("--expand needs a single-model workload (c1 or c5-batch)")
+        if args.per_pair and args.expand == "homogeneous":
+            raise SystemExit("--per-pair outputs follow one record per dispatch; not with --expand homogeneous")
+        mode = abi.KS_EXPAND_HOMOGENEOUS if args.expand == "homogeneous" else abi.KS_EXPAND_PER_LAYER
+        db = abi.DeviceBatch(traces[0], mode)
+        ews = torch.empty(abi.ks_workspace_bytes(db.desc, di.n_specs) + 256, dtype=torch.uint8,
+                          device="cuda")
+        ews_ptr = ews.data_ptr() + (-ews.data_ptr()) % 256
+        ews_bytes = abi.ks_workspace_bytes(db.desc, di.n_specs)
 
     def step():
+        if db is not None:
+            db.expand(stream)
+            if args.expand_only:
+                return
+            abi.ks_eval_steps(db.desc, db.steps, di.specs_ptr, di.n_specs, heads, di.host, so, ko,
+                              ews_ptr, ews_bytes, stream)
+            return
         abi.ks_eval_steps(di.desc, di.steps, di.specs_ptr, di.n_specs, heads, di.host, so, ko,
                           di.ws_ptr, di.ws_bytes, stream)
+
+    def kernel_ms(n: int) -> float:
+        """Mean duration of the call's main kernel (the evaluation kernel, or
+        the expansion's record writer with --expand-only) over n calls, from
+        HIP events the library records around that launch on the stream."""
+        ev = abi.HipEvents(2 * n)
+        try:
+            for i in range(n):
+                if db is not None and not args.expand_only:
+                    db.expand(stream)       # untimed: the hook brackets the evaluation kernel
+                    abi.ks_set_timing_events(ev.ev[2 * i], ev.ev[2 * i + 1])
+                    abi.ks_eval_steps(db.desc, db.steps, di.specs_ptr, di.n_specs, heads, di.host, so, ko,
+                                      ews_ptr, ews_bytes, stream)
+                else:
+                    abi.ks_set_timing_events(ev.ev[2 * i], ev.ev[2 * i + 1])
+                    step()
+                abi.ks_set_timing_events(None, None)
+            abi.ks_set_timing_events(None, None)
+            torch.cuda.synchronize()
+            return sum(ev.elapsed_ms(2 * i, 2 * i + 1) for i in range(n)) / n
+        finally:
+            abi.ks_set_timing_events(None, None)
+            ev.close()
+
+    def expand_kernel_ms(n: int) -> float:
+        ev = abi.HipEvents(2 * n)
+        try:
+            for i in range(n):
+                abi.ks_set_timing_events(ev.ev[2 * i], ev.ev[2 * i + 1])
+                db.expand(stream)
+            abi.ks_set_timing_events(None, None)
+            torch.cuda.synchronize()
+            return sum(ev.elapsed_ms(2 * i, 2 * i + 1) for i in range(n)) / n
+        finally:
+            abi.ks_set_timing_events(None, None)
+            ev.close()
 
     print(f"[bench] {wl.desc.n_rows} records x {di.n_specs} specs; warmup {args.warmup}",
           file=sys.stderr, flush=True)
@@ -212,25 +304,50 @@ def main() -> int:
     torch.cuda.synchronize()
     ms = ev0.elapsed_time(ev1) / args.steps
     print(f"[bench] {args.steps} steps: {ms:.3f} ms/step", file=sys.stderr, flush=True)
+    if db is not None:
+        abi.ks_device_status(db.ws_ptr, db.ws_bytes, stream)
+    # the main kernel alone, in a second pass of as many calls (the timed
+    # region above has no extra event records)
+    k_ms = kernel_ms(args.steps)
+    print(f"[bench] main kernel: {k_ms:.3f} ms/launch", file=sys.stderr, flush=True)
 
+    if args.expand_only:
+        return _print_expand_only(args, wl, wdesc, db, ms, k_ms)
+    exp = None
+    if db is not None:
+        e_ms = expand_kernel_ms(args.steps)
+        hom = args.expand == "homogeneous"
+        eb = expand_bytes(db.fam_off[-1], db.desc.n_steps, hom)
+        exp = {"form": args.expand, "records": db.fam_off[-1], "records_kernel_ms": e_ms,
+               "roofline": {"bound": "hbm", "achieved": eb / (e_ms * 1e-3) / 1e9, "peak": PEAK["hbm"] / 1e9,
+                            "unit": "GB/s", "frac": eb / (e_ms * 1e-3) / PEAK["hbm"], "traffic": None}}
     pairs = wl.desc.n_rows * di.n_specs
     value = pairs / (ms * 1e-3)
     step_evals = wl.desc.n_steps * di.n_specs / (ms * 1e-3)
     # records on the MLP: the families outside the bounded mask
     import numpy as np
     on_mlp = ((bmask >> wl.desc.family()) & 1) == 0
+    eval_desc = db.desc if db is not None else None
+    if db is not None and args.expand == "homogeneous":
+        # the evaluation sees the homogeneous records (one per layer-identical
+        # kernel): its work is per record, while value counts dispatches
+        n_eval = db.fam_off[-1]
+        on_mlp_n = n_eval - sum(db.fam_off[f + 1] - db.fam_off[f] for f in range(gen.NFAM) if (bmask >> f) & 1)
+    else:
+        n_eval = wl.desc.n_rows
+        on_mlp_n = int(np.count_nonzero(on_mlp))
     if args.eta_one or bmask == gen.BOUNDED_ALL:
-        alg = stream_bytes(wl, di.n_specs)
+        alg = stream_bytes(wl, di.n_specs) if eval_desc is None or args.expand != "homogeneous" else None
         bound, unit, peak = "hbm", "GB/s", PEAK["hbm"] / 1e9
-        achieved = alg / (ms * 1e-3) / 1e9
+        achieved = alg / (k_ms * 1e-3) / 1e9 if alg is not None else None
         dtype = "f32"
     else:
         per_pair = head_flops_per_pair(wl.heads.in_dim, wl.heads.hidden)
-        alg = float(int(np.count_nonzero(on_mlp)) * di.n_specs) * per_pair
+        alg = float(on_mlp_n * di.n_specs) * per_pair
         bf16 = wl.heads.precision == "bf16"
         bound, unit = "mfma", "TFLOP/s"
         peak = (PEAK["bf16"] if bf16 else PEAK["f32"]) / 1e12
-        achieved = alg / (ms * 1e-3) / 1e12
+        achieved = alg / (k_ms * 1e-3) / 1e12
         dtype = "bf16" if bf16 else "f32"
 
     out = {
@@ -243,16 +360,22 @@ def main() -> int:
                    "head": ("eta=1" if args.eta_one else
                             f"{wl.heads.precision} {wl.heads.in_dim}-{wl.heads.hidden}-{wl.heads.hidden}-1")
                            + ("" if not bmask else f"; bounded head on families 0x{bmask:03x}"),
-                   "per_pair_outputs": bool(args.per_pair)},
+                   "per_pair_outputs": bool(args.per_pair),
+                   "input": ("batch descriptors, expanded on the GPU every step ("
+                             + args.expand + " records)") if db is not None else "kernel records"},
         "step_evals_per_s": step_evals,
         "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
-                     "frac": achieved / peak,
+                     "frac": achieved / peak if achieved is not None else None,
                      "traffic": (recorded_traffic(f"{args.workload}{'-eta1' if args.eta_one else ''}")
-                                 if not bmask else None),
-                     "note": "achieved = algorithmic work of the evaluation kernel per call "
-                             "(FLOPs of the head, or the bytes the model reads and writes) / HIP-event "
-                             "time of the whole call (all of its kernels)"},
+                                 if not bmask and db is None else None),
+                     "kernel_ms": k_ms, "evaluated_records": n_eval,
+                     "note": "achieved = algorithmic work of one evaluation-kernel launch (FLOPs of the "
+                             "head over the records it evaluates, or the bytes the model reads and "
+                             "writes) / that kernel's mean duration from HIP events recorded around "
+                             "its launch on the call's stream"},
     }
+    if exp is not None:
+        out["expand"] = exp
     if not args.no_cpu_baseline:
         threads = args.cpu_threads or min(16, os.cpu_count() or 1)
         print(f"[bench] cpu baseline: oracle on {sample}, {threads} threads", file=sys.stderr, flush=True)

@@ -316,6 +316,15 @@ ks_status ks_validate(const ks_desc* desc, const ks_steps* steps,
  * workspace's last evaluation (or expansion) call started (KS_OK if none). */
 ks_status ks_device_status(const void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Measurement hook for benchmarks: with both events non-NULL, every later
+ * call on this thread of ks_eval_kernels / ks_eval_steps records `before` on
+ * its stream right before the evaluation kernel and `after` right after it,
+ * and every ks_expand call does the same around its record-writing kernel,
+ * so hipEventElapsedTime(before, after) is that one kernel's duration.
+ * Calling it with NULLs turns the hook off.  The events are the caller's
+ * (created with timing enabled, never destroyed by the library). */
+ks_status ks_set_timing_events(hipEvent_t before, hipEvent_t after);
+
 /* Message of the last non-OK status returned on this thread. */
 const char* ks_last_error(void);
 

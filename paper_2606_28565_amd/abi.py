@@ -127,6 +127,8 @@ def load(path: str = LIB_PATH) -> C.CDLL:
     lib.ks_expand.argtypes = [C.POINTER(ks_model), C.POINTER(ks_batch), C.c_int32,
                               C.POINTER(ks_records), P, C.c_size_t, P]
     lib.ks_expand.restype = C.c_int
+    lib.ks_set_timing_events.argtypes = [P, P]
+    lib.ks_set_timing_events.restype = C.c_int
     lib.ks_last_error.argtypes = []
     lib.ks_last_error.restype = C.c_char_p
     lib.ks_version.argtypes = []
@@ -191,6 +193,41 @@ def ks_expand_workspace_bytes(n_steps: int) -> int:
 def ks_expand(model, batch, mode, out, ws_ptr, ws_bytes, stream, check=True):
     st = load().ks_expand(C.byref(model), C.byref(batch), mode, C.byref(out), ws_ptr, ws_bytes, stream)
     return _check(st) if check else st
+
+
+def ks_set_timing_events(before, after, check=True):
+    """before, after: raw hipEvent_t handles (see HipEvents), or None."""
+    st = load().ks_set_timing_events(before, after)
+    return _check(st) if check else st
+
+
+class HipEvents:
+    """A pool of timing-enabled HIP events, created and read through the HIP
+    runtime directly (for ks_set_timing_events)."""
+
+    def __init__(self, n: int):
+        import torch  # noqa: F401  (initialises the runtime)
+        self.rt = C.CDLL("libamdhip64.so")
+        self.rt.hipEventCreate.argtypes = [C.POINTER(C.c_void_p)]
+        self.rt.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), C.c_void_p, C.c_void_p]
+        self.rt.hipEventDestroy.argtypes = [C.c_void_p]
+        self.ev = []
+        for _ in range(n):
+            h = C.c_void_p()
+            if self.rt.hipEventCreate(C.byref(h)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+            self.ev.append(h.value)
+
+    def elapsed_ms(self, a: int, b: int) -> float:
+        ms = C.c_float()
+        if self.rt.hipEventElapsedTime(C.byref(ms), self.ev[a], self.ev[b]) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return ms.value
+
+    def close(self):
+        for h in self.ev:
+            self.rt.hipEventDestroy(h)
+        self.ev = []
 
 
 def ks_last_error() -> str:

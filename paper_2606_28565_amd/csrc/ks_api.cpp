@@ -14,6 +14,20 @@
 namespace {
 
 thread_local std::string g_err;
+// measurement hook (ks_set_timing_events)
+thread_local hipEvent_t g_ev_before = nullptr, g_ev_after = nullptr;
+
+// the evaluation kernel, bracketed by the hook's events when they are set
+hipError_t timed_eval(int kind, const ks::EvalParams &p, hipStream_t s) {
+  const bool timed = g_ev_before && g_ev_after;
+  if (timed) {
+    const hipError_t e = hipEventRecord(g_ev_before, s);
+    if (e != hipSuccess) return e;
+  }
+  const hipError_t e = ks::launch_eval(kind, p, s);
+  if (e != hipSuccess) return e;
+  return timed ? hipEventRecord(g_ev_after, s) : hipSuccess;
+}
 
 ks_status fail(ks_status st, const char *fmt, ...) {
   char buf[512];
@@ -388,7 +402,7 @@ ks_status ks_eval_kernels(const ks_desc *desc, const ks_spec *specs, int32_t n_s
   if (st != KS_OK) return st;
   ks::EvalParams p;
   fill_eval(p, desc, specs, n_specs, heads, out, w, L);
-  hipError_t e = ks::launch_eval(kind, p, stream);
+  hipError_t e = timed_eval(kind, p, stream);
   if (e != hipSuccess) return hip_fail(e, "evaluation launch");
   return KS_OK;
 }
@@ -419,7 +433,7 @@ ks_status ks_eval_steps(const ks_desc *desc, const ks_steps *steps, const ks_spe
   p.partial = reinterpret_cast<double *>(w + L.partial);
   p.carry = reinterpret_cast<double *>(w + L.carry);
   p.range = reinterpret_cast<uint32_t *>(w + L.range);
-  hipError_t e = ks::launch_eval(kind, p, stream);
+  hipError_t e = timed_eval(kind, p, stream);
   if (e != hipSuccess) return hip_fail(e, "evaluation launch");
 
   ks::FinishParams f;
@@ -584,8 +598,15 @@ ks_status ks_expand(const ks_model *model, const ks_batch *batch, int32_t mode, 
   p.o_nlaunch = out->n_launch;
   hipError_t e = ks::launch_clear(p.err, nullptr, 0, stream);
   if (e != hipSuccess) return hip_fail(e, "clear launch");
-  e = ks::launch_expand(p, stream);
+  e = ks::launch_expand(p, stream, g_ev_before, g_ev_after);
   if (e != hipSuccess) return hip_fail(e, "expansion launch");
+  return KS_OK;
+}
+
+ks_status ks_set_timing_events(hipEvent_t before, hipEvent_t after) {
+  if ((before == nullptr) != (after == nullptr)) return fail(KS_EINVAL, "set both timing events or neither");
+  g_ev_before = before;
+  g_ev_after = after;
   return KS_OK;
 }
 

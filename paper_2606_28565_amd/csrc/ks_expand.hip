@@ -173,7 +173,7 @@ static int grid_cap(int64_t n, int block, int cap) {
   return (int)(g < cap ? g : cap);
 }
 
-hipError_t launch_expand(const ExpandParams &p, hipStream_t s) {
+hipError_t launch_expand(const ExpandParams &p, hipStream_t s, hipEvent_t before, hipEvent_t after) {
   if (p.n_steps == 0) return hipSuccess;
   hipLaunchKernelGGL(k_expand_steps, dim3(grid_cap(p.n_steps * kTokLanes, 256, 16384)), dim3(256), 0, s, p);
   hipError_t e = hipGetLastError();
@@ -184,9 +184,16 @@ hipError_t launch_expand(const ExpandParams &p, hipStream_t s) {
   hipLaunchKernelGGL(k_expand_scan, dim3(1), dim3(256), 0, s, p);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (p.item_off[KS_NFAM] == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_expand_records, dim3(grid_cap(p.item_off[KS_NFAM], 256, 8192)), dim3(256), 0, s, p);
-  return hipGetLastError();
+  if (before && after) {
+    e = hipEventRecord(before, s);
+    if (e != hipSuccess) return e;
+  }
+  if (p.item_off[KS_NFAM] > 0) {
+    hipLaunchKernelGGL(k_expand_records, dim3(grid_cap(p.item_off[KS_NFAM], 256, 8192)), dim3(256), 0, s, p);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return before && after ? hipEventRecord(after, s) : hipSuccess;
 }
 
 }  // namespace ks

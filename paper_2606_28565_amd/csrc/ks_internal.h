@@ -149,7 +149,8 @@ struct ExpandParams {
   uint32_t *o_layers, *o_hidden, *o_tp, *o_nlaunch;
 };
 
-hipError_t launch_expand(const ExpandParams &p, hipStream_t s);
+// events recorded around the record-writing kernel (both null: none)
+hipError_t launch_expand(const ExpandParams &p, hipStream_t s, hipEvent_t before, hipEvent_t after);
 
 hipError_t launch_clear(uint32_t *err, uint32_t *range, int64_t n_range, hipStream_t s);
 hipError_t launch_spec_prep(const ks_spec *specs, int32_t n_specs, SpecC *out, uint32_t *err, hipStream_t s);

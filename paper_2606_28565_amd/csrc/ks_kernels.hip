@@ -1099,6 +1099,7 @@ struct Fields {
   float mult;   // dispatches the record stands for (1 without a multiplicity array)
 };
 
+template <bool MULT>
 __device__ __forceinline__ Fields load_fields(const EvalParams &p, const Tile &t, int lane) {
   Fields f = {0, 0, 0, 0, 0, 0, kNoKey, kNoKey, 1.0f};
   if (t.nvalid == 0) return f;
@@ -1115,16 +1116,21 @@ __device__ __forceinline__ Fields load_fields(const EvalParams &p, const Tile &t
   if (fam != KS_RMSNORM && fam != KS_SILU_MUL && fam != KS_EMBED) f.k = (p.k + r0)[off];
   if (grouped || attn) f.a = (p.a + r0)[off];
   if (grouped) f.b = (p.b + r0)[off];
-  if (p.mult) f.mult = (float)(p.mult + r0)[off];   // exact below 2^24
+  if constexpr (MULT) f.mult = (float)(p.mult + r0)[off];   // exact below 2^24
   if (t.row0 > t.fam_lo) f.prev = p.step[t.row0 - 1];
   if (t.row0 + kTileRows < t.fam_hi) f.next = p.step[t.row0 + kTileRows];
   return f;
 }
 
-// GRID: compiled with Tier B routing (a separate instantiation, so the
-// kernels without a grid keep their registers)
-template <int KIND, bool GRID>
+// Variants, each a separate instantiation so that the kernels without them
+// keep their registers and schedule: kVarGrid compiles Tier B routing in,
+// kVarMult weights each record's step-sum term by its multiplicity.
+enum : int { kVarGrid = 1, kVarMult = 2, kNumVars = 4 };
+
+template <int KIND, int VAR>
 __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalParams p) {
+  constexpr bool GRID = (VAR & kVarGrid) != 0;
+  constexpr bool MULT = (VAR & kVarMult) != 0;
   using H = typename KindOf<KIND>::H;
   constexpr int IN = KindOf<KIND>::IN;
   __shared__ uint32_t lds[H::LDS_DW];
@@ -1138,14 +1144,14 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
   Fields fn = {0, 0, 0, 0, 0, 0, kNoKey, kNoKey, 1.0f};
   if ((int)blockIdx.x < n_wgt) {
     tn = locate(p, blockIdx.x, wave, 0);
-    fn = load_fields(p, tn, lane);
+    fn = load_fields<MULT>(p, tn, lane);
   }
   for (int wt = blockIdx.x; wt < n_wgt; wt += gridDim.x) {
     const Tile tc = tn;
     const Fields fc = fn;
     if (wt + (int)gridDim.x < n_wgt) {
       tn = locate(p, wt + gridDim.x, wave, tc.fam);
-      fn = load_fields(p, tn, lane);
+      fn = load_fields<MULT>(p, tn, lane);
     }
     const int fam = tc.fam;
     // this family takes the bounded head (the plain eta = 1 stream has none)
@@ -1217,6 +1223,13 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
     // (spec, family, step) partial.
     float fac[7];
     seg_factors(key, fac);
+    // the scan input is m t for a live record of multiplicity m (1 without
+    // a multiplicity array) and 0 otherwise: one product per spec instead
+    // of a select.  A lane that is not live either repeats lane 0's record
+    // (a tail lane past nvalid, whose t is finite whenever lane 0's is) or
+    // is flagged bad data; both sit at or after the wave's last live lane or
+    // carry a flagged record, so the scan of every live segment is unchanged.
+    const float tfac = MULT ? (live ? fc.mult : 0.0f) : 0.0f;
     double *dst = nullptr;
     size_t dst_stride = 0;
     if (p.partial && is_tail) {
@@ -1264,9 +1277,8 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
         if (p.o_t) p.o_t[i] = t;
       }
       if (p.partial) {
-        // a record of multiplicity m adds m t (the product is exact to fp32
-        // rounding; m is 1 without a multiplicity array)
-        const float v = seg_scan(live ? t * fc.mult : 0.0f, fac);
+        // a record of multiplicity m adds m t (one fp32 rounding)
+        const float v = seg_scan(MULT ? t * tfac : (live ? t : 0.0f), fac);
         if (dst) dst[(size_t)s * dst_stride] = (double)v;
       }
     }
@@ -1388,18 +1400,18 @@ hipError_t launch_spec_prep(const ks_spec *specs, int32_t n_specs, SpecC *out, u
 // count), so no workgroup of the head kinds waits for another to finish.
 // Cached per device and kernel.
 constexpr int kMaxDevices = 64;
-static std::atomic<int> g_resident[kMaxDevices][kNumKinds][2];
+static std::atomic<int> g_resident[kMaxDevices][kNumKinds][kNumVars];
 
-template <int KIND, bool GRID>
+template <int KIND, int VAR>
 static hipError_t resident_wgs(int *out) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
-  std::atomic<int> *slot = dev < kMaxDevices ? &g_resident[dev][KIND][GRID] : nullptr;
+  std::atomic<int> *slot = dev < kMaxDevices ? &g_resident[dev][KIND][VAR] : nullptr;
   int r = slot ? slot->load(std::memory_order_relaxed) : 0;
   if (r == 0) {
     int per_cu = 0, n_cu = 0;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_eval<KIND, GRID>, kWgThreads, 0);
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_eval<KIND, VAR>, kWgThreads, 0);
     if (e != hipSuccess) return e;
     e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
@@ -1413,14 +1425,14 @@ static hipError_t resident_wgs(int *out) {
   return hipSuccess;
 }
 
-template <int KIND, bool GRID>
+template <int KIND, int VAR>
 static hipError_t launch_grid(const EvalParams &p, hipStream_t s) {
   int cap = 0;
-  const hipError_t e = resident_wgs<KIND, GRID>(&cap);
+  const hipError_t e = resident_wgs<KIND, VAR>(&cap);
   if (e != hipSuccess) return e;
   const int n_wgt = p.wgt_off[KS_NFAM];
   const int grid = n_wgt < cap ? n_wgt : cap;
-  hipLaunchKernelGGL((k_eval<KIND, GRID>), dim3(grid), dim3(kWgThreads), 0, s, p);
+  hipLaunchKernelGGL((k_eval<KIND, VAR>), dim3(grid), dim3(kWgThreads), 0, s, p);
   return hipGetLastError();
 }
 
@@ -1428,10 +1440,15 @@ static hipError_t launch_grid(const EvalParams &p, hipStream_t s) {
 // head-less kind)
 template <int KIND>
 static hipError_t launch_kind(const EvalParams &p, hipStream_t s) {
+  // multiplicities matter only for the step sums
+  const bool mult = p.mult && p.partial;
   if constexpr (KIND == kEtaOne) {
-    return p.grid_mask ? hipErrorInvalidValue : launch_grid<KIND, false>(p, s);
+    if (p.grid_mask) return hipErrorInvalidValue;
+    return mult ? launch_grid<KIND, kVarMult>(p, s) : launch_grid<KIND, 0>(p, s);
   } else {
-    return p.grid_mask ? launch_grid<KIND, true>(p, s) : launch_grid<KIND, false>(p, s);
+    if (p.grid_mask)
+      return mult ? launch_grid<KIND, kVarGrid | kVarMult>(p, s) : launch_grid<KIND, kVarGrid>(p, s);
+    return mult ? launch_grid<KIND, kVarMult>(p, s) : launch_grid<KIND, 0>(p, s);
   }
 }
 

@@ -246,3 +246,32 @@ def test_full_size_batch_sampled():
     sel = torch.tensor(idx, dtype=torch.int64, device="cuda")
     got = np.stack([_u32(db.t[f][sel]) for f in FIELDS], axis=1)
     np.testing.assert_array_equal(got, np.array(want, np.int64))
+
+
+@pytest.mark.parametrize("variant", ["bf16", "bf16-grid", "bounded"])
+def test_homogeneous_matches_per_layer_on_gpu(variant):
+    """Both forms price the same kernels with the same per-record latency;
+    the step sums differ only in fp32 summation order (m t once against t
+    added m times), for the MFMA head, the grid-routed variant and the
+    bounded head alike."""
+    tr = gen.trace_c1().slice(0, 120)
+    wl = gen.config1(0, 120).with_heads(gen.make_heads(16, 128, "bf16"))
+    bounded = gen.make_bounded(gen.BOUNDED_MIXED) if variant == "bounded" else None
+    grid = gen.make_grid(gen.GRID_ALL) if variant == "bf16-grid" else None
+    res = {}
+    for mode in (abi.KS_EXPAND_PER_LAYER, abi.KS_EXPAND_HOMOGENEOUS):
+        db, _ = run_expand(tr, mode)
+        di = abi.DeviceInputs(wl)
+        heads = di.make_heads("bf16", 16, 128, abi.KS_ETA_MLP, bounded, grid)
+        so_t, so = abi.step_outputs(db.desc.n_steps, di.n_specs)
+        wsb = abi.ks_workspace_bytes(db.desc, di.n_specs)
+        ws = torch.empty(wsb + 256, dtype=torch.uint8, device="cuda")
+        wsp = ws.data_ptr() + (-ws.data_ptr()) % 256
+        abi.ks_eval_steps(db.desc, db.steps, di.specs_ptr, di.n_specs, heads, di.host, so, None, wsp, wsb,
+                          abi.current_stream())
+        torch.cuda.synchronize()
+        abi.ks_device_status(wsp, wsb, abi.current_stream())
+        res[mode] = {k: v.cpu().numpy() for k, v in so_t.items()}
+    for key in ("t_body", "t_gpu", "t_step"):
+        err = g.rel_err(res[abi.KS_EXPAND_HOMOGENEOUS][key], res[abi.KS_EXPAND_PER_LAYER][key]).max()
+        assert err <= 1e-5, (key, err)
