@@ -65,7 +65,7 @@ def expand_bytes(n_records: int, n_steps: int, with_mult: bool) -> float:
 def kernel_source_hash() -> str:
     import hashlib
     h = hashlib.sha256()
-    for f in ("ks_kernels.hip", "ks_internal.h"):
+    for f in ("ks_kernels.hip", "ks_expand.hip", "ks_internal.h"):
         with open(os.path.join(ROOT, "paper_2606_28565_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
@@ -162,7 +162,8 @@ def _print_expand_only(args, wl, wdesc, db, ms, k_ms) -> int:
                                + ("homogeneous" if hom else "per-layer") + " records)",
                    "records": db.fam_off[-1], "serving_steps": db.desc.n_steps},
         "roofline": {"bound": "hbm", "achieved": eb / (k_ms * 1e-3) / 1e9, "peak": PEAK["hbm"] / 1e9,
-                     "unit": "GB/s", "frac": eb / (k_ms * 1e-3) / PEAK["hbm"], "traffic": None,
+                     "unit": "GB/s", "frac": eb / (k_ms * 1e-3) / PEAK["hbm"],
+                     "traffic": None if hom else recorded_traffic(f"{args.workload}-expand"),
                      "kernel_ms": k_ms,
                      "note": "achieved = record bytes written (+ per-step inputs read) by the record "
                              "writer / its mean HIP-event duration"},
