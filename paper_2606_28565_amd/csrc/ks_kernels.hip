@@ -373,9 +373,11 @@ template <bool kSmall>
 __device__ __forceinline__ Roof roofline(const RowC &r, const SpecC &s) {
   Roof o;
   if constexpr (kSmall) {
+    // (selects, not branches: the correction stays in the VALU stream)
     const uint32_t B = (uint32_t)r.B;
-    uint32_t W = (uint32_t)ceilf(r.Bf * s.rcp_n);
-    if (W > 0u && __umul24(W - 1u, s.n) >= B) W -= 1u;
+    const uint32_t W0 = (uint32_t)ceilf(r.Bf * s.rcp_n);
+    const uint32_t Wm = W0 > 0u ? W0 - 1u : 0u;
+    const uint32_t W = (W0 > 0u && __umul24(Wm, s.n) >= B) ? Wm : W0;
     o.W = (float)W;
     o.u = B > 0u ? (float)__umul24(W, s.n) * r.rcp_b : 1.0f;
   } else if (r.B > 0) {
@@ -395,15 +397,17 @@ __device__ __forceinline__ Roof roofline(const RowC &r, const SpecC &s) {
 // the 16 dimensionless features (x[16 + i] = x[i]^2 for 32 inputs);
 // x1 = log2(AI / ridge) = log2(AI) + log2(BW / P), and the last-wave
 // occupancy B / (W N) is 1 / u
+template <bool RAW = false>
 __device__ __forceinline__ float feature(int i, const RowC &r, const SpecC &s, const Roof &o) {
+  constexpr float k16 = RAW ? 1.0f : 1.0f / 16;
   switch (i) {
     case 0: return r.x0;
-    case 1: return fmaxf(r.la + s.lr, -20.0f) * (1.0f / 16);
-    case 2: return log2f_fast(fmaf(r.Bf, s.rcp_n, 1.0f)) * (1.0f / 16);
+    case 1: return fmaxf(r.la + s.lr, -20.0f) * k16;
+    case 2: return log2f_fast(fmaf(r.Bf, s.rcp_n, 1.0f)) * k16;
     case 3: return rcpf(o.u);
-    case 4: return log2f_fast(1.0f + o.W) * (1.0f / 16);
+    case 4: return log2f_fast(1.0f + o.W) * k16;
     case 5: return fminf(1.0f, s.l2 * r.rcp_bt1);
-    case 6: return log2f_fast(fmaxf(o.t_roof * s.rcp_t0, 0x1p-20f)) * (1.0f / 16);
+    case 6: return log2f_fast(fmaxf(o.t_roof * s.rcp_t0, 0x1p-20f)) * k16;
     case 7: {
       const float den = o.t_comp + o.t_mem;
       return den > 0.0f ? o.t_comp * rcpf(den) : 0.0f;
@@ -419,10 +423,10 @@ __device__ __forceinline__ float feature(int i, const RowC &r, const SpecC &s, c
   }
 }
 
-template <int IN>
+template <int IN, bool RAW = false>
 __device__ __forceinline__ void features(const RowC &r, const SpecC &s, const Roof &o, float (&x)[IN]) {
 #pragma unroll
-  for (int i = 0; i < 16; ++i) x[i] = feature(i, r, s, o);
+  for (int i = 0; i < 16; ++i) x[i] = feature<RAW>(i, r, s, o);
   if constexpr (IN == 32) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) x[16 + i] = x[i] * x[i];
@@ -530,6 +534,19 @@ struct HeadBF16 {
     return mb * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
   }
 
+  // The head takes the raw features (x1, x2, x4 and x6 without their 1/16,
+  // the squares of 32-input heads without 1/256) and W1's columns carry the
+  // scale instead.  Both are powers of two: bf16 rounding commutes with
+  // them and the MFMA's products are exact, so every product and sum is the
+  // same bit for bit, and the spec loop saves four multiplies per record.
+  static constexpr bool kRaw = true;
+  // W1 column k times the scale its feature drops in the raw form
+  __device__ static __forceinline__ uint32_t raw_scaled(uint16_t w, int k) {
+    const int b = k & 15;
+    if (b != 1 && b != 2 && b != 4 && b != 6) return w;
+    const float f = bf16_to_f32(w) * (k < 16 ? 1.0f / 16 : 1.0f / 256);
+    return __builtin_bit_cast(uint32_t, f) >> 16;
+  }
   __device__ static void stage(uint32_t *lds, int fam, const EvalParams &p) {
     const uint16_t *w1 = (const uint16_t *)p.w1 + (size_t)fam * HID * IN;
     const uint16_t *w2 = (const uint16_t *)p.w2 + (size_t)fam * HID * HID;
@@ -541,7 +558,7 @@ struct HeadBF16 {
       const int kc = frag % KC1, mb = frag / KC1;
       const int row = mb * 32 + (lane & 31);
       const int k0 = kc * 16 + (lane >> 5) * 8 + 2 * q;
-      lds[d] = (uint32_t)w1[row * IN + k0] | ((uint32_t)w1[row * IN + k0 + 1] << 16);
+      lds[d] = raw_scaled(w1[row * IN + k0], k0) | (raw_scaled(w1[row * IN + k0 + 1], k0 + 1) << 16);
     }
     for (int d = threadIdx.x; d < W2_DW; d += kWgThreads) {
       const int q = d & 3, lane = (d >> 2) & 63, frag = d >> 8;
@@ -589,12 +606,19 @@ struct HeadBF16 {
   }
 
   // relu + bf16 rounding of register pairs [2 q0, 2 q1) of one layer-1 block
+  // (every conversion before the first relu: no op waits on the one just
+  // before it)
   __device__ static __forceinline__ void pack_part(const f32x16 &c0, const f32x16 &c1, u32x4 (&h0)[2],
                                                    u32x4 (&h1)[2], int q0, int q1) {
 #pragma unroll
     for (int q = q0; q < q1; ++q) {
-      h0[q >> 2][q & 3] = relu_bf16x2(pack_bf16(c0[2 * q], c0[2 * q + 1]));
-      h1[q >> 2][q & 3] = relu_bf16x2(pack_bf16(c1[2 * q], c1[2 * q + 1]));
+      h0[q >> 2][q & 3] = pack_bf16(c0[2 * q], c0[2 * q + 1]);
+      h1[q >> 2][q & 3] = pack_bf16(c1[2 * q], c1[2 * q + 1]);
+    }
+#pragma unroll
+    for (int q = q0; q < q1; ++q) {
+      h0[q >> 2][q & 3] = relu_bf16x2(h0[q >> 2][q & 3]);
+      h1[q >> 2][q & 3] = relu_bf16x2(h1[q >> 2][q & 3]);
     }
   }
 
@@ -640,14 +664,6 @@ struct HeadBF16 {
     return *(const u32x4 *)(lds + lo[off >> 14] + (off & 16383));
   }
 
-  // one dot product pair of the layer-3 epilogue of the block held in p0/p1
-  __device__ static __forceinline__ void epi_pair(S4 &st, int slot, int j) {
-    const uint32_t w = st.w3r[slot][j];
-    st.zacc[j & 1] = dot2_bf16(relu_bf16x2(pack_bf16(st.p0[2 * j], st.p0[2 * j + 1])), w, st.zacc[j & 1]);
-    st.zacc[2 + (j & 1)] =
-        dot2_bf16(relu_bf16x2(pack_bf16(st.p1[2 * j], st.p1[2 * j + 1])), w, st.zacc[2 + (j & 1)]);
-  }
-
   template <int I>
   __device__ static __forceinline__ void group(S4 &st, const uint32_t *lds) {
     constexpr Grp q = sched(I);
@@ -690,8 +706,22 @@ struct HeadBF16 {
     if constexpr (q.vk == kPackV) {
       pack_part(st.a1[q.vb & 1][0], st.a1[q.vb & 1][1], st.H0[q.vb], st.H1[q.vb], 4 * q.vj, 4 * q.vj + 4);
     } else if constexpr (q.vk == kEpiV) {
+      // relu + bf16 of the slice's pairs first, then their dot products
+      // with w3: a v_dot2c that reads a VGPR the instruction just before
+      // wrote waits for it, and the dots cost the most of this slice's
+      // VALU ops (measured: 1.1% of the capacity-grid kernel)
+      uint32_t hp0[2], hp1[2];
 #pragma unroll
-      for (int j = q.vj; j < q.vj + q.vn; ++j) epi_pair(st, q.vb & 1, j);
+      for (int j = q.vj; j < q.vj + q.vn; ++j) {
+        hp0[j - q.vj] = relu_bf16x2(pack_bf16(st.p0[2 * j], st.p0[2 * j + 1]));
+        hp1[j - q.vj] = relu_bf16x2(pack_bf16(st.p1[2 * j], st.p1[2 * j + 1]));
+      }
+#pragma unroll
+      for (int j = q.vj; j < q.vj + q.vn; ++j) {
+        const uint32_t w = st.w3r[q.vb & 1][j];
+        st.zacc[j & 1] = dot2_bf16(hp0[j - q.vj], w, st.zacc[j & 1]);
+        st.zacc[2 + (j & 1)] = dot2_bf16(hp1[j - q.vj], w, st.zacc[2 + (j & 1)]);
+      }
       // an empty use pins the slice here; otherwise the dot chain, whose
       // result is only needed at the end, is sunk below every MFMA
       asm volatile("" ::"v"(st.zacc[0]), "v"(st.zacc[1]), "v"(st.zacc[2]), "v"(st.zacc[3]));
@@ -744,11 +774,23 @@ struct HeadBF16 {
     for (int j = 0; j < 4; ++j) st.zacc[j] = 0.0f;
     fence();
     groups(st, lds, std::make_integer_sequence<int, kNG>{});
-    // block 3's epilogue
+    // the last block's epilogue: packing of four pairs ahead of their dots
     st.p0 = st.c0;
     st.p1 = st.c1;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) epi_pair(st, 1, j);
+    for (int j0 = 0; j0 < 8; j0 += 4) {
+      uint32_t f0[4], f1[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        f0[j] = relu_bf16x2(pack_bf16(st.p0[2 * (j0 + j)], st.p0[2 * (j0 + j) + 1]));
+        f1[j] = relu_bf16x2(pack_bf16(st.p1[2 * (j0 + j)], st.p1[2 * (j0 + j) + 1]));
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        st.zacc[j & 1] = dot2_bf16(f0[j], st.w3r[(MB - 1) & 1][j0 + j], st.zacc[j & 1]);
+        st.zacc[2 + (j & 1)] = dot2_bf16(f1[j], st.w3r[(MB - 1) & 1][j0 + j], st.zacc[2 + (j & 1)]);
+      }
+    }
     // lanes l and l ^ 32 hold the two halves of the same record's dot
     // product; after the swap lane l < 32 adds block 0's halves of record
     // l and lane l >= 32 block 1's halves of record l.
@@ -890,6 +932,7 @@ struct HeadBF16 {
 //   C as for the bf16 instruction.
 template <int IN, int HID>
 struct HeadF32 {
+  static constexpr bool kRaw = false;
   static constexpr int MB = HID / 32;
   static constexpr int C1 = IN / 2;
   static constexpr int W1_DW = MB * C1 * 64;
@@ -1014,19 +1057,15 @@ template <> struct KindOf<kBF16_32_256> { using H = HeadBF16<32, 256>; static co
 
 // ------------------------------------------------------------ segmented scan
 // Inclusive scan of a wave's 64 values, segmented by sorted keys, with DPP
-// lane moves (no LDS round trips).  Within rows of 16 lanes: add lanes
-// l-1, l-2, l-3, then l-4 (lanes 4..15) and l-8 (lanes 8..15); across rows:
-// lane 15 of each row into rows 1 and 3, lane 31 into rows 2 and 3.  Each
-// step adds a contiguous partial that ends where the lane's current partial
-// begins; its factor is 1 when that source lane holds the same key (then, the
-// keys being sorted, every lane between does too) and 0 otherwise.  Sums are
-// built in at most 7 levels of adds of non-negative terms, so the fp32 result
-// errs by at most 7 * 2^-24 relative; tiles and families are then summed in
-// fp64.
-template <int CTRL, int ROW, int BANK>
-__device__ __forceinline__ float dpp(float x) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, ROW, BANK, true));
-}
+// lane moves (no LDS round trips), in Hillis-Steele form: within each row
+// of 16 lanes every lane adds the partial of the lane 1, 2, 4 and 8 below
+// it (the last two only for lanes 4..15 and 8..15), then lane 15 of each
+// row is added into rows 1 and 3 and lane 31 into rows 2 and 3.  A step's
+// factor is 1 where its source lane holds the same key, so, the keys being
+// sorted, the source's partial covers only lanes of the same segment; 0
+// otherwise.  Sums are built in at most 6 levels of adds of non-negative
+// terms, so the fp32 result errs by at most 6 * 2^-24 relative; tiles and
+// families are then summed in fp64.
 
 // key of the DPP source lane, or a value unequal to key where the pattern
 // has no source (bound_ctrl off: such lanes keep `old`)
@@ -1035,27 +1074,38 @@ __device__ __forceinline__ uint32_t dpp_key(uint32_t key) {
   return (uint32_t)__builtin_amdgcn_update_dpp((int)(key ^ 1u), (int)key, CTRL, ROW, BANK, false);
 }
 
-// Factor of each seg_scan step: 1 where that step's DPP source lane holds
-// the same key (keys are sorted, so the lanes in between do too).
-__device__ __forceinline__ void seg_factors(uint32_t key, float (&f)[7]) {
+// Factor of each seg_scan step (row_shr:1, 2, 4, 8, row_bcast:15, 31).
+__device__ __forceinline__ void seg_factors(uint32_t key, float (&f)[6]) {
   f[0] = dpp_key<0x111, 0xf, 0xf>(key) == key ? 1.0f : 0.0f;
   f[1] = dpp_key<0x112, 0xf, 0xf>(key) == key ? 1.0f : 0.0f;
-  f[2] = dpp_key<0x113, 0xf, 0xf>(key) == key ? 1.0f : 0.0f;
-  f[3] = dpp_key<0x114, 0xf, 0xe>(key) == key ? 1.0f : 0.0f;
-  f[4] = dpp_key<0x118, 0xf, 0xc>(key) == key ? 1.0f : 0.0f;
-  f[5] = dpp_key<0x142, 0xa, 0xf>(key) == key ? 1.0f : 0.0f;
-  f[6] = dpp_key<0x143, 0xc, 0xf>(key) == key ? 1.0f : 0.0f;
+  f[2] = dpp_key<0x114, 0xf, 0xe>(key) == key ? 1.0f : 0.0f;
+  f[3] = dpp_key<0x118, 0xf, 0xc>(key) == key ? 1.0f : 0.0f;
+  f[4] = dpp_key<0x142, 0xa, 0xf>(key) == key ? 1.0f : 0.0f;
+  f[5] = dpp_key<0x143, 0xc, 0xf>(key) == key ? 1.0f : 0.0f;
 }
 
-__device__ __forceinline__ float seg_scan(float v0, const float (&f)[7]) {
-  float v = v0;
-  v = fmaf(dpp<0x111, 0xf, 0xf>(v0), f[0], v);   // row_shr:1
-  v = fmaf(dpp<0x112, 0xf, 0xf>(v0), f[1], v);   // row_shr:2
-  v = fmaf(dpp<0x113, 0xf, 0xf>(v0), f[2], v);   // row_shr:3
-  v = fmaf(dpp<0x114, 0xf, 0xe>(v), f[3], v);    // row_shr:4, lanes 4..15 of each row
-  v = fmaf(dpp<0x118, 0xf, 0xc>(v), f[4], v);    // row_shr:8, lanes 8..15 of each row
-  v = fmaf(dpp<0x142, 0xa, 0xf>(v), f[5], v);    // row_bcast:15 into rows 1, 3
-  v = fmaf(dpp<0x143, 0xc, 0xf>(v), f[6], v);    // row_bcast:31 into rows 2, 3
+// Each step is one v_fmac_f32 with its first source read through DPP
+// (v += f * v[source lane]); lanes a step's bank or row mask leaves out keep
+// v, and lanes whose source lies outside the row read 0 (bound_ctrl).  A DPP
+// read of a VGPR written by the VALU op just before needs two wait states,
+// hence the s_nop 1 before every step (the compiler does not see into the
+// block, so the waits are explicit).
+__device__ __forceinline__ float seg_scan(float v, const float (&f)[6]) {
+  asm volatile(
+      "s_nop 1\n"
+      "v_fmac_f32_dpp %0, %0, %1 row_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "s_nop 1\n"
+      "v_fmac_f32_dpp %0, %0, %2 row_shr:2 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "s_nop 1\n"
+      "v_fmac_f32_dpp %0, %0, %3 row_shr:4 row_mask:0xf bank_mask:0xe\n"
+      "s_nop 1\n"
+      "v_fmac_f32_dpp %0, %0, %4 row_shr:8 row_mask:0xf bank_mask:0xc\n"
+      "s_nop 1\n"
+      "v_fmac_f32_dpp %0, %0, %5 row_bcast:15 row_mask:0xa bank_mask:0xf\n"
+      "s_nop 1\n"
+      "v_fmac_f32_dpp %0, %0, %6 row_bcast:31 row_mask:0xc bank_mask:0xf\n"
+      : "+v"(v)
+      : "v"(f[0]), "v"(f[1]), "v"(f[2]), "v"(f[3]), "v"(f[4]), "v"(f[5]));
   return v;
 }
 
@@ -1221,7 +1271,7 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
     // A tail lane stores its segment's sum (seg_scan): into the tile's carry
     // slot if the segment continues from the previous tile, else into the
     // (spec, family, step) partial.
-    float fac[7];
+    float fac[6];
     seg_factors(key, fac);
     // the scan input is m t for a live record of multiplicity m (1 without
     // a multiplicity array) and 0 otherwise: one product per spec instead
@@ -1262,7 +1312,7 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
         if constexpr (H::kMlp) {
           if (other) {
             float x[IN];
-            features<IN>(rc, sc, o, x);
+            features<IN, H::kRaw>(rc, sc, o, x);
             const float z = H::mlp(x, lds);
             eta = 1.0f + __expf(-z);
           }
