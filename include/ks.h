@@ -284,6 +284,89 @@ size_t ks_expand_workspace_bytes(int64_t n_steps);
 ks_status ks_expand(const ks_model* model, const ks_batch* batch, int32_t mode, const ks_records* out,
                     void* ws, size_t ws_bytes, hipStream_t stream);
 
+/*
+ * Serving simulation with the scheduler in the loop (Sec. 4.1-4.2: the
+ * discrete-event simulator asks the predictor for every batch the scheduler
+ * forms and advances its clock by the predicted step time; Sec. 5.8: one
+ * token-budget loop over computed-token counts gives continuous batching,
+ * chunked prefill and prefix-cache-aware FCFS admission, with preemption by
+ * recompute under KV pressure; Sec. 2.1: TTFT, TPOT, output throughput).
+ * The scheduler runs on the host; each step's batch descriptor (request r:
+ * q_r new tokens over h_r computed ones; prefill flag) is expanded on the
+ * GPU in the homogeneous form and priced by the evaluation kernels for one
+ * spec vector, and the host reads its t_step back before the next step.
+ *
+ * Rules (per step, at the simulation clock):
+ *  - requests that have arrived join the waiting queue (FCFS);
+ *  - running requests, in admission order, get n = min(target - computed,
+ *    budget) tokens, target = prompt + generated; KV blocks of block_tokens
+ *    tokens are allocated for computed + n; when they do not fit, cached
+ *    prefixes no running request shares are evicted (least recently used
+ *    first), then the most recently admitted running request is preempted
+ *    (blocks freed, computed reset to 0, back to the front of the queue);
+ *  - unless a request was preempted in this step, waiting requests are
+ *    admitted FCFS while budget > 0 and fewer than max_num_seqs run: a
+ *    cached prefix of c blocks starts computed at min(c, floor((target - 1)
+ *    / block_tokens)) blocks; admission stops at the first request whose
+ *    blocks do not fit after evicting unused prefixes; a request whose
+ *    prompt + output tokens exceed the whole cache is rejected;
+ *  - a request whose computed count first covers its group's full prefix
+ *    blocks (floor(prefix / block_tokens)) when the group has none cached
+ *    turns them into the group's cache entry;
+ *  - the step carries a prefill chunk if some scheduled request has more
+ *    than one token left to compute; after the step each request's computed
+ *    count grows by n; one that reaches its target samples a token (the
+ *    first one sets TTFT) and finishes at `output` tokens.
+ * TTFT = first token - arrival; TPOT = (last token - first token) /
+ * (output - 1), 0 for one output token; E2E = finish - arrival.
+ * Dense decoders only (experts = 0).
+ */
+typedef struct ks_sched {
+  int32_t max_num_seqs;        /* running requests per step, >= 1           */
+  int32_t max_batched_tokens;  /* token budget per step, >= 1               */
+  int32_t block_tokens;        /* tokens per KV block, >= 1                 */
+  int32_t prefix_cache;        /* 1: reuse cached prefix blocks, else 0     */
+  int64_t kv_blocks;           /* KV-cache capacity in blocks, >= 1         */
+} ks_sched;
+
+/* Requests, HOST arrays [n], sorted by arrival (non-decreasing). */
+typedef struct ks_requests {
+  int64_t n;
+  const double *arrival;       /* seconds, finite                           */
+  const uint32_t *prompt;      /* prompt tokens, 1 .. 2^24 - 1              */
+  const uint32_t *output;      /* output tokens, 1 .. 2^24 - 1              */
+  const uint32_t *group;       /* shared-prefix group, 0 = none; NULL: none */
+  const uint32_t *prefix;      /* tokens the group shares, <= prompt; NULL if group is NULL */
+} ks_requests;
+
+/* Results, HOST arrays owned by the caller (any array may be NULL = skip;
+ * the step record stops silently at step_cap steps or entry_cap entries). */
+typedef struct ks_sim_out {
+  double *ttft, *tpot, *e2e;        /* [n] seconds, 0 for rejected requests  */
+  int32_t *state;                   /* [n] 2 finished, 3 rejected            */
+  int64_t step_cap, entry_cap;
+  double *step_start, *step_latency;   /* [step_cap]                         */
+  uint8_t *step_prefill;               /* [step_cap]                         */
+  int64_t *step_entry_off;             /* [step_cap + 1] into the entries    */
+  uint32_t *entry_req, *entry_q, *entry_h;  /* [entry_cap]: request, q, h   */
+  /* written by ks_simulate: */
+  int64_t n_steps, n_entries, preemptions;
+  double clock;                     /* simulated time when the last request finished */
+} ks_sim_out;
+
+/* Bytes of device workspace ks_simulate needs (0 on bad arguments). */
+size_t ks_simulate_workspace_bytes(const ks_model* model, const ks_sched* sched);
+
+/* Runs the simulation to completion (synchronous: it waits for each step's
+ * latency on `stream`).  spec: DEVICE pointer to one ks_spec; heads and host
+ * as for ks_eval_steps.  KS_EINVAL / KS_ERANGE on bad arguments (unsorted
+ * arrivals, zero-length prompts or outputs, prefix > prompt, a model with
+ * experts), KS_EHIP on a failed runtime call, and the evaluation's own
+ * statuses. */
+ks_status ks_simulate(const ks_model* model, const ks_spec* spec, const ks_heads* heads,
+                      const ks_host* host, const ks_sched* sched, const ks_requests* requests,
+                      ks_sim_out* out, void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Bytes of device workspace ks_eval_kernels / ks_eval_steps / ks_validate
  * need for this record set and spec count (256-byte aligned).  0 on bad
  * arguments. */

@@ -85,6 +85,24 @@ class ks_records(C.Structure):
 KS_EXPAND_PER_LAYER, KS_EXPAND_HOMOGENEOUS = 0, 1
 
 
+class ks_sched(C.Structure):
+    _fields_ = [("max_num_seqs", C.c_int32), ("max_batched_tokens", C.c_int32),
+                ("block_tokens", C.c_int32), ("prefix_cache", C.c_int32), ("kv_blocks", C.c_int64)]
+
+
+class ks_requests(C.Structure):
+    _fields_ = [("n", C.c_int64), ("arrival", P), ("prompt", P), ("output", P), ("group", P),
+                ("prefix", P)]
+
+
+class ks_sim_out(C.Structure):
+    _fields_ = [("ttft", P), ("tpot", P), ("e2e", P), ("state", P), ("step_cap", C.c_int64),
+                ("entry_cap", C.c_int64), ("step_start", P), ("step_latency", P), ("step_prefill", P),
+                ("step_entry_off", P), ("entry_req", P), ("entry_q", P), ("entry_h", P),
+                ("n_steps", C.c_int64), ("n_entries", C.c_int64), ("preemptions", C.c_int64),
+                ("clock", C.c_double)]
+
+
 assert C.sizeof(ks_spec) == 64
 
 
@@ -127,6 +145,12 @@ def load(path: str = LIB_PATH) -> C.CDLL:
     lib.ks_expand.argtypes = [C.POINTER(ks_model), C.POINTER(ks_batch), C.c_int32,
                               C.POINTER(ks_records), P, C.c_size_t, P]
     lib.ks_expand.restype = C.c_int
+    lib.ks_simulate_workspace_bytes.argtypes = [C.POINTER(ks_model), C.POINTER(ks_sched)]
+    lib.ks_simulate_workspace_bytes.restype = C.c_size_t
+    lib.ks_simulate.argtypes = [C.POINTER(ks_model), P, C.POINTER(ks_heads), C.POINTER(ks_host),
+                                C.POINTER(ks_sched), C.POINTER(ks_requests), C.POINTER(ks_sim_out), P,
+                                C.c_size_t, P]
+    lib.ks_simulate.restype = C.c_int
     lib.ks_set_timing_events.argtypes = [P, P]
     lib.ks_set_timing_events.restype = C.c_int
     lib.ks_last_error.argtypes = []
@@ -192,6 +216,16 @@ def ks_expand_workspace_bytes(n_steps: int) -> int:
 
 def ks_expand(model, batch, mode, out, ws_ptr, ws_bytes, stream, check=True):
     st = load().ks_expand(C.byref(model), C.byref(batch), mode, C.byref(out), ws_ptr, ws_bytes, stream)
+    return _check(st) if check else st
+
+
+def ks_simulate_workspace_bytes(model: ks_model, sched: ks_sched) -> int:
+    return load().ks_simulate_workspace_bytes(C.byref(model), C.byref(sched))
+
+
+def ks_simulate(model, spec_ptr, heads, host, sched, requests, out, ws_ptr, ws_bytes, stream, check=True):
+    st = load().ks_simulate(C.byref(model), spec_ptr, C.byref(heads), C.byref(host), C.byref(sched),
+                            C.byref(requests), C.byref(out), ws_ptr, ws_bytes, stream)
     return _check(st) if check else st
 
 
@@ -457,3 +491,50 @@ class DeviceBatch:
     def expand(self, stream, check=True):
         return ks_expand(self.model, self.batch, self.mode, self.out, self.ws_ptr, self.ws_bytes,
                          stream, check)
+
+
+# --------------------------------------------------------------------------
+# serving simulation: host arrays in, host arrays out
+# --------------------------------------------------------------------------
+def simulate(shape, spec_row: dict, heads: ks_heads, host: ks_host, sched: ks_sched, requests: dict,
+             step_cap: int = 1 << 20, entry_cap: int = 1 << 24, device="cuda", check=True):
+    """Runs ks_simulate.  shape: a decoder shape (ks_model field names);
+    spec_row: one spec vector (dict of scalars); requests: dict of arrays
+    arrival, prompt, output and optionally group, prefix.  Returns a dict of
+    numpy arrays (per request and per step) and the counters."""
+    import torch
+    model = model_of(shape)
+    rec = pack_specs({k: np.asarray([v]) for k, v in spec_row.items()})
+    spec_t = torch.from_numpy(rec.view(np.uint8).copy()).to(device)
+    n = len(requests["arrival"])
+    arr = {"arrival": np.ascontiguousarray(requests["arrival"], np.float64)}
+    for k in ("prompt", "output", "group", "prefix"):
+        if k in requests:
+            arr[k] = np.ascontiguousarray(requests[k], np.uint32)
+    rq = ks_requests(n, arr["arrival"].ctypes.data, arr["prompt"].ctypes.data, arr["output"].ctypes.data,
+                     arr["group"].ctypes.data if "group" in arr else None,
+                     arr["prefix"].ctypes.data if "group" in arr else None)
+    res = {"ttft": np.zeros(n), "tpot": np.zeros(n), "e2e": np.zeros(n), "state": np.zeros(n, np.int32),
+           "step_start": np.zeros(step_cap), "step_latency": np.zeros(step_cap),
+           "step_prefill": np.zeros(step_cap, np.uint8), "step_entry_off": np.zeros(step_cap + 1, np.int64),
+           "entry_req": np.zeros(entry_cap, np.uint32), "entry_q": np.zeros(entry_cap, np.uint32),
+           "entry_h": np.zeros(entry_cap, np.uint32)}
+    out = ks_sim_out(res["ttft"].ctypes.data, res["tpot"].ctypes.data, res["e2e"].ctypes.data,
+                     res["state"].ctypes.data, step_cap, entry_cap, res["step_start"].ctypes.data,
+                     res["step_latency"].ctypes.data, res["step_prefill"].ctypes.data,
+                     res["step_entry_off"].ctypes.data, res["entry_req"].ctypes.data,
+                     res["entry_q"].ctypes.data, res["entry_h"].ctypes.data, 0, 0, 0, 0.0)
+    wsb = ks_simulate_workspace_bytes(model, sched)
+    if wsb == 0:
+        raise KsError(KS_EINVAL, ks_last_error())
+    ws = torch.empty(wsb + 256, dtype=torch.uint8, device=device)
+    wsp = ws.data_ptr() + (-ws.data_ptr()) % 256
+    st = ks_simulate(model, spec_t.data_ptr(), heads, host, sched, rq, out, wsp, wsb, current_stream(), check)
+    ns, ne = int(out.n_steps), int(out.n_entries)
+    for k in ("step_start", "step_latency", "step_prefill"):
+        res[k] = res[k][:min(ns, step_cap)]
+    res["step_entry_off"] = res["step_entry_off"][:min(ns, step_cap) + 1]
+    for k in ("entry_req", "entry_q", "entry_h"):
+        res[k] = res[k][:ne]
+    res.update(status=st, n_steps=ns, n_entries=ne, preemptions=int(out.preemptions), clock=float(out.clock))
+    return res

@@ -48,7 +48,10 @@ def build(verbose: bool = False) -> str:
     _run([HIPCC, *DEVICE_FLAGS, *common, "-c", os.path.join(CSRC, "ks_expand.hip"), "-o", expand])
     _run([HIPCC, *HOST_FLAGS, *common, "-D__HIP_PLATFORM_AMD__", "-c",
           os.path.join(CSRC, "ks_api.cpp"), "-o", api])
-    objs = [kern, expand, api]
+    simo = os.path.join(tmp, "ks_sim.o")
+    _run([HIPCC, *HOST_FLAGS, *common, "-D__HIP_PLATFORM_AMD__", "-c",
+          os.path.join(CSRC, "ks_sim.cpp"), "-o", simo])
+    objs = [kern, expand, api, simo]
     tmp_lib = LIB + ".tmp"
     _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp_lib])
     os.replace(tmp_lib, LIB)

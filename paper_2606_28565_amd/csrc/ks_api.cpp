@@ -381,6 +381,25 @@ ks_status flag_status(uint32_t f) {
 
 }  // namespace
 
+size_t ks::eval_workspace_bytes(const int64_t fam_off[KS_NFAM + 1], int64_t n_steps, int32_t n_specs) {
+  ks_desc d;
+  std::memset(&d, 0, sizeof d);
+  for (int f = 0; f <= KS_NFAM; ++f) d.fam_off[f] = fam_off[f];
+  d.n_rows = fam_off[KS_NFAM];
+  d.n_steps = n_steps;
+  return layout_of(&d, n_specs).total;
+}
+
+ks_status ks::set_error(ks_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
 extern "C" {
 
 size_t ks_workspace_bytes(const ks_desc *desc, int32_t n_specs) {

@@ -152,6 +152,13 @@ struct ExpandParams {
 // events recorded around the record-writing kernel (both null: none)
 hipError_t launch_expand(const ExpandParams &p, hipStream_t s, hipEvent_t before, hipEvent_t after);
 
+// workspace bytes of one evaluation call for a record layout (family
+// offsets), step count and spec count, without the descriptor's pointers
+size_t eval_workspace_bytes(const int64_t fam_off[KS_NFAM + 1], int64_t n_steps, int32_t n_specs);
+
+// the thread-local message ks_last_error() reports; returns st
+ks_status set_error(ks_status st, const char *fmt, ...);
+
 hipError_t launch_clear(uint32_t *err, uint32_t *range, int64_t n_range, hipStream_t s);
 hipError_t launch_spec_prep(const ks_spec *specs, int32_t n_specs, SpecC *out, uint32_t *err, hipStream_t s);
 hipError_t launch_attn_agg(const uint32_t *req_off, const uint32_t *q, const uint32_t *h,

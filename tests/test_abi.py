@@ -25,7 +25,8 @@ def test_library_exports_every_declared_symbol():
     names = _declared_functions()
     assert {"ks_eval_kernels", "ks_eval_steps", "ks_workspace_bytes", "ks_validate",
             "ks_device_status", "ks_last_error", "ks_version", "ks_expand", "ks_expand_layout",
-            "ks_expand_workspace_bytes"} <= set(names)
+            "ks_expand_workspace_bytes", "ks_simulate", "ks_simulate_workspace_bytes",
+            "ks_set_timing_events"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
     assert abi.ks_version().startswith("ks ")
@@ -37,7 +38,8 @@ def test_struct_layout_matches_header(tmp_path):
     structs = {"ks_desc": abi.ks_desc, "ks_spec": abi.ks_spec, "ks_heads": abi.ks_heads,
                "ks_steps": abi.ks_steps, "ks_host": abi.ks_host,
                "ks_kernel_out": abi.ks_kernel_out, "ks_step_out": abi.ks_step_out,
-               "ks_model": abi.ks_model, "ks_batch": abi.ks_batch, "ks_records": abi.ks_records}
+               "ks_model": abi.ks_model, "ks_batch": abi.ks_batch, "ks_records": abi.ks_records,
+               "ks_sched": abi.ks_sched, "ks_requests": abi.ks_requests, "ks_sim_out": abi.ks_sim_out}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "ks.h"', "int main(void){"]
     for s, cls in structs.items():
         lines.append(f'printf("{s} size %zu\\n", sizeof({s}));')
@@ -249,3 +251,55 @@ def test_expand_host_checks():
         setattr(out, name, 16)
     assert abi.ks_expand(md, b, 0, out, wsp, 8, None, check=False) == abi.KS_EWORKSPACE
     assert abi.ks_expand(md, b, 0, out, wsp + 8, 1 << 15, None, check=False) == abi.KS_EWORKSPACE
+
+
+# ---- serving simulation (host side only)
+def _sched(**kw):
+    base = dict(max_num_seqs=64, max_batched_tokens=4096, block_tokens=16, prefix_cache=1, kv_blocks=4096)
+    base.update(kw)
+    return abi.ks_sched(*(base[n] for n, _ in abi.ks_sched._fields_))
+
+
+@pytest.mark.parametrize("kw,needle", [
+    (dict(max_num_seqs=0), "max_num_seqs"),
+    (dict(max_batched_tokens=1 << 24), "max_batched_tokens"),
+    (dict(block_tokens=0), "block_tokens"),
+    (dict(prefix_cache=2), "prefix_cache"),
+    (dict(kv_blocks=0), "kv_blocks"),
+])
+def test_simulate_rejects_bad_schedulers(kw, needle):
+    assert abi.ks_simulate_workspace_bytes(_model(), _sched(**kw)) == 0
+    assert needle in abi.ks_last_error()
+
+
+def test_simulate_workspace_and_model_checks():
+    assert abi.ks_simulate_workspace_bytes(_model(), _sched()) > 0
+    assert abi.ks_simulate_workspace_bytes(_model(experts=8, top_k=2, expert_ffn=1024, ffn=0), _sched()) == 0
+    assert "dense" in abi.ks_last_error()
+
+
+def _sim_call(arrival, prompt, output, ws_bytes=1 << 22, group=None, prefix=None):
+    import numpy as np
+    arr = {"a": np.ascontiguousarray(arrival, np.float64), "p": np.ascontiguousarray(prompt, np.uint32),
+           "o": np.ascontiguousarray(output, np.uint32)}
+    g = np.ascontiguousarray(group, np.uint32) if group is not None else None
+    x = np.ascontiguousarray(prefix, np.uint32) if prefix is not None else None
+    rq = abi.ks_requests(len(arrival), arr["a"].ctypes.data, arr["p"].ctypes.data, arr["o"].ctypes.data,
+                         g.ctypes.data if g is not None else None, x.ctypes.data if x is not None else None)
+    out = abi.ks_sim_out()
+    ws = C.create_string_buffer(ws_bytes + 256)
+    wsp = (C.addressof(ws) + 255) & ~255
+    st = abi.ks_simulate(_model(), 16, abi.ks_heads(), abi.ks_host(), _sched(), rq, out, wsp, ws_bytes, None,
+                         check=False)
+    return st, abi.ks_last_error()
+
+
+def test_simulate_rejects_bad_requests_on_host():
+    # every case fails before any device call (the spec pointer is a dummy)
+    assert _sim_call([1.0, 0.5], [10, 10], [2, 2]) == (abi.KS_EINVAL, _sim_call([1.0, 0.5], [10, 10], [2, 2])[1])
+    assert "non-decreasing" in _sim_call([1.0, 0.5], [10, 10], [2, 2])[1]
+    assert _sim_call([0.0], [0], [2])[0] == abi.KS_ERANGE
+    assert _sim_call([0.0], [5], [0])[0] == abi.KS_ERANGE
+    assert _sim_call([0.0], [5], [2], group=[1], prefix=[9])[0] == abi.KS_EINVAL
+    assert _sim_call([0.0], [5], [2], group=[1])[0] == abi.KS_EINVAL
+    assert _sim_call([0.0], [5], [2], ws_bytes=64)[0] == abi.KS_EWORKSPACE

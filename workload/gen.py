@@ -668,3 +668,30 @@ def config5(step_lo=0, step_hi=C5_STEPS) -> Workload:
     tr = trace_c5().slice(step_lo, step_hi)
     return _wl("c5-70b-prefix", [tr], specs_datasheet(), make_heads(32, 256, "bf16"),
                {"steps": (step_lo, step_hi)})
+
+
+# --------------------------------------------------------------------------
+# serving requests for the simulator (synthetic arrival process)
+# --------------------------------------------------------------------------
+REQ_SEED = SEED + 200
+
+
+def make_requests(n: int, rate: float, seed: int = REQ_SEED, prompt_median=512, prompt_sigma=1.0,
+                  prompt_max=8192, output_median=128, output_sigma=0.8, output_max=2048,
+                  groups=8, group_frac=0.5, prefix_lo=256, prefix_hi=2048) -> dict:
+    """n requests from a Poisson process of `rate` requests/s; prompt and
+    output lengths lognormal (clipped to [1, max]); a fraction group_frac of
+    the requests carries one of `groups` shared system prompts, whose
+    lengths are U{prefix_lo..prefix_hi} (a request's prompt is at least its
+    prefix).  Stand-in for the paper's production conversation trace, which
+    is not available."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    arrival = np.cumsum(rng.exponential(1.0 / rate, n))
+    prompt = np.clip(np.floor(rng.lognormal(np.log(prompt_median), prompt_sigma, n)), 1, prompt_max)
+    output = np.clip(np.floor(rng.lognormal(np.log(output_median), output_sigma, n)), 1, output_max)
+    plen = rng.integers(prefix_lo, prefix_hi, groups + 1, endpoint=True)
+    group = np.where(rng.random(n) < group_frac, rng.integers(1, groups + 1, n), 0)
+    prefix = np.where(group > 0, plen[group], 0)
+    prompt = np.maximum(prompt, prefix)
+    return {"arrival": arrival, "prompt": prompt.astype(np.uint32), "output": output.astype(np.uint32),
+            "group": group.astype(np.uint32), "prefix": prefix.astype(np.uint32)}
