@@ -172,6 +172,113 @@ def _print_expand_only(args, wl, wdesc, db, ms, k_ms) -> int:
     return 0
 
 
+def nearest_rank(x, p):
+    """P_p = x_(k), k = ceil(p/100 n) over the ascending sample (the paper's
+    percentile definition)."""
+    import math
+    xs = sorted(float(v) for v in x)
+    return xs[max(1, math.ceil(p / 100.0 * len(xs))) - 1]
+
+
+SIM_SCHED = dict(max_num_seqs=256, max_batched_tokens=8192, block_tokens=16, prefix_cache=1,
+                 kv_blocks=12_500)   # about 100 GB of bf16 KV for the Llama-7B shape
+
+
+def _sim_inputs(n, rate):
+    from workload import gen
+    from paper_2606_28565_amd import abi
+    import numpy as np
+    import torch
+    reqs = gen.make_requests(n, rate)
+    specs = gen.specs_datasheet()
+    row = {k: (int(v[0]) if k == "n_cu" else float(v[0])) for k, v in specs.items()}
+    h = gen.make_heads(16, 64, "f32")
+    hd = abi.ks_heads()
+    hd.in_dim, hd.hidden, hd.precision, hd.mode = 16, 64, abi.KS_F32, abi.KS_ETA_MLP
+    keep = {}
+    for name in ("w1", "w2", "b2", "w3", "b3"):
+        keep[name] = torch.from_numpy(np.ascontiguousarray(h.storage[name]).reshape(-1).copy()).cuda()
+        setattr(hd, name, keep[name].data_ptr())
+    hc = gen.HostConsts()
+    host = abi.ks_host(hc.c_disp, hc.ell, hc.c_ovl, hc.c_tail, hc.body_scale)
+    sched = abi.ks_sched(*(SIM_SCHED[k] for k, _ in abi.ks_sched._fields_))
+    return reqs, row, hd, keep, host, sched, h
+
+
+def _bench_simulate(args) -> int:
+    """Serving simulation: the host scheduler forms every step's batch, the
+    GPU path prices it, the clock advances by its t_step.  value = simulated
+    steps per wall-clock second of the whole ks_simulate call."""
+    import numpy as np
+    import torch
+    from workload import gen
+    from paper_2606_28565_amd import abi
+    reqs, row, hd, keep, host, sched, h = _sim_inputs(args.simulate, args.rate)
+    warm = {k: v[:min(50, len(v))] for k, v in reqs.items()}
+    abi.simulate(gen.LLAMA7B, row, hd, host, sched, warm)
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    res = abi.simulate(gen.LLAMA7B, row, hd, host, sched, reqs)
+    wall = time.perf_counter() - t
+    fin = res["state"] == 2
+    out_tok = int(np.asarray(reqs["output"])[fin].sum())
+    span = float(np.max((res["e2e"] + reqs["arrival"])[fin]) - reqs["arrival"][0])
+    line = {
+        "metric": "simulated serving steps/s (scheduler in the loop, each step priced on the GPU)",
+        "value": res["n_steps"] / wall, "unit": "steps/s", "n_gpus": 1, "steps": 1, "warmup": 1,
+        "ms_per_step": wall * 1e3, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"serving simulation: {args.simulate} Poisson requests at {args.rate}/s, "
+                               "llama-7b shape, GB200 datasheet row, fp32 16-64-64-1 heads",
+                   "scheduler": SIM_SCHED},
+        "simulated_steps": res["n_steps"], "wall_ms_per_simulated_step": wall * 1e3 / max(res["n_steps"], 1),
+        "serving": {"finished": int(fin.sum()), "preemptions": res["preemptions"],
+                    "simulated_seconds": res["clock"],
+                    "output_tokens_per_s": out_tok / span if span > 0 else None,
+                    "ttft_s": {f"p{p}": nearest_rank(res["ttft"][fin], p) for p in (50, 90, 99)},
+                    "tpot_s": {f"p{p}": nearest_rank(res["tpot"][fin & (np.asarray(reqs["output"]) > 1)], p)
+                               for p in (50, 90, 99)}},
+        "roofline": None,
+        "note": "launch- and round-trip-bound by design: every step waits for its own latency before the "
+                "scheduler forms the next one",
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = _sim_cpu_baseline(reqs, h, min(args.simulate, 120))
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+def _sim_cpu_baseline(reqs, h, n):
+    """The oracle's scheduler with the oracle latency model on the first n
+    requests."""
+    import numpy as np
+    from oracle import ks_expand as ox
+    from oracle import ks_oracle as o
+    from oracle import ks_sim as osim
+    from workload import gen
+    u = lambda x: np.asarray(x, np.uint32)
+    specs = {k: np.asarray(v[:1]) for k, v in gen.specs_datasheet().items()}
+    hc = gen.HostConsts()
+
+    def lat(batch, prefill):
+        q = [b[0] for b in batch]
+        hh = [b[1] for b in batch]
+        e = ox.expand(gen.LLAMA7B, [0, len(q)], q, [prefill], homogeneous=True)
+        d = gen.Desc(e["fam_off"], *(u(e[k]) for k in ("step", "m", "n", "k", "a", "b")), u([0, len(q)]),
+                     u(q), u(hh), u([]), 2, u(e["mult"]))
+        rec = gen.StepRec(*(u(e[k]) for k in ("layers", "hidden", "tp", "n_launch")))
+        return float(o.eval_steps(d, rec, specs, hc, h)["t_step"][0, 0])
+    lst = [{k: (float(reqs[k][i]) if k == "arrival" else int(reqs[k][i])) for k in reqs} for i in range(n)]
+    cfg = osim.SchedCfg(SIM_SCHED["max_num_seqs"], SIM_SCHED["max_batched_tokens"], SIM_SCHED["block_tokens"],
+                        SIM_SCHED["kv_blocks"], bool(SIM_SCHED["prefix_cache"]))
+    t = time.perf_counter()
+    r = osim.simulate(lst, cfg, lat)
+    dt = time.perf_counter() - t
+    return {"value": len(r.steps) / dt, "unit": "steps/s", "cores": 1, "kind": "oracle",
+            "sample": f"the first {n} requests ({len(r.steps)} steps, {dt:.1f} s, Python scheduler with the "
+                      "fp64 numpy latency model per step)"}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -189,6 +296,10 @@ def main() -> int:
                          "multiplicity L) and then ks_eval_steps on its records")
     ap.add_argument("--expand-only", action="store_true",
                     help="time ks_expand alone (the records are not evaluated)")
+    ap.add_argument("--simulate", type=int, default=0, metavar="N",
+                    help="serving simulation of N requests (Llama-7B shape, GB200 datasheet row, fp32 "
+                         "16-64 heads) with the scheduler in the loop; reports simulated steps/s")
+    ap.add_argument("--rate", type=float, default=40.0, help="request arrival rate of --simulate (1/s)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -213,6 +324,9 @@ def main() -> int:
     if args.copy_calibration:
         copy_calibration(args.copy_calibration, max(args.steps, 1))
         return 0
+
+    if args.simulate:
+        return _bench_simulate(args)
 
     print(f"[bench] generating workload {args.workload}", file=sys.stderr, flush=True)
     wl, wdesc, sample, traces = _workload(args.workload)
