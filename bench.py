@@ -125,7 +125,7 @@ def head_flops_per_pair(in_dim: int, hidden: int) -> int:
     return 2 * (in_dim * hidden + hidden * hidden + hidden)
 
 
-def cpu_baseline(wl, sample: dict, eta_one: bool, threads: int, bounded=None):
+def cpu_baseline(wl, sample: dict, eta_one: bool, threads: int, bounded=None, grid=None):
     """The oracle as it stands, on a bounded sample of the same workload:
     the first sample["specs"] spec vectors and, if sample["steps"] is set,
     only the records of the first sample["steps"] steps."""
@@ -139,7 +139,7 @@ def cpu_baseline(wl, sample: dict, eta_one: bool, threads: int, bounded=None):
     with threadpool_limits(limits=threads):
         t = time.perf_counter()
         k = o.eval_kernels(wl.desc, wl.specs, None if eta_one else wl.heads, eta_one=eta_one,
-                           spec_ids=spec_ids, rows=rows, bounded=bounded)
+                           spec_ids=spec_ids, rows=rows, bounded=bounded, grid=grid)
         if rows is None:
             o.eval_steps(wl.desc, wl.steps, wl.specs, wl.host, spec_ids=spec_ids, kern=k)
         dt = time.perf_counter() - t
@@ -290,6 +290,9 @@ def main() -> int:
     ap.add_argument("--bounded", default="none", choices=["none", "mixed", "all"],
                     help="families on the bounded analytical head: none; the GEMMs, embedding and "
                          "KV writes (mixed, the rest on the MLP or eta = 1); or all")
+    ap.add_argument("--grid", default="none", choices=["none", "all"],
+                    help="Tier B: a measured eta grid (8x8x8 over features x1, x2, x6, 8%% of the nodes "
+                         "unmeasured) on every family, the head of the mode where a pair falls outside")
     ap.add_argument("--expand", default="none", choices=["none", "per-layer", "homogeneous"],
                     help="start from the batch descriptors: each step runs ks_expand (one record "
                          "per dispatched kernel, or layer-identical kernels as one record of "
@@ -333,9 +336,23 @@ def main() -> int:
     from workload import gen
     bmask = {"none": 0, "mixed": gen.BOUNDED_MIXED, "all": gen.BOUNDED_ALL}[args.bounded]
     bounded = gen.make_bounded(bmask) if bmask else None
+    grid = gen.make_grid(gen.GRID_ALL) if args.grid == "all" else None
     di = abi.DeviceInputs(wl)
     heads = di.make_heads(wl.heads.precision, wl.heads.in_dim, wl.heads.hidden,
-                          abi.KS_ETA_ONE if args.eta_one else abi.KS_ETA_MLP, bounded)
+                          abi.KS_ETA_ONE if args.eta_one else abi.KS_ETA_MLP, bounded, grid)
+    head_pairs = None
+    if grid is not None:
+        # where each pair's eta comes from (one untimed call): only the pairs
+        # left to the head count as its work
+        src_t, src_o = abi.kernel_outputs(wl.desc.n_rows, di.n_specs, counts=False, t_roof=False, eta=False,
+                                          t_kernel=False, source=True)
+        so0_t, so0 = abi.step_outputs(wl.desc.n_steps, di.n_specs)
+        abi.ks_eval_steps(di.desc, di.steps, di.specs_ptr, di.n_specs, heads, di.host, so0, src_o,
+                          di.ws_ptr, di.ws_bytes, abi.current_stream())
+        torch.cuda.synchronize()
+        head_pairs = int((src_t["source"] == 0).sum().item())
+        routed_frac = float((src_t["source"] == 2).float().mean().item())
+        del src_t, so0_t
     so_t, so = abi.step_outputs(wl.desc.n_steps, di.n_specs)
     if args.per_pair:
         ko_t, ko = abi.kernel_outputs(wl.desc.n_rows, di.n_specs, counts=False)
@@ -451,6 +468,7 @@ def main() -> int:
     else:
         n_eval = wl.desc.n_rows
         on_mlp_n = int(np.count_nonzero(on_mlp))
+    mlp_pairs = on_mlp_n * di.n_specs if head_pairs is None else head_pairs
     if args.eta_one or bmask == gen.BOUNDED_ALL:
         alg = stream_bytes(wl, di.n_specs) if eval_desc is None or args.expand != "homogeneous" else None
         bound, unit, peak = "hbm", "GB/s", PEAK["hbm"] / 1e9
@@ -458,7 +476,7 @@ def main() -> int:
         dtype = "f32"
     else:
         per_pair = head_flops_per_pair(wl.heads.in_dim, wl.heads.hidden)
-        alg = float(on_mlp_n * di.n_specs) * per_pair
+        alg = float(mlp_pairs) * per_pair
         bf16 = wl.heads.precision == "bf16"
         bound, unit = "mfma", "TFLOP/s"
         peak = (PEAK["bf16"] if bf16 else PEAK["f32"]) / 1e12
@@ -474,7 +492,9 @@ def main() -> int:
                    "serving_steps": wl.desc.n_steps, "predictions_per_step": pairs,
                    "head": ("eta=1" if args.eta_one else
                             f"{wl.heads.precision} {wl.heads.in_dim}-{wl.heads.hidden}-{wl.heads.hidden}-1")
-                           + ("" if not bmask else f"; bounded head on families 0x{bmask:03x}"),
+                           + ("" if not bmask else f"; bounded head on families 0x{bmask:03x}")
+                           + ("" if grid is None else f"; Tier B grid on every family, {100 * routed_frac:.1f}% of "
+                                                      f"the pairs routed to it"),
                    "per_pair_outputs": bool(args.per_pair),
                    "input": ("batch descriptors, expanded on the GPU every step ("
                              + args.expand + " records)") if db is not None else "kernel records"},
@@ -482,7 +502,7 @@ def main() -> int:
         "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
                      "frac": achieved / peak if achieved is not None else None,
                      "traffic": (recorded_traffic(f"{args.workload}{'-eta1' if args.eta_one else ''}")
-                                 if not bmask and db is None else None),
+                                 if not bmask and db is None and grid is None else None),
                      "kernel_ms": k_ms, "evaluated_records": n_eval,
                      "note": "achieved = algorithmic work of one evaluation-kernel launch (FLOPs of the "
                              "head over the records it evaluates, or the bytes the model reads and "
@@ -494,7 +514,7 @@ def main() -> int:
     if not args.no_cpu_baseline:
         threads = args.cpu_threads or min(16, os.cpu_count() or 1)
         print(f"[bench] cpu baseline: oracle on {sample}, {threads} threads", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(wl, sample, args.eta_one, threads, bounded)
+        out["cpu_baseline"] = cpu_baseline(wl, sample, args.eta_one, threads, bounded, grid)
         try:
             model = subprocess.run(["lscpu"], capture_output=True, text=True).stdout
             model = [l.split(":", 1)[1].strip() for l in model.splitlines() if l.startswith("Model name")]

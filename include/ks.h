@@ -186,10 +186,14 @@ typedef struct ks_host {
 } ks_host;
 
 /* Per-record and per-pair outputs (device; any pointer may be NULL = skip).
- * flops, bytes, blocks: [n_rows]; t_roof, eta, t_kernel: [n_specs][n_rows]. */
+ * flops, bytes, blocks: [n_rows]; t_roof, eta, t_kernel: [n_specs][n_rows].
+ * source: [n_specs][n_rows], where each pair's eta came from: 0 the head of
+ * heads.mode (the MLP, or eta = 1), 1 the bounded analytical head, 2 the
+ * measured Tier B grid (density routing, Sec. 5.5). */
 typedef struct ks_kernel_out {
   uint64_t *flops, *bytes, *blocks;
   float *t_roof, *eta, *t_kernel;
+  uint8_t *source;
 } ks_kernel_out;
 
 /* Per-step outputs (device, [n_specs][n_steps], none may be NULL). */

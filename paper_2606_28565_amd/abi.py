@@ -57,7 +57,7 @@ class ks_host(C.Structure):
 
 class ks_kernel_out(C.Structure):
     _fields_ = [("flops", P), ("bytes", P), ("blocks", P),
-                ("t_roof", P), ("eta", P), ("t_kernel", P)]
+                ("t_roof", P), ("eta", P), ("t_kernel", P), ("source", P)]
 
 
 class ks_step_out(C.Structure):
@@ -391,7 +391,7 @@ class DeviceInputs:
 
 
 def kernel_outputs(n_rows: int, n_specs: int, device="cuda", counts=True, t_roof=True,
-                   eta=True, t_kernel=True):
+                   eta=True, t_kernel=True, source=False):
     """Allocate per-record / per-pair output tensors and the struct."""
     import torch
     dev = torch.device(device)
@@ -402,8 +402,10 @@ def kernel_outputs(n_rows: int, n_specs: int, device="cuda", counts=True, t_roof
     for name, want in (("t_roof", t_roof), ("eta", eta), ("t_kernel", t_kernel)):
         if want:
             o[name] = torch.empty((n_specs, n_rows), dtype=torch.float32, device=dev)
+    if source:
+        o["source"] = torch.empty((n_specs, n_rows), dtype=torch.uint8, device=dev)
     s = ks_kernel_out()
-    for name in ("flops", "bytes", "blocks", "t_roof", "eta", "t_kernel"):
+    for name in ("flops", "bytes", "blocks", "t_roof", "eta", "t_kernel", "source"):
         setattr(s, name, _ptr(o.get(name)) if name in o and o[name].numel() else None)
     return o, s
 

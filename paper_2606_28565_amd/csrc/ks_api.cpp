@@ -24,9 +24,14 @@ hipError_t timed_eval(int kind, const ks::EvalParams &p, hipStream_t s) {
     const hipError_t e = hipEventRecord(g_ev_before, s);
     if (e != hipSuccess) return e;
   }
-  const hipError_t e = ks::launch_eval(kind, p, s);
+  hipError_t e = ks::launch_eval(kind, p, s);
   if (e != hipSuccess) return e;
-  return timed ? hipEventRecord(g_ev_after, s) : hipSuccess;
+  if (timed) {
+    e = hipEventRecord(g_ev_after, s);
+    if (e != hipSuccess) return e;
+  }
+  // without a grid the evaluation kernel leaves the eta source to this pass
+  return p.grid_mask ? hipSuccess : ks::launch_fill_source(p, s);
 }
 
 ks_status fail(ks_status st, const char *fmt, ...) {
@@ -234,6 +239,7 @@ void fill_eval(ks::EvalParams &p, const ks_desc *d, const ks_spec *specs, int32_
     p.o_troof = out->t_roof;
     p.o_eta = out->eta;
     p.o_t = out->t_kernel;
+    p.o_src = out->source;
   }
   p.err = reinterpret_cast<uint32_t *>(ws);
 }

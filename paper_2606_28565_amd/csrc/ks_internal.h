@@ -77,6 +77,7 @@ struct EvalParams {
   double *carry;     // [n_specs][n_tiles]
   uint32_t *range;   // [KS_NFAM][n_steps][2] record range of each (family, step); nullable
   uint32_t *err;
+  uint8_t *o_src;    // per pair: 0 head of the mode, 1 bounded head, 2 grid (nullable)
 };
 
 struct FinishParams {
@@ -166,6 +167,8 @@ hipError_t launch_attn_agg(const uint32_t *req_off, const uint32_t *q, const uin
                            hipStream_t s);
 hipError_t launch_eval(int kind, const EvalParams &p, hipStream_t s);
 hipError_t launch_finish(const FinishParams &p, hipStream_t s);
+// per-pair eta source of a call without a grid (p.o_src, families' bounded bit)
+hipError_t launch_fill_source(const EvalParams &p, hipStream_t s);
 hipError_t launch_validate(const ValidateParams &p, hipStream_t s);
 
 }  // namespace ks

@@ -1325,6 +1325,11 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
         if (p.o_troof) p.o_troof[i] = o.t_roof;
         if (p.o_eta) p.o_eta[i] = eta;
         if (p.o_t) p.o_t[i] = t;
+        // (without a grid the source is a per-family constant, written by
+        // k_fill_source instead, so the plain kernels keep their registers)
+        if constexpr (GRID) {
+          if (p.o_src) p.o_src[i] = routed ? 2 : (bnd ? 1 : 0);
+        }
       }
       if (p.partial) {
         // a record of multiplicity m adds m t (one fp32 rounding)
@@ -1332,6 +1337,21 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
         if (dst) dst[(size_t)s * dst_stride] = (double)v;
       }
     }
+  }
+}
+
+// ------------------------------------------------------------ eta source
+// Per pair, where eta came from when no grid routes any pair: 1 for the
+// families on the bounded head, 0 (the head of the mode) for the others.
+__global__ void k_fill_source(uint8_t *src, EvalParams p) {
+  const int64_t n_rows = p.fam_off[KS_NFAM];
+  const int64_t total = (int64_t)p.n_specs * n_rows;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t row = i % n_rows;
+    int f = 0;
+    while (row >= p.fam_off[f + 1]) ++f;
+    src[i] = (uint8_t)((p.bounded_mask >> f) & 1u);
   }
 }
 
@@ -1519,6 +1539,13 @@ hipError_t launch_eval(int kind, const EvalParams &p, hipStream_t s) {
     case kBF16_32_256: return launch_kind<kBF16_32_256>(p, s);
     default: return hipErrorInvalidValue;
   }
+}
+
+hipError_t launch_fill_source(const EvalParams &p, hipStream_t s) {
+  const int64_t total = (int64_t)p.n_specs * p.fam_off[KS_NFAM];
+  if (!p.o_src || total == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_fill_source, dim3(grid_for(total, 256, 8192)), dim3(256), 0, s, p.o_src, p);
+  return hipGetLastError();
 }
 
 hipError_t launch_finish(const FinishParams &p, hipStream_t s) {

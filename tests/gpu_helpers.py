@@ -24,7 +24,7 @@ def eval_kernels(wl, eta_one=False, n_specs=None, counts=True, bounded=None, gri
 
 
 def eval_steps(wl, eta_one=False, n_specs=None, per_pair=True, counts=True, bounded=None,
-               null_mlp=False, grid=None):
+               null_mlp=False, grid=None, source=False):
     """counts=False asks for per-pair outputs without the per-record counts
     (the eta = 1 stream then forms F and Bt in fp32).  bounded: a
     ``workload.gen.Bounded``; grid: a ``workload.gen.Grid``; null_mlp
@@ -36,7 +36,7 @@ def eval_steps(wl, eta_one=False, n_specs=None, per_pair=True, counts=True, boun
     if null_mlp:
         heads.w1 = heads.w2 = heads.b2 = heads.w3 = heads.b3 = None
     so_t, so = abi.step_outputs(wl.desc.n_steps, di.n_specs)
-    ko_t, ko = (abi.kernel_outputs(wl.desc.n_rows, di.n_specs, counts=counts) if per_pair
+    ko_t, ko = (abi.kernel_outputs(wl.desc.n_rows, di.n_specs, counts=counts, source=source) if per_pair
                 else ({}, None))
     abi.ks_eval_steps(di.desc, di.steps, di.specs_ptr, di.n_specs, heads, di.host, so, ko,
                       di.ws_ptr, di.ws_bytes, abi.current_stream())

@@ -534,10 +534,12 @@ def _grid_eta_check(wl, gr, ref, plain, gpu_eta, n_specs, fallback_tol):
     n = np.asarray(gr.n, np.float64)
     step = (gr.hi - gr.lo) / (n - 1)
     n_amb = 0
+    amb_all = np.zeros((n_specs, len(fam)), bool)
     for s in range(n_specs):
         x = ref["x16"][s]
         t = (x[:, ax] - gr.lo) / step
         amb = on & (np.abs(t - np.round(t)) < GRID_EPS).any(axis=1)
+        amb_all[s] = amb
         n_amb += int(amb.sum())
         routed = ref["routed"][s] & ~amb
         rest = ~routed & ~amb
@@ -554,6 +556,7 @@ def _grid_eta_check(wl, gr, ref, plain, gpu_eta, n_specs, fallback_tol):
             tol = max(REL * 4, fallback_tol)
             assert min(g.rel_err(gpu_eta[s, r], c) for c in cands) <= tol, (s, r, gpu_eta[s, r], cands)
     assert n_amb <= 0.01 * on.sum() * n_specs
+    return amb_all
 
 
 def _grid_case(wl, gr, eta_one=False, bounded=None, null_mlp=False, n_specs=None, expect_routed=True):
@@ -562,7 +565,8 @@ def _grid_case(wl, gr, eta_one=False, bounded=None, null_mlp=False, n_specs=None
     kw = dict(eta_one=eta_one, spec_ids=range(n_specs), bounded=bounded)
     ref = o.eval_kernels(wl.desc, wl.specs, heads, grid=gr, **kw)
     plain = o.eval_kernels(wl.desc, wl.specs, heads, **kw)
-    gpu = g.eval_steps(wl, eta_one=eta_one, n_specs=n_specs, bounded=bounded, grid=gr, null_mlp=null_mlp)
+    gpu = g.eval_steps(wl, eta_one=eta_one, n_specs=n_specs, bounded=bounded, grid=gr, null_mlp=null_mlp,
+                       source=True)
     if expect_routed:
         assert ref["routed"].any() and (~ref["routed"]).any()
     np.testing.assert_array_equal(gpu["flops"], ref["counts"]["F"])
@@ -571,7 +575,15 @@ def _grid_case(wl, gr, eta_one=False, bounded=None, null_mlp=False, n_specs=None
     fam = wl.desc.family()
     on_b = ((bounded.mask if bounded is not None else 0) >> fam) & 1
     mlp_fallback = bf16 and not (on_b.astype(bool)).all()
-    _grid_eta_check(wl, gr, ref, plain, gpu["eta"], n_specs, REL_BF16 if mlp_fallback else REL)
+    amb = _grid_eta_check(wl, gr, ref, plain, gpu["eta"], n_specs, REL_BF16 if mlp_fallback else REL)
+    # where each pair's eta came from: the grid where the oracle routes it
+    # (pairs within GRID_EPS of a cell face may go either way), else the
+    # bounded head for its families, else the mode's head
+    fallback = np.broadcast_to(np.where(on_b.astype(bool), 1, 0)[None, :], ref["routed"].shape)
+    want = np.where(ref["routed"], 2, fallback)
+    src = gpu["source"].astype(np.int64)
+    np.testing.assert_array_equal(src[~amb], want[~amb])
+    assert ((src[amb] == 2) | (src[amb] == fallback[amb])).all()
     t0 = wl.specs["t0"][:n_specs, None]
     assert g.rel_err(gpu["t_kernel"], np.maximum(ref["t_roof"] * gpu["eta"].astype(np.float64), t0)).max() <= REL
     _check_steps(wl, gpu, _steps_given_eta(wl, gpu, ref, n_specs), bf16=False, n_specs=n_specs)
@@ -631,3 +643,14 @@ def test_grid_sizes_and_degenerate_grids():
     plain = g.eval_steps(wl)
     np.testing.assert_array_equal(gpu["eta"], plain["eta"])
     np.testing.assert_array_equal(gpu["t_step"], plain["t_step"])
+
+
+@pytest.mark.parametrize("bounded_mask", [0, gen.BOUNDED_MIXED, gen.BOUNDED_ALL])
+def test_eta_source_without_grid(bounded_mask):
+    """Without a grid every pair's eta comes from its family's head: the
+    bounded head for the families in the mask, the MLP for the others."""
+    wl = gen.config1(0, 30)
+    bd = gen.make_bounded(bounded_mask) if bounded_mask else None
+    gpu = g.eval_steps(wl, bounded=bd, source=True)
+    want = ((bounded_mask >> wl.desc.family()) & 1).astype(np.uint8)
+    np.testing.assert_array_equal(gpu["source"], np.broadcast_to(want, gpu["source"].shape))
