@@ -177,6 +177,8 @@ def nearest_rank(x, p):
     percentile definition)."""
     import math
     xs = sorted(float(v) for v in x)
+    if not xs:
+        return None
     return xs[max(1, math.ceil(p / 100.0 * len(xs))) - 1]
 
 
@@ -184,14 +186,23 @@ SIM_SCHED = dict(max_num_seqs=256, max_batched_tokens=8192, block_tokens=16, pre
                  kv_blocks=12_500)   # about 100 GB of bf16 KV for the Llama-7B shape
 
 
-def _sim_inputs(n, rate):
+SIM_GRID_SEED = 20260602 + 300
+
+
+def _sim_inputs(n, rate, n_specs=1):
+    """Requests, spec table (the GB200 datasheet row, then n_specs - 1
+    hypothetical GPUs of the capacity-planning grid), heads, host constants
+    and scheduler of the serving simulation."""
     from workload import gen
     from paper_2606_28565_amd import abi
     import numpy as np
     import torch
     reqs = gen.make_requests(n, rate)
-    specs = gen.specs_datasheet()
-    row = {k: (int(v[0]) if k == "n_cu" else float(v[0])) for k, v in specs.items()}
+    ds = gen.specs_datasheet()
+    table = {k: np.asarray(v[:1]) for k, v in ds.items()}
+    if n_specs > 1:
+        grid = gen.specs_grid(n_specs - 1, SIM_GRID_SEED)
+        table = {k: np.concatenate([table[k], np.asarray(grid[k], table[k].dtype)]) for k in table}
     h = gen.make_heads(16, 64, "f32")
     hd = abi.ks_heads()
     hd.in_dim, hd.hidden, hd.precision, hd.mode = 16, 64, abi.KS_F32, abi.KS_ETA_MLP
@@ -202,46 +213,65 @@ def _sim_inputs(n, rate):
     hc = gen.HostConsts()
     host = abi.ks_host(hc.c_disp, hc.ell, hc.c_ovl, hc.c_tail, hc.body_scale)
     sched = abi.ks_sched(*(SIM_SCHED[k] for k, _ in abi.ks_sched._fields_))
-    return reqs, row, hd, keep, host, sched, h
+    return reqs, table, hd, keep, host, sched, h
+
+
+def _serving_summary(reqs, res):
+    import numpy as np
+    fin = res["state"] == 2
+    out_tok = int(np.asarray(reqs["output"])[fin].sum())
+    span = float(np.max((res["e2e"] + reqs["arrival"])[fin]) - reqs["arrival"][0]) if fin.any() else 0.0
+    return {"finished": int(fin.sum()), "preemptions": res["preemptions"], "simulated_steps": res["n_steps"],
+            "simulated_seconds": res["clock"],
+            "output_tokens_per_s": out_tok / span if span > 0 else None,
+            "ttft_s": {f"p{p}": nearest_rank(res["ttft"][fin], p) for p in (50, 90, 99)},
+            "tpot_s": {f"p{p}": nearest_rank(res["tpot"][fin & (np.asarray(reqs["output"]) > 1)], p)
+                       for p in (50, 90, 99)}}
 
 
 def _bench_simulate(args) -> int:
     """Serving simulation: the host scheduler forms every step's batch, the
-    GPU path prices it, the clock advances by its t_step.  value = simulated
-    steps per wall-clock second of the whole ks_simulate call."""
-    import numpy as np
+    GPU path prices it, the clock advances by its t_step; with --sim-specs
+    S, S simulations (one per spec vector) run in lockstep and each round's
+    steps are priced by one expansion and one evaluation call.  value =
+    simulated steps (all simulations) per wall-clock second of the whole
+    ks_simulate call."""
     import torch
     from workload import gen
     from paper_2606_28565_amd import abi
-    reqs, row, hd, keep, host, sched, h = _sim_inputs(args.simulate, args.rate)
+    S = args.sim_specs
+    reqs, table, hd, keep, host, sched, h = _sim_inputs(args.simulate, args.rate, S)
     warm = {k: v[:min(50, len(v))] for k, v in reqs.items()}
-    abi.simulate(gen.LLAMA7B, row, hd, host, sched, warm)
+    abi.simulate_many(gen.LLAMA7B, table, hd, host, sched, warm, step_cap=1 << 16, entry_cap=1 << 20)
     torch.cuda.synchronize()
     t = time.perf_counter()
-    res = abi.simulate(gen.LLAMA7B, row, hd, host, sched, reqs)
+    many = abi.simulate_many(gen.LLAMA7B, table, hd, host, sched, reqs, step_cap=1 << 16, entry_cap=1 << 20)
     wall = time.perf_counter() - t
-    fin = res["state"] == 2
-    out_tok = int(np.asarray(reqs["output"])[fin].sum())
-    span = float(np.max((res["e2e"] + reqs["arrival"])[fin]) - reqs["arrival"][0])
+    steps = sum(r["n_steps"] for r in many)
+    rounds = max(r["n_steps"] for r in many)
+    spec_desc = "GB200 datasheet row" + (f" + {S - 1} capacity-grid GPUs (seed {SIM_GRID_SEED})" if S > 1 else "")
     line = {
         "metric": "simulated serving steps/s (scheduler in the loop, each step priced on the GPU)",
-        "value": res["n_steps"] / wall, "unit": "steps/s", "n_gpus": 1, "steps": 1, "warmup": 1,
+        "value": steps / wall, "unit": "steps/s", "n_gpus": 1, "steps": 1, "warmup": 1,
         "ms_per_step": wall * 1e3, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32", "data": "synthetic",
         "config": {"workload": f"serving simulation: {args.simulate} Poisson requests at {args.rate}/s, "
-                               "llama-7b shape, GB200 datasheet row, fp32 16-64-64-1 heads",
-                   "scheduler": SIM_SCHED},
-        "simulated_steps": res["n_steps"], "wall_ms_per_simulated_step": wall * 1e3 / max(res["n_steps"], 1),
-        "serving": {"finished": int(fin.sum()), "preemptions": res["preemptions"],
-                    "simulated_seconds": res["clock"],
-                    "output_tokens_per_s": out_tok / span if span > 0 else None,
-                    "ttft_s": {f"p{p}": nearest_rank(res["ttft"][fin], p) for p in (50, 90, 99)},
-                    "tpot_s": {f"p{p}": nearest_rank(res["tpot"][fin & (np.asarray(reqs["output"]) > 1)], p)
-                               for p in (50, 90, 99)}},
+                               f"llama-7b shape, {S} spec vector(s) in lockstep ({spec_desc}), "
+                               "fp32 16-64-64-1 heads",
+                   "scheduler": SIM_SCHED, "simulations": S},
+        "simulated_steps": steps, "rounds": rounds, "wall_ms_per_round": wall * 1e3 / max(rounds, 1),
+        "wall_ms_per_simulated_step": wall * 1e3 / max(steps, 1),
+        "serving": _serving_summary(reqs, many[0]),
         "roofline": None,
-        "note": "launch- and round-trip-bound by design: every step waits for its own latency before the "
-                "scheduler forms the next one",
+        "note": "launch- and round-trip-bound by design: every round waits for its latencies before the "
+                "schedulers form the next steps",
     }
+    if S > 1:
+        line["per_spec"] = [{"peak_flops": float(table["peak_flops"][i]), "hbm_bw": float(table["hbm_bw"][i]),
+                             **{k: v for k, v in _serving_summary(reqs, r).items()
+                                if k in ("simulated_steps", "output_tokens_per_s", "preemptions")},
+                             "ttft_p50_s": nearest_rank(r["ttft"][r["state"] == 2], 50)}
+                            for i, r in enumerate(many[:16])]
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = _sim_cpu_baseline(reqs, h, min(args.simulate, 120))
     print(json.dumps(line), flush=True)
@@ -303,6 +333,8 @@ def main() -> int:
                     help="serving simulation of N requests (Llama-7B shape, GB200 datasheet row, fp32 "
                          "16-64 heads) with the scheduler in the loop; reports simulated steps/s")
     ap.add_argument("--rate", type=float, default=40.0, help="request arrival rate of --simulate (1/s)")
+    ap.add_argument("--sim-specs", type=int, default=1, metavar="S",
+                    help="--simulate: S simulations in lockstep, one per spec vector (1 .. 256)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",

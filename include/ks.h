@@ -295,10 +295,14 @@ ks_status ks_expand(const ks_model* model, const ks_batch* batch, int32_t mode, 
  * token-budget loop over computed-token counts gives continuous batching,
  * chunked prefill and prefix-cache-aware FCFS admission, with preemption by
  * recompute under KV pressure; Sec. 2.1: TTFT, TPOT, output throughput).
- * The scheduler runs on the host; each step's batch descriptor (request r:
- * q_r new tokens over h_r computed ones; prefill flag) is expanded on the
- * GPU in the homogeneous form and priced by the evaluation kernels for one
- * spec vector, and the host reads its t_step back before the next step.
+ * The scheduler runs on the host, one simulation per spec vector, all fed
+ * the same requests and run in lockstep: each round every unfinished
+ * simulation forms its next step (request r: q_r new tokens over h_r
+ * computed ones; prefill flag); the round's steps are expanded on the GPU
+ * as one batch in the homogeneous form and priced by one evaluation call
+ * against all the spec vectors (A steps x n_specs pairs of steps and specs,
+ * of which each step keeps its own simulation's t_step); the host reads one
+ * latency per simulation back before the next round.
  *
  * Rules (per step, at the simulation clock):
  *  - requests that have arrived join the waiting queue (FCFS);
@@ -358,16 +362,22 @@ typedef struct ks_sim_out {
   double clock;                     /* simulated time when the last request finished */
 } ks_sim_out;
 
-/* Bytes of device workspace ks_simulate needs (0 on bad arguments). */
-size_t ks_simulate_workspace_bytes(const ks_model* model, const ks_sched* sched);
+/* Bytes of device workspace ks_simulate needs for n_specs simulations (0 on
+ * bad arguments). */
+size_t ks_simulate_workspace_bytes(const ks_model* model, const ks_sched* sched, int32_t n_specs);
 
-/* Runs the simulation to completion (synchronous: it waits for each step's
- * latency on `stream`).  spec: DEVICE pointer to one ks_spec; heads and host
- * as for ks_eval_steps.  KS_EINVAL / KS_ERANGE on bad arguments (unsorted
- * arrivals, zero-length prompts or outputs, prefix > prompt, a model with
- * experts), KS_EHIP on a failed runtime call, and the evaluation's own
- * statuses. */
-ks_status ks_simulate(const ks_model* model, const ks_spec* spec, const ks_heads* heads,
+/* Runs n_specs simulations (1 .. 256) to completion (synchronous: it waits
+ * for each round's latencies on `stream`).  specs: DEVICE array of n_specs
+ * ks_spec; heads and host as for ks_eval_steps; out: HOST array of n_specs
+ * results, out[s] for specs[s] (the same request arrays are read by all).
+ * A simulation's results do not depend on the others run beside it, up to
+ * the rounding order of its steps' sums (which depends on where a step sits
+ * in the round's batch).
+ * KS_EINVAL / KS_ERANGE on bad arguments (unsorted arrivals, zero-length
+ * prompts or outputs, prefix > prompt, a model with experts, n_specs out of
+ * range), KS_EHIP on a failed runtime call, and the evaluation's own
+ * statuses; the results are then undefined. */
+ks_status ks_simulate(const ks_model* model, const ks_spec* specs, int32_t n_specs, const ks_heads* heads,
                       const ks_host* host, const ks_sched* sched, const ks_requests* requests,
                       ks_sim_out* out, void* ws, size_t ws_bytes, hipStream_t stream);
 

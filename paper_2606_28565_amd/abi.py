@@ -145,9 +145,9 @@ def load(path: str = LIB_PATH) -> C.CDLL:
     lib.ks_expand.argtypes = [C.POINTER(ks_model), C.POINTER(ks_batch), C.c_int32,
                               C.POINTER(ks_records), P, C.c_size_t, P]
     lib.ks_expand.restype = C.c_int
-    lib.ks_simulate_workspace_bytes.argtypes = [C.POINTER(ks_model), C.POINTER(ks_sched)]
+    lib.ks_simulate_workspace_bytes.argtypes = [C.POINTER(ks_model), C.POINTER(ks_sched), C.c_int32]
     lib.ks_simulate_workspace_bytes.restype = C.c_size_t
-    lib.ks_simulate.argtypes = [C.POINTER(ks_model), P, C.POINTER(ks_heads), C.POINTER(ks_host),
+    lib.ks_simulate.argtypes = [C.POINTER(ks_model), P, C.c_int32, C.POINTER(ks_heads), C.POINTER(ks_host),
                                 C.POINTER(ks_sched), C.POINTER(ks_requests), C.POINTER(ks_sim_out), P,
                                 C.c_size_t, P]
     lib.ks_simulate.restype = C.c_int
@@ -219,13 +219,16 @@ def ks_expand(model, batch, mode, out, ws_ptr, ws_bytes, stream, check=True):
     return _check(st) if check else st
 
 
-def ks_simulate_workspace_bytes(model: ks_model, sched: ks_sched) -> int:
-    return load().ks_simulate_workspace_bytes(C.byref(model), C.byref(sched))
+def ks_simulate_workspace_bytes(model: ks_model, sched: ks_sched, n_specs: int = 1) -> int:
+    return load().ks_simulate_workspace_bytes(C.byref(model), C.byref(sched), n_specs)
 
 
-def ks_simulate(model, spec_ptr, heads, host, sched, requests, out, ws_ptr, ws_bytes, stream, check=True):
-    st = load().ks_simulate(C.byref(model), spec_ptr, C.byref(heads), C.byref(host), C.byref(sched),
-                            C.byref(requests), C.byref(out), ws_ptr, ws_bytes, stream)
+def ks_simulate(model, specs_ptr, n_specs, heads, host, sched, requests, outs, ws_ptr, ws_bytes, stream,
+                check=True):
+    """outs: a ks_sim_out, or a ctypes array of n_specs of them."""
+    st = load().ks_simulate(C.byref(model), specs_ptr, n_specs, C.byref(heads), C.byref(host), C.byref(sched),
+                            C.byref(requests), outs if isinstance(outs, C.Array) else C.byref(outs),
+                            ws_ptr, ws_bytes, stream)
     return _check(st) if check else st
 
 
@@ -498,15 +501,17 @@ class DeviceBatch:
 # --------------------------------------------------------------------------
 # serving simulation: host arrays in, host arrays out
 # --------------------------------------------------------------------------
-def simulate(shape, spec_row: dict, heads: ks_heads, host: ks_host, sched: ks_sched, requests: dict,
-             step_cap: int = 1 << 20, entry_cap: int = 1 << 24, device="cuda", check=True):
-    """Runs ks_simulate.  shape: a decoder shape (ks_model field names);
-    spec_row: one spec vector (dict of scalars); requests: dict of arrays
-    arrival, prompt, output and optionally group, prefix.  Returns a dict of
-    numpy arrays (per request and per step) and the counters."""
+def simulate_many(shape, specs: dict, heads: ks_heads, host: ks_host, sched: ks_sched, requests: dict,
+                  step_cap: int = 1 << 20, entry_cap: int = 1 << 22, device="cuda", check=True):
+    """Runs ks_simulate with one simulation per spec vector.  shape: a
+    decoder shape (ks_model field names); specs: dict of arrays [n_specs];
+    requests: dict of arrays arrival, prompt, output and optionally group,
+    prefix.  Returns one dict per spec vector of numpy arrays (per request
+    and per step) and the counters."""
     import torch
     model = model_of(shape)
-    rec = pack_specs({k: np.asarray([v]) for k, v in spec_row.items()})
+    rec = pack_specs({k: np.atleast_1d(np.asarray(v)) for k, v in specs.items()})
+    S = len(rec)
     spec_t = torch.from_numpy(rec.view(np.uint8).copy()).to(device)
     n = len(requests["arrival"])
     arr = {"arrival": np.ascontiguousarray(requests["arrival"], np.float64)}
@@ -516,27 +521,43 @@ def simulate(shape, spec_row: dict, heads: ks_heads, host: ks_host, sched: ks_sc
     rq = ks_requests(n, arr["arrival"].ctypes.data, arr["prompt"].ctypes.data, arr["output"].ctypes.data,
                      arr["group"].ctypes.data if "group" in arr else None,
                      arr["prefix"].ctypes.data if "group" in arr else None)
-    res = {"ttft": np.zeros(n), "tpot": np.zeros(n), "e2e": np.zeros(n), "state": np.zeros(n, np.int32),
-           "step_start": np.zeros(step_cap), "step_latency": np.zeros(step_cap),
-           "step_prefill": np.zeros(step_cap, np.uint8), "step_entry_off": np.zeros(step_cap + 1, np.int64),
-           "entry_req": np.zeros(entry_cap, np.uint32), "entry_q": np.zeros(entry_cap, np.uint32),
-           "entry_h": np.zeros(entry_cap, np.uint32)}
-    out = ks_sim_out(res["ttft"].ctypes.data, res["tpot"].ctypes.data, res["e2e"].ctypes.data,
-                     res["state"].ctypes.data, step_cap, entry_cap, res["step_start"].ctypes.data,
-                     res["step_latency"].ctypes.data, res["step_prefill"].ctypes.data,
-                     res["step_entry_off"].ctypes.data, res["entry_req"].ctypes.data,
-                     res["entry_q"].ctypes.data, res["entry_h"].ctypes.data, 0, 0, 0, 0.0)
-    wsb = ks_simulate_workspace_bytes(model, sched)
+    results = []
+    outs = (ks_sim_out * S)()
+    for s in range(S):
+        res = {"ttft": np.zeros(n), "tpot": np.zeros(n), "e2e": np.zeros(n), "state": np.zeros(n, np.int32),
+               "step_start": np.zeros(step_cap), "step_latency": np.zeros(step_cap),
+               "step_prefill": np.zeros(step_cap, np.uint8),
+               "step_entry_off": np.zeros(step_cap + 1, np.int64),
+               "entry_req": np.zeros(entry_cap, np.uint32), "entry_q": np.zeros(entry_cap, np.uint32),
+               "entry_h": np.zeros(entry_cap, np.uint32)}
+        outs[s] = ks_sim_out(res["ttft"].ctypes.data, res["tpot"].ctypes.data, res["e2e"].ctypes.data,
+                             res["state"].ctypes.data, step_cap, entry_cap, res["step_start"].ctypes.data,
+                             res["step_latency"].ctypes.data, res["step_prefill"].ctypes.data,
+                             res["step_entry_off"].ctypes.data, res["entry_req"].ctypes.data,
+                             res["entry_q"].ctypes.data, res["entry_h"].ctypes.data, 0, 0, 0, 0.0)
+        results.append(res)
+    wsb = ks_simulate_workspace_bytes(model, sched, S)
     if wsb == 0:
         raise KsError(KS_EINVAL, ks_last_error())
     ws = torch.empty(wsb + 256, dtype=torch.uint8, device=device)
     wsp = ws.data_ptr() + (-ws.data_ptr()) % 256
-    st = ks_simulate(model, spec_t.data_ptr(), heads, host, sched, rq, out, wsp, wsb, current_stream(), check)
-    ns, ne = int(out.n_steps), int(out.n_entries)
-    for k in ("step_start", "step_latency", "step_prefill"):
-        res[k] = res[k][:min(ns, step_cap)]
-    res["step_entry_off"] = res["step_entry_off"][:min(ns, step_cap) + 1]
-    for k in ("entry_req", "entry_q", "entry_h"):
-        res[k] = res[k][:ne]
-    res.update(status=st, n_steps=ns, n_entries=ne, preemptions=int(out.preemptions), clock=float(out.clock))
-    return res
+    st = ks_simulate(model, spec_t.data_ptr(), S, heads, host, sched, rq, outs, wsp, wsb, current_stream(),
+                     check)
+    for s, res in enumerate(results):
+        out = outs[s]
+        ns, ne = int(out.n_steps), int(out.n_entries)
+        for k in ("step_start", "step_latency", "step_prefill"):
+            res[k] = res[k][:min(ns, step_cap)]
+        res["step_entry_off"] = res["step_entry_off"][:min(ns, step_cap) + 1]
+        for k in ("entry_req", "entry_q", "entry_h"):
+            res[k] = res[k][:ne]
+        res.update(status=st, n_steps=ns, n_entries=ne, preemptions=int(out.preemptions),
+                   clock=float(out.clock))
+    return results
+
+
+def simulate(shape, spec_row: dict, heads: ks_heads, host: ks_host, sched: ks_sched, requests: dict,
+             step_cap: int = 1 << 20, entry_cap: int = 1 << 22, device="cuda", check=True):
+    """ks_simulate for one spec vector (dict of scalars); one result dict."""
+    return simulate_many(shape, {k: np.asarray([v]) for k, v in spec_row.items()}, heads, host, sched,
+                         requests, step_cap, entry_cap, device, check)[0]

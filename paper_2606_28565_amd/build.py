@@ -23,7 +23,9 @@ DEVICE_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
                 # work, and accumulator-register round trips cost a VALU op each
                 "-mllvm", "-amdgpu-mfma-vgpr-form",
                 "-Wall", "-Wno-unused-function"]
-HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall"]
+# host-only translation units: plain C++ against the HIP runtime API
+HOST_FLAGS = ["-x", "c++", "-O2", "-std=c++17", "-fPIC", "-Wall",
+              "-I", os.path.join(os.path.dirname(os.path.dirname(os.path.realpath(HIPCC))), "include")]
 
 
 def _run(cmd):

@@ -196,4 +196,19 @@ hipError_t launch_expand(const ExpandParams &p, hipStream_t s, hipEvent_t before
   return before && after ? hipEventRecord(after, s) : hipSuccess;
 }
 
+// lat[i] = t_step[own[i]][i]: step i's latency under its own spec vector
+// (t_step is [n_specs][n_steps]; the host bounds own[i] below n_specs)
+__global__ void k_gather_own(const double *t_step, int64_t n_steps, const uint32_t *own, double *lat) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n_steps) lat[i] = t_step[(int64_t)own[i] * n_steps + i];
+}
+
+hipError_t launch_gather_own(const double *t_step, int64_t n_steps, const uint32_t *own, double *lat,
+                             hipStream_t s) {
+  if (n_steps <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_gather_own, dim3((unsigned)((n_steps + 255) / 256)), dim3(256), 0, s, t_step, n_steps, own,
+                     lat);
+  return hipGetLastError();
+}
+
 }  // namespace ks

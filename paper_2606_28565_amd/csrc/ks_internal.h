@@ -153,6 +153,10 @@ struct ExpandParams {
 // events recorded around the record-writing kernel (both null: none)
 hipError_t launch_expand(const ExpandParams &p, hipStream_t s, hipEvent_t before, hipEvent_t after);
 
+// lat[i] = t_step[own[i] * n_steps + i] for i < n_steps (device arrays)
+hipError_t launch_gather_own(const double *t_step, int64_t n_steps, const uint32_t *own, double *lat,
+                             hipStream_t s);
+
 // workspace bytes of one evaluation call for a record layout (family
 // offsets), step count and spec count, without the descriptor's pointers
 size_t eval_workspace_bytes(const int64_t fam_off[KS_NFAM + 1], int64_t n_steps, int32_t n_specs);

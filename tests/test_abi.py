@@ -274,6 +274,12 @@ def test_simulate_rejects_bad_schedulers(kw, needle):
 
 def test_simulate_workspace_and_model_checks():
     assert abi.ks_simulate_workspace_bytes(_model(), _sched()) > 0
+    # the workspace grows with the number of simulations run in lockstep
+    one, many = (abi.ks_simulate_workspace_bytes(_model(), _sched(), s) for s in (1, 8))
+    assert many > one
+    for bad in (0, 257):
+        assert abi.ks_simulate_workspace_bytes(_model(), _sched(), bad) == 0
+        assert "n_specs" in abi.ks_last_error()
     assert abi.ks_simulate_workspace_bytes(_model(experts=8, top_k=2, expert_ffn=1024, ffn=0), _sched()) == 0
     assert "dense" in abi.ks_last_error()
 
@@ -289,8 +295,8 @@ def _sim_call(arrival, prompt, output, ws_bytes=1 << 22, group=None, prefix=None
     out = abi.ks_sim_out()
     ws = C.create_string_buffer(ws_bytes + 256)
     wsp = (C.addressof(ws) + 255) & ~255
-    st = abi.ks_simulate(_model(), 16, abi.ks_heads(), abi.ks_host(), _sched(), rq, out, wsp, ws_bytes, None,
-                         check=False)
+    st = abi.ks_simulate(_model(), 16, 1, abi.ks_heads(), abi.ks_host(), _sched(), rq, out, wsp, ws_bytes,
+                         None, check=False)
     return st, abi.ks_last_error()
 
 

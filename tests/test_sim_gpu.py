@@ -10,7 +10,12 @@ the oracle's scheduler and latency model.
 * End to end: the oracle's scheduler with the oracle model against the GPU
   run: metrics within 1e-5 relative (eta = 1, fp32 heads), when no
   scheduling decision sits within rounding of a tie (asserted by the
-  replay matching first)."""
+  replay matching first).
+* Lockstep: several simulations (one per spec vector) priced together each
+  round; every one replays exactly against the oracle's scheduler, its
+  latencies follow the oracle model under its own spec vector, and they
+  agree with a lone run of the same spec to the rounding order of the
+  per-step sums."""
 import numpy as np
 import pytest
 import torch  # noqa: F401
@@ -64,8 +69,8 @@ def sched_struct(cfg):
                         cfg.kv_blocks)
 
 
-def oracle_latency(shape, heads, eta_one, spec_i=0):
-    specs = one_spec(spec_i)
+def oracle_latency(shape, heads, eta_one, spec_i=0, table=None):
+    specs = one_spec(spec_i) if table is None else {k: np.asarray(v)[spec_i:spec_i + 1] for k, v in table.items()}
     hostc = gen.HostConsts()
 
     def f(batch, prefill):
@@ -196,3 +201,70 @@ def test_prefix_cache_saves_prefill_tokens():
     off = run_gpu(gen.LLAMA7B, reqs, off_cfg, "eta1")[0]
     assert on["entry_q"].sum() < off["entry_q"].sum()
     assert np.median(on["ttft"]) <= np.median(off["ttft"])
+
+
+def _lockstep(kind, cfg, reqs, table, shape=gen.LLAMA7B):
+    hd, keep, h, eta_one = device_heads(kind)
+    many = abi.simulate_many(shape, table, hd, host_struct(), sched_struct(cfg), reqs)
+    return many, hd, keep, h, eta_one
+
+
+def _rows(table, rows):
+    return {k: np.asarray(v)[rows] for k, v in table.items()}
+
+
+@pytest.mark.parametrize("kind", ["eta1", "bf16"])
+def test_lockstep_simulations_each_follow_their_own_spec(kind):
+    # six hypothetical GPUs of the capacity-planning grid and the two
+    # datasheet rows, all fed the same requests
+    cfg = CFGS["tight"]
+    reqs = gen.make_requests(50, rate=35.0, seed=15, prompt_median=320, output_median=40)
+    grid, ds = gen.specs_grid(6, 7), gen.specs_datasheet()
+    table = {k: np.concatenate([np.asarray(grid[k]), np.asarray(ds[k])]) for k in ds}
+    many, hd, keep, h, eta_one = _lockstep(kind, cfg, reqs, table)
+    assert len(many) == 8
+    tol = 1e-2 if kind == "bf16" else 1e-5
+    for i, res in enumerate(many):
+        assert res["n_steps"] > 0 and (res["state"] == osim.FINISHED).all()
+        r = replay(reqs, cfg, res)
+        np.testing.assert_array_equal(res["ttft"], r.ttft)
+        np.testing.assert_array_equal(res["e2e"], r.e2e)
+        f = oracle_latency(gen.LLAMA7B, h, eta_one, spec_i=i, table=table)
+        steps = gpu_steps(res)
+        for j in np.unique(np.linspace(0, res["n_steps"] - 1, 12).astype(int)):
+            want = f([(q, hh) for (_, q, hh) in steps[j]], bool(res["step_prefill"][j]))
+            assert abs(res["step_latency"][j] - want) <= tol * want, (i, j, res["step_latency"][j], want)
+    # the spec vectors differ, so the runs do: distinct clocks and step counts
+    assert len({res["clock"] for res in many}) == len(many)
+    assert len({res["n_steps"] for res in many}) > 1
+
+
+def test_lockstep_agrees_with_lone_runs():
+    cfg = CFGS["roomy"]
+    reqs = gen.make_requests(40, rate=30.0, seed=16, prompt_median=256, output_median=32)
+    table = gen.specs_grid(3, 8)
+    many, hd, keep, h, eta_one = _lockstep("f32", cfg, reqs, table)
+    for i, res in enumerate(many):
+        lone = abi.simulate_many(gen.LLAMA7B, _rows(table, [i]), hd, host_struct(), sched_struct(cfg), reqs)[0]
+        assert lone["n_steps"] == res["n_steps"]
+        np.testing.assert_array_equal(lone["entry_q"], res["entry_q"])
+        np.testing.assert_array_equal(lone["entry_h"], res["entry_h"])
+        np.testing.assert_allclose(res["step_latency"], lone["step_latency"], rtol=1e-6, atol=0)
+        np.testing.assert_allclose(res["e2e"], lone["e2e"], rtol=1e-6, atol=0)
+
+
+def test_lockstep_with_a_repeated_spec_and_an_empty_run():
+    # the same spec twice gives the same schedule twice, with latencies equal
+    # up to where each step sits in the round's batch (the rounding order of
+    # its sums); no requests leaves every simulation empty
+    cfg = CFGS["noprefix"]
+    reqs = gen.make_requests(20, rate=20.0, seed=17, prompt_median=128, output_median=16)
+    ds = gen.specs_datasheet()
+    many = _lockstep("eta1", cfg, reqs, _rows(ds, [1, 1]))[0]
+    np.testing.assert_array_equal(many[0]["entry_q"], many[1]["entry_q"])
+    np.testing.assert_array_equal(many[0]["entry_h"], many[1]["entry_h"])
+    np.testing.assert_allclose(many[0]["step_latency"], many[1]["step_latency"], rtol=1e-6, atol=0)
+    np.testing.assert_allclose(many[0]["e2e"], many[1]["e2e"], rtol=1e-6, atol=0)
+    empty = {"arrival": np.zeros(0), "prompt": u32([]), "output": u32([])}
+    for res in _lockstep("eta1", cfg, empty, _rows(ds, [0, 1, 0]))[0]:
+        assert res["n_steps"] == 0 and res["clock"] == 0.0
