@@ -275,12 +275,15 @@ def round_bf16(x):
 
 def head_forward(x, w1, w2, b2, w3, b3, emulate_bf16=False):
     """z = w3 . relu(W2 relu(W1 x) + b2) + b3 for the rows of x (one family's
-    parameters).  With emulate_bf16 the layer inputs x, h1 and h2 are rounded
-    to bfloat16 before each product; products and sums stay float64."""
+    parameters).  With emulate_bf16 the inputs of the two matrix layers, x
+    and h1, are rounded to bfloat16 before their products (the layers the
+    bf16 heads run as bfloat16 matrix products); the last layer, a dot
+    product with w3, takes relu(h2) unrounded.  Products and sums stay
+    float64."""
     r = round_bf16 if emulate_bf16 else (lambda v: v)
     h1 = np.maximum(r(x) @ w1.T, 0.0)
     h2 = np.maximum(r(h1) @ w2.T + b2, 0.0)
-    return r(h2) @ w3 + b3
+    return h2 @ w3 + b3
 
 
 def bounded_eta(x16, W, g, a):

@@ -49,16 +49,17 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
 }
 
+// relu on an fp32 value through its bits: a negative float is a negative
+// int32 (one integer max, no canonicalization of the input)
+__device__ __forceinline__ float relu_f(float x) {
+  return __builtin_bit_cast(float, max(__builtin_bit_cast(int, x), 0));
+}
+
 // relu on a packed bfloat16 pair: a negative bf16 is a negative int16
 __device__ __forceinline__ uint32_t relu_bf16x2(uint32_t v) {
   s16x2 s = __builtin_bit_cast(s16x2, v);
   s16x2 z = {0, 0};
   return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(s, z));
-}
-
-__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
-  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a),
-                                         __builtin_bit_cast(bf16x2, b), c, false);
 }
 
 __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
@@ -516,7 +517,7 @@ struct HeadBF16 {
   static constexpr int W1_DW = MB * KC1 * 64 * 4;
   static constexpr int W2_DW = MB * KC2 * 64 * 4;
   static constexpr int B2_DW = MB * 2 * 16;
-  static constexpr int W3_DW = MB * 2 * 8;
+  static constexpr int W3_DW = MB * 2 * 16;
   static constexpr int OFF_W2 = W1_DW;
   static constexpr int OFF_B2 = OFF_W2 + W2_DW;
   static constexpr int OFF_W3 = OFF_B2 + B2_DW;
@@ -573,21 +574,20 @@ struct HeadBF16 {
       lds[OFF_B2 + d] = __builtin_bit_cast(uint32_t, bf16_to_f32(b2[out_of(mb, g, r)]));
     }
     for (int d = threadIdx.x; d < W3_DW; d += kWgThreads) {
-      const int r = (d & 7) * 2, g = (d >> 3) & 1, mb = d >> 4;
-      lds[OFF_W3 + d] = (uint32_t)w3[out_of(mb, g, r)] | ((uint32_t)w3[out_of(mb, g, r + 1)] << 16);
+      const int r = d & 15, g = (d >> 4) & 1, mb = d >> 5;
+      lds[OFF_W3 + d] = __builtin_bit_cast(uint32_t, bf16_to_f32(w3[out_of(mb, g, r)]));
     }
     if (threadIdx.x == 0) lds[OFF_B3] = __builtin_bit_cast(uint32_t, bf16_to_f32(b3[0]));
   }
 
-  // layer 3 over one 32-unit block of layer 2: z += w3 . bf16(relu(h2))
+  // layer 3 over one 32-unit block of layer 2, in fp32: z += w3 . relu(h2)
   template <typename W3>
   __device__ static __forceinline__ void epilogue(const f32x16 &c0, const f32x16 &c1, const W3 &w3,
                                                   float &z0, float &z1) {
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const uint32_t w = w3[q];
-      z0 = dot2_bf16(relu_bf16x2(pack_bf16(c0[2 * q], c0[2 * q + 1])), w, z0);
-      z1 = dot2_bf16(relu_bf16x2(pack_bf16(c1[2 * q], c1[2 * q + 1])), w, z1);
+    for (int r = 0; r < 16; ++r) {
+      z0 = fmaf(w3[r], relu_f(c0[r]), z0);
+      z1 = fmaf(w3[r], relu_f(c1[r]), z1);
     }
   }
 
@@ -647,7 +647,7 @@ struct HeadBF16 {
     f32x16 a1[2][2];
     u32x4 H0[MB][2], H1[MB][2];
     f32x16 c0, c1, p0, p1, bias;
-    uint32_t w3r[2][8];
+    float w3r[2][16];
     float zacc[4];
     uint32_t lo[3];   // the lane's fragment offset (dwords) from LDS 0, 64 KB and 128 KB
     int lane, g;
@@ -687,7 +687,8 @@ struct HeadBF16 {
           st.p0 = st.c0;
           st.p1 = st.c1;
 #pragma unroll
-          for (int j = 0; j < 8; ++j) st.w3r[(q.mb - 1) & 1][j] = lds[OFF_W3 + ((q.mb - 1) * 2 + st.g) * 8 + j];
+          for (int j = 0; j < 16; ++j)
+            st.w3r[(q.mb - 1) & 1][j] = __builtin_bit_cast(float, lds[OFF_W3 + ((q.mb - 1) * 2 + st.g) * 16 + j]);
         }
         st.c1 = mfma(a, st.H1[0][0], st.bias);
         st.c0 = mfma(a, st.H0[0][0], st.bias);
@@ -699,28 +700,25 @@ struct HeadBF16 {
         st.bias = *(const f32x16 *)(lds + OFF_B2 + ((q.mb + 1) * 2 + st.g) * 16);
       if constexpr (q.kc == KC2 - 1 && q.mb == MB - 1) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) st.w3r[q.mb & 1][j] = lds[OFF_W3 + (q.mb * 2 + st.g) * 8 + j];
+        for (int j = 0; j < 16; ++j)
+          st.w3r[q.mb & 1][j] = __builtin_bit_cast(float, lds[OFF_W3 + (q.mb * 2 + st.g) * 16 + j]);
       }
     }
     fence();
     if constexpr (q.vk == kPackV) {
       pack_part(st.a1[q.vb & 1][0], st.a1[q.vb & 1][1], st.H0[q.vb], st.H1[q.vb], 4 * q.vj, 4 * q.vj + 4);
     } else if constexpr (q.vk == kEpiV) {
-      // relu + bf16 of the slice's pairs first, then their dot products
-      // with w3: a v_dot2c that reads a VGPR the instruction just before
-      // wrote waits for it, and the dots cost the most of this slice's
-      // VALU ops (measured: 1.1% of the capacity-grid kernel)
-      uint32_t hp0[2], hp1[2];
+      // layer 3 in fp32: relu through the sign bit, one FMA per hidden
+      // unit with w3 staged as fp32 (a v_dot2c on bf16 pairs issues
+      // alongside the MFMAs far worse than plain VALU ops: measured 1.7%
+      // slower on the capacity grid)
 #pragma unroll
       for (int j = q.vj; j < q.vj + q.vn; ++j) {
-        hp0[j - q.vj] = relu_bf16x2(pack_bf16(st.p0[2 * j], st.p0[2 * j + 1]));
-        hp1[j - q.vj] = relu_bf16x2(pack_bf16(st.p1[2 * j], st.p1[2 * j + 1]));
-      }
-#pragma unroll
-      for (int j = q.vj; j < q.vj + q.vn; ++j) {
-        const uint32_t w = st.w3r[q.vb & 1][j];
-        st.zacc[j & 1] = dot2_bf16(hp0[j - q.vj], w, st.zacc[j & 1]);
-        st.zacc[2 + (j & 1)] = dot2_bf16(hp1[j - q.vj], w, st.zacc[2 + (j & 1)]);
+        const float *w = st.w3r[q.vb & 1];
+        st.zacc[j & 1] = fmaf(w[2 * j], relu_f(st.p0[2 * j]), st.zacc[j & 1]);
+        st.zacc[2 + (j & 1)] = fmaf(w[2 * j], relu_f(st.p1[2 * j]), st.zacc[2 + (j & 1)]);
+        st.zacc[j & 1] = fmaf(w[2 * j + 1], relu_f(st.p0[2 * j + 1]), st.zacc[j & 1]);
+        st.zacc[2 + (j & 1)] = fmaf(w[2 * j + 1], relu_f(st.p1[2 * j + 1]), st.zacc[2 + (j & 1)]);
       }
       // an empty use pins the slice here; otherwise the dot chain, whose
       // result is only needed at the end, is sunk below every MFMA
@@ -778,18 +776,12 @@ struct HeadBF16 {
     st.p0 = st.c0;
     st.p1 = st.c1;
 #pragma unroll
-    for (int j0 = 0; j0 < 8; j0 += 4) {
-      uint32_t f0[4], f1[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        f0[j] = relu_bf16x2(pack_bf16(st.p0[2 * (j0 + j)], st.p0[2 * (j0 + j) + 1]));
-        f1[j] = relu_bf16x2(pack_bf16(st.p1[2 * (j0 + j)], st.p1[2 * (j0 + j) + 1]));
-      }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        st.zacc[j & 1] = dot2_bf16(f0[j], st.w3r[(MB - 1) & 1][j0 + j], st.zacc[j & 1]);
-        st.zacc[2 + (j & 1)] = dot2_bf16(f1[j], st.w3r[(MB - 1) & 1][j0 + j], st.zacc[2 + (j & 1)]);
-      }
+    for (int j = 0; j < 8; ++j) {
+      const float *w = st.w3r[(MB - 1) & 1];
+      st.zacc[j & 1] = fmaf(w[2 * j], relu_f(st.p0[2 * j]), st.zacc[j & 1]);
+      st.zacc[2 + (j & 1)] = fmaf(w[2 * j], relu_f(st.p1[2 * j]), st.zacc[2 + (j & 1)]);
+      st.zacc[j & 1] = fmaf(w[2 * j + 1], relu_f(st.p0[2 * j + 1]), st.zacc[j & 1]);
+      st.zacc[2 + (j & 1)] = fmaf(w[2 * j + 1], relu_f(st.p1[2 * j + 1]), st.zacc[2 + (j & 1)]);
     }
     // lanes l and l ^ 32 hold the two halves of the same record's dot
     // product; after the swap lane l < 32 adds block 0's halves of record
@@ -869,7 +861,7 @@ struct HeadBF16 {
       wf[1] = frag_w2(lds, 0, 1, lane);
       f32x16 bias = *(const f32x16 *)(lds + OFF_B2 + g * 16);
       f32x16 c0 = {}, c1 = {}, p0 = {}, p1 = {};
-      uint32_t w3r[8];
+      float w3r[16];
       float z0 = 0.0f, z1 = 0.0f;
       fence();
 #pragma unroll
@@ -881,7 +873,7 @@ struct HeadBF16 {
           p0 = c0;
           p1 = c1;
 #pragma unroll
-          for (int q = 0; q < 8; ++q) w3r[q] = lds[OFF_W3 + ((mb - 1) * 2 + g) * 8 + q];
+          for (int q = 0; q < 16; ++q) w3r[q] = __builtin_bit_cast(float, lds[OFF_W3 + ((mb - 1) * 2 + g) * 16 + q]);
         }
         const u32x4 a = wf[i % 3];
         if (kc == 0) {
@@ -903,8 +895,10 @@ struct HeadBF16 {
           // [8 kc / KC2, 8 (kc + 1) / KC2) of the 8
 #pragma unroll
           for (int q = kc * 8 / KC2; q < (kc + 1) * 8 / KC2; ++q) {
-            z0 = dot2_bf16(relu_bf16x2(pack_bf16(p0[2 * q], p0[2 * q + 1])), w3r[q], z0);
-            z1 = dot2_bf16(relu_bf16x2(pack_bf16(p1[2 * q], p1[2 * q + 1])), w3r[q], z1);
+            z0 = fmaf(w3r[2 * q], relu_f(p0[2 * q]), z0);
+            z1 = fmaf(w3r[2 * q], relu_f(p1[2 * q]), z1);
+            z0 = fmaf(w3r[2 * q + 1], relu_f(p0[2 * q + 1]), z0);
+            z1 = fmaf(w3r[2 * q + 1], relu_f(p1[2 * q + 1]), z1);
           }
           // an empty use pins this part here; otherwise the dot chain, whose
           // result is only needed at the end, is sunk below every MFMA
@@ -913,7 +907,7 @@ struct HeadBF16 {
         fence();
       }
 #pragma unroll
-      for (int q = 0; q < 8; ++q) w3r[q] = lds[OFF_W3 + ((MB - 1) * 2 + g) * 8 + q];
+      for (int q = 0; q < 16; ++q) w3r[q] = __builtin_bit_cast(float, lds[OFF_W3 + ((MB - 1) * 2 + g) * 16 + q]);
       epilogue(c0, c1, w3r, z0, z1);
       // lanes l and l ^ 32 hold the two halves of the same record's dot
       // product; after the swap lane l < 32 adds block 0's halves of record

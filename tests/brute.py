@@ -86,7 +86,9 @@ def ring_allreduce_bytes(P, S):
 
 
 def mlp_scalar(x, w1, w2, b2, w3, b3, rnd=lambda v: v):
-    """z for one feature vector, with explicit [out][in] indexing."""
+    """z for one feature vector, with explicit [out][in] indexing; rnd
+    rounds the inputs of the two matrix layers (x and h1), the last layer
+    takes relu(h2) as it is."""
     H, I = len(w1), len(x)
     xr = [rnd(v) for v in x]
     h1 = []
@@ -100,7 +102,7 @@ def mlp_scalar(x, w1, w2, b2, w3, b3, rnd=lambda v: v):
         s = b2[o]
         for i in range(H):
             s += w2[o][i] * h1[i]
-        h2.append(rnd(max(s, 0.0)))
+        h2.append(max(s, 0.0))
     z = b3
     for i in range(H):
         z += w3[i] * h2[i]
