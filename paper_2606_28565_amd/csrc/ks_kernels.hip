@@ -359,7 +359,7 @@ __device__ __forceinline__ RowC row_consts(const Cnt &c, uint32_t n, uint32_t k)
 }
 
 // Block counts below 2^23 (every record of the workloads): the wave count
-// in fp32 and 24-bit integer products.  With B < 2^23, fl(B fl(1/N)) is
+// in fp32 with exact integer-valued products.  With B < 2^23, fl(B fl(1/N)) is
 // within 1/N of B/N, so its ceiling is exact unless B/N is an integer k,
 // where it may come out k + 1; one test of (W - 1) N >= B corrects that.
 // W N <= B + N < 2^24, so the products are exact.
@@ -374,13 +374,12 @@ template <bool kSmall>
 __device__ __forceinline__ Roof roofline(const RowC &r, const SpecC &s) {
   Roof o;
   if constexpr (kSmall) {
-    // (selects, not branches: the correction stays in the VALU stream)
-    const uint32_t B = (uint32_t)r.B;
-    const uint32_t W0 = (uint32_t)ceilf(r.Bf * s.rcp_n);
-    const uint32_t Wm = W0 > 0u ? W0 - 1u : 0u;
-    const uint32_t W = (W0 > 0u && __umul24(Wm, s.n) >= B) ? Wm : W0;
-    o.W = (float)W;
-    o.u = B > 0u ? (float)__umul24(W, s.n) * r.rcp_b : 1.0f;
+    // in fp32 with selects: W0 N and (W0 - 1) N are integers below 2^24,
+    // exact in fp32; for B = 0, W0 = 0 and the test fails
+    const float W0 = ceilf(r.Bf * s.rcp_n);
+    const float W = (W0 - 1.0f) * s.n_f >= r.Bf ? W0 - 1.0f : W0;
+    o.W = W;
+    o.u = r.Bf > 0.0f ? W * s.n_f * r.rcp_b : 1.0f;
   } else if (r.B > 0) {
     const uint64_t W = ceil_div(r.B, s.n, s.rcp_nd);
     o.W = (float)W;
