@@ -463,11 +463,14 @@ class DeviceBatch:
         _, fam_off = ks_expand_layout(self.model, S, n_pre, mode)
         self.fam_off = fam_off
         n = fam_off[-1]
-        for name in ("step", "m", "n", "k", "a", "b", "mult"):
+        # the per-layer form has no multiplicities: its records are written
+        # without them (NULL), and the descriptor carries none
+        fields = ("step", "m", "n", "k", "a", "b") + (("mult",) if mode == KS_EXPAND_HOMOGENEOUS else ())
+        for name in fields:
             self.t[name] = torch.empty(n, dtype=torch.int32, device=dev)
         for name in ("layers", "hidden", "tp", "n_launch"):
             self.t["s_" + name] = torch.empty(S, dtype=torch.int32, device=dev)
-        self.out = ks_records(*(_ptr(self.t[name]) if n else None
+        self.out = ks_records(*(_ptr(self.t[name]) if n and name in self.t else None
                                 for name in ("step", "m", "n", "k", "a", "b", "mult")),
                               *(_ptr(self.t["s_" + name]) if S else None
                                 for name in ("layers", "hidden", "tp", "n_launch")))

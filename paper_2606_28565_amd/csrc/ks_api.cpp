@@ -604,7 +604,15 @@ ks_status ks_expand(const ks_model *model, const ks_batch *batch, int32_t mode, 
     for (int t = 0; t < ks::kExpandTpl; ++t) p.tpl[f][t] = pl.tpl[f][t];
     p.item_off[f + 1] = p.item_off[f] + (int64_t)p.per_step[f] * S;
     p.fam_off[f + 1] = p.fam_off[f] + pl.count[f];
+    if (p.per_step[f] >= (1u << 16) || p.item_off[f + 1] - p.item_off[f] >= (int64_t(1) << 31))
+      return fail(KS_ERANGE, "family %d: %u records per step or %lld items beyond the expansion's limits", f,
+                  p.per_step[f], (long long)(p.item_off[f + 1] - p.item_off[f]));
+    p.inv_ps[f] = p.per_step[f] ? 1.0 / (double)p.per_step[f] : 0.0;
+    p.inv_tpl[f] = 1.0f / (float)p.n_tpl[f];
   }
+  p.chunk_off[0] = 0;
+  for (int f = 0; f < KS_NFAM; ++f)
+    p.chunk_off[f + 1] = p.chunk_off[f] + (p.item_off[f + 1] - p.item_off[f] + 255) / 256;
   p.tok = reinterpret_cast<uint32_t *>(w + L.tok);
   p.rank = reinterpret_cast<uint32_t *>(w + L.rank);
   p.blk = reinterpret_cast<uint32_t *>(w + L.blk);

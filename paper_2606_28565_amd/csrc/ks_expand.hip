@@ -116,52 +116,67 @@ __global__ __launch_bounds__(256) void k_expand_scan(ExpandParams p) {
 // steps, the others to ATTN_DECODE at their rank among the rest (an item
 // whose rank is beyond the family's records, when the flags disagree with
 // n_prefill, is not written).
+//
+// A workgroup pass covers one 256-item chunk of one family, so the family,
+// its templates and its divisors are wave-uniform: the step index comes from
+// one fp64 FMA (i / per_step: exact below 2^31 items with per_step < 2^16,
+// the 2^-20 lift keeps whole quotients whole), the layer from one fp32 FMA
+// (slot / n_tpl with slot < 2^16), the template from selects among the
+// family's at most four, and the record index is 32-bit.
 __global__ __launch_bounds__(256) void k_expand_records(ExpandParams p) {
-  const int64_t total = p.item_off[KS_NFAM];
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t n_chunks = p.chunk_off[KS_NFAM];
   const int64_t n_pre = p.n_prefill, n_dec = p.n_steps - p.n_prefill;
   uint32_t bad = 0;
   int f = 0;
-  for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < total; g += stride) {
-    while (g >= p.item_off[f + 1]) ++f;
-    const uint32_t idx = (uint32_t)(g - p.item_off[f]);
+  for (int64_t c = blockIdx.x; c < n_chunks; c += gridDim.x) {
+    while (c >= p.chunk_off[f + 1]) ++f;
+    const int64_t i64 = (c - p.chunk_off[f]) * 256 + threadIdx.x;
+    if (i64 >= p.item_off[f + 1] - p.item_off[f]) continue;
+    const uint32_t idx = (uint32_t)i64;
     const uint32_t ps = p.per_step[f];
-    const uint32_t j = idx / ps;
+    const uint32_t j = (uint32_t)__builtin_fma((double)idx, p.inv_ps[f], 0x1p-20);
     const uint32_t slot = idx - j * ps;
-    const uint32_t nt = p.n_tpl[f];
-    const uint32_t layer = slot / nt;
-    const ExpandTpl t = p.tpl[f][slot - layer * nt];
-    int64_t dst;
+    const uint32_t layer = (uint32_t)fmaf((float)slot, p.inv_tpl[f], 0x1p-6f);
+    const uint32_t ti = slot - layer * p.n_tpl[f];
+    const ExpandTpl t0 = p.tpl[f][0], t1 = p.tpl[f][1], t2 = p.tpl[f][2], t3 = p.tpl[f][3];
+    const uint32_t tn = ti == 0 ? t0.n : ti == 1 ? t1.n : ti == 2 ? t2.n : t3.n;
+    const uint32_t tk = ti == 0 ? t0.k : ti == 1 ? t1.k : ti == 2 ? t2.k : t3.k;
+    const uint32_t ta = ti == 0 ? t0.a : ti == 1 ? t1.a : ti == 2 ? t2.a : t3.a;
+    const uint32_t tm = ti == 0 ? t0.msrc : ti == 1 ? t1.msrc : ti == 2 ? t2.msrc : t3.msrc;
+    const uint32_t tg = ti == 0 ? t0.grouped : ti == 1 ? t1.grouped : ti == 2 ? t2.grouped : t3.grouped;
+    uint32_t dst;
     if (f == KS_ATTN_PREFILL) {
       const int64_t r = (int64_t)p.blk[j / kExpandBlk] + p.rank[j];
+      int64_t d;
       if (p.prefill[j] != 0) {
-        dst = r < n_pre ? p.fam_off[KS_ATTN_PREFILL] + r * ps + slot : -1;
+        d = r < n_pre ? p.fam_off[KS_ATTN_PREFILL] + r * ps + slot : -1;
       } else {
         const int64_t rd = (int64_t)j - r;
-        dst = (rd >= 0 && rd < n_dec) ? p.fam_off[KS_ATTN_DECODE] + rd * ps + slot : -1;
+        d = (rd >= 0 && rd < n_dec) ? p.fam_off[KS_ATTN_DECODE] + rd * ps + slot : -1;
       }
-      if (dst < 0) {
+      if (d < 0) {
         bad |= kErrPrefill;
         continue;
       }
+      dst = (uint32_t)d;
     } else {
-      dst = p.fam_off[f] + idx;
+      dst = (uint32_t)p.fam_off[f] + idx;
     }
     uint32_t m = 0;
-    if (t.msrc == kMTok) {
+    if (tm == kMTok) {
       m = p.tok[j];
-    } else if (t.msrc == kMTopk) {
+    } else if (tm == kMTopk) {
       m = p.tok[j] * p.top_k;
-    } else if (t.msrc == kMReq) {
+    } else if (tm == kMReq) {
       const uint32_t r0 = p.req_off[j], r1 = p.req_off[j + 1];
       m = r1 >= r0 ? r1 - r0 : 0u;
     }
     p.o_step[dst] = j;
     p.o_m[dst] = m;
-    p.o_n[dst] = t.n;
-    p.o_k[dst] = t.k;
-    p.o_a[dst] = t.a;
-    p.o_b[dst] = t.grouped ? (j * p.L + layer) * p.E : 0u;
+    p.o_n[dst] = tn;
+    p.o_k[dst] = tk;
+    p.o_a[dst] = ta;
+    p.o_b[dst] = tg ? (j * p.L + layer) * p.E : 0u;
     if (p.o_mult) p.o_mult[dst] = p.mult[f];
   }
   if (bad) atomicOr(p.err, bad);
@@ -189,7 +204,7 @@ hipError_t launch_expand(const ExpandParams &p, hipStream_t s, hipEvent_t before
     if (e != hipSuccess) return e;
   }
   if (p.item_off[KS_NFAM] > 0) {
-    hipLaunchKernelGGL(k_expand_records, dim3(grid_cap(p.item_off[KS_NFAM], 256, 8192)), dim3(256), 0, s, p);
+    hipLaunchKernelGGL(k_expand_records, dim3(grid_cap(p.chunk_off[KS_NFAM] * 256, 256, 8192)), dim3(256), 0, s, p);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -126,7 +126,8 @@ constexpr int kExpandBlk = 1024;      // steps per block of the prefill-rank sca
 // KS_ATTN_DECODE has no items) owns items [item_off[f], item_off[f+1]),
 // per_step[f] per step; item i of the family is step i / per_step[f] and
 // slot i % per_step[f], whose template is slot % n_tpl[f] and whose layer is
-// slot / n_tpl[f].
+// slot / n_tpl[f].  The host guarantees per_step[f] < 2^16 and fewer than
+// 2^31 items per family (the quotients are then exact in floating point).
 struct ExpandParams {
   const uint32_t *req_off, *req_q;
   int64_t n_req;
@@ -134,6 +135,9 @@ struct ExpandParams {
   int64_t n_steps, n_prefill;
   uint32_t L, E, top_k, D, P;
   int64_t item_off[KS_NFAM + 1];
+  int64_t chunk_off[KS_NFAM + 1];   // 256-item chunks of each family: one per workgroup pass
+  double inv_ps[KS_NFAM];           // 1 / per_step[f], for the step index of an item
+  float inv_tpl[KS_NFAM];           // 1 / n_tpl[f], for the layer of a slot
   uint32_t per_step[KS_NFAM];
   uint32_t n_tpl[KS_NFAM];
   uint32_t mult[KS_NFAM];
