@@ -282,7 +282,7 @@ size_t ks_expand_workspace_bytes(int64_t n_steps);
 /* Writes the records of the batch (asynchronous on `stream`).  Host checks
  * as ks_expand_layout plus null pointers and the workspace, and KS_ERANGE
  * for a family with 2^16 or more records per step or 2^31 or more records
- * in the batch (the record writer's index arithmetic).  Device data
+ * in all (the record writer's index arithmetic).  Device data
  * that disagrees with the call (request offsets out of order or beyond
  * n_req, a step's T or top_k T at or above 2^24, a prefill flag count other
  * than n_prefill) raises a flag that ks_device_status(ws) reports; the
