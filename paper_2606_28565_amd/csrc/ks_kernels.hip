@@ -1136,15 +1136,17 @@ __device__ __forceinline__ Tile locate(const EvalParams &p, int wt, int wave, in
 }
 
 // The record fields a lane's family uses (the others are never read), plus
-// the steps just before and after the tile within its family.
+// the steps just before and after the tile within its family: prev and next
+// by scalar loads, or (VEC) pn by one vector load, the one before in lane 0
+// and the one after in the other lanes (see tile_edges).
 struct Fields {
-  uint32_t st, m, n, k, a, b, prev, next;
+  uint32_t st, m, n, k, a, b, prev, next, pn;
   float mult;   // dispatches the record stands for (1 without a multiplicity array)
 };
 
-template <bool MULT>
+template <bool MULT, bool VEC>
 __device__ __forceinline__ Fields load_fields(const EvalParams &p, const Tile &t, int lane) {
-  Fields f = {0, 0, 0, 0, 0, 0, kNoKey, kNoKey, 1.0f};
+  Fields f = {0, 0, 0, 0, 0, 0, kNoKey, kNoKey, kNoKey, 1.0f};
   if (t.nvalid == 0) return f;
   // wave-uniform bases plus a 32-bit lane offset (no per-lane 64-bit
   // address arithmetic)
@@ -1160,9 +1162,32 @@ __device__ __forceinline__ Fields load_fields(const EvalParams &p, const Tile &t
   if (grouped || attn) f.a = (p.a + r0)[off];
   if (grouped) f.b = (p.b + r0)[off];
   if constexpr (MULT) f.mult = (float)(p.mult + r0)[off];   // exact below 2^24
-  if (t.row0 > t.fam_lo) f.prev = p.step[t.row0 - 1];
-  if (t.row0 + kTileRows < t.fam_hi) f.next = p.step[t.row0 + kTileRows];
+  const bool hp = t.row0 > t.fam_lo, hn = t.row0 + kTileRows < t.fam_hi;
+  if constexpr (VEC) {
+    // one vector load for both neighbours (each lane's address stays inside
+    // the family: the tile's first row where a neighbour does not exist).
+    // In a short loop a scalar load here costs its whole latency: the next
+    // scalar load of the spec loop waits for it (scalar loads complete out
+    // of order, so waits are for all of them).
+    const int pn_off = lane == 0 ? (hp ? -1 : 0) : (hn ? kTileRows : 0);
+    f.pn = (p.step + r0)[pn_off];
+  } else {
+    if (hp) f.prev = p.step[t.row0 - 1];
+    if (hn) f.next = p.step[t.row0 + kTileRows];
+  }
   return f;
+}
+
+// the steps just before and after tile t (kNoKey where the family ends)
+template <bool VEC>
+__device__ __forceinline__ void tile_edges(const Tile &t, const Fields &f, uint32_t &prev, uint32_t &next) {
+  if constexpr (VEC) {
+    prev = t.row0 > t.fam_lo ? __builtin_amdgcn_readlane(f.pn, 0) : kNoKey;
+    next = t.row0 + kTileRows < t.fam_hi ? __builtin_amdgcn_readlane(f.pn, 1) : kNoKey;
+  } else {
+    prev = f.prev;
+    next = f.next;
+  }
 }
 
 // Variants, each a separate instantiation so that the kernels without them
@@ -1184,17 +1209,19 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
   int staged = -1;
   // the next tile's fields are loaded while the current one is evaluated
   Tile tn = {};
-  Fields fn = {0, 0, 0, 0, 0, 0, kNoKey, kNoKey, 1.0f};
+  Fields fn = {0, 0, 0, 0, 0, 0, kNoKey, kNoKey, kNoKey, 1.0f};
+  // tiles without a head take their neighbour steps by a vector load
+  constexpr bool VEC = !H::kMlp;
   if ((int)blockIdx.x < n_wgt) {
     tn = locate(p, blockIdx.x, wave, 0);
-    fn = load_fields<MULT>(p, tn, lane);
+    fn = load_fields<MULT, VEC>(p, tn, lane);
   }
   for (int wt = blockIdx.x; wt < n_wgt; wt += gridDim.x) {
     const Tile tc = tn;
     const Fields fc = fn;
     if (wt + (int)gridDim.x < n_wgt) {
       tn = locate(p, wt + gridDim.x, wave, tc.fam);
-      fn = load_fields<MULT>(p, tn, lane);
+      fn = load_fields<MULT, VEC>(p, tn, lane);
     }
     const int fam = tc.fam;
     // this family takes the bounded head (the plain eta = 1 stream has none)
@@ -1250,14 +1277,16 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
     const uint32_t key_dn = dpp_key<0x130, 0xf, 0xf>(key);   // wave_shl:1, lane 63: unequal
     const bool is_tail = live && key_dn != key;
     const uint32_t key0 = __builtin_amdgcn_readfirstlane(key);
-    const bool to_carry = is_tail && key == key0 && fc.prev == key0;
+    uint32_t prev, next;
+    tile_edges<VEC>(tc, fc, prev, next);
+    const bool to_carry = is_tail && key == key0 && prev == key0;
     const int tile_id = p.tile_off[fam] + tc.tile_in_fam;
     if (p.range) {
       // the (family, step) record range, written where its global first
       // and last records are
       const uint32_t key_up = dpp_key<0x138, 0xf, 0xf>(key);   // wave_shr:1
-      const bool head = live && (lane == 0 ? fc.prev != key : key_up != key);
-      const bool tail = live && (lane == nvalid - 1 ? fc.next != key : key_dn != key);
+      const bool head = live && (lane == 0 ? prev != key : key_up != key);
+      const bool tail = live && (lane == nvalid - 1 ? next != key : key_dn != key);
       if (head) p.range[2 * ((size_t)fam * p.n_steps + key)] = (uint32_t)row;
       if (tail) p.range[2 * ((size_t)fam * p.n_steps + key) + 1] = (uint32_t)(row + 1);
     }
