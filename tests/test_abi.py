@@ -251,6 +251,11 @@ def test_expand_host_checks():
         setattr(out, name, 16)
     assert abi.ks_expand(md, b, 0, out, wsp, 8, None, check=False) == abi.KS_EWORKSPACE
     assert abi.ks_expand(md, b, 0, out, wsp + 8, 1 << 15, None, check=False) == abi.KS_EWORKSPACE
+    # the record writer's index arithmetic: a family with 2^16 or more
+    # records per step (20,000 layers x 4 GEMMs) is refused before any launch
+    deep = _model(layers=20_000)
+    assert abi.ks_expand(deep, b, 0, out, wsp, 1 << 15, None, check=False) == abi.KS_ERANGE
+    assert "limits" in abi.ks_last_error()
 
 
 # ---- serving simulation (host side only)
