@@ -399,6 +399,9 @@ __device__ __forceinline__ Roof roofline(const RowC &r, const SpecC &s) {
 // occupancy B / (W N) is 1 / u
 template <bool RAW = false>
 __device__ __forceinline__ float feature(int i, const RowC &r, const SpecC &s, const Roof &o) {
+  // the same rounding wherever the features are formed: no product is fused
+  // into a sum (t_comp + t_mem of feature 7 would be, in some schedules)
+#pragma clang fp contract(off)
   constexpr float k16 = RAW ? 1.0f : 1.0f / 16;
   switch (i) {
     case 0: return r.x0;
@@ -663,8 +666,13 @@ struct HeadBF16 {
     return *(const u32x4 *)(lds + lo[off >> 14] + (off & 16383));
   }
 
-  template <int I>
-  __device__ static __forceinline__ void group(S4 &st, const uint32_t *lds) {
+  struct NoHook {
+    template <class IC>
+    __device__ __forceinline__ void operator()(IC) const {}
+  };
+
+  template <int I, class F = NoHook>
+  __device__ static __forceinline__ void group(S4 &st, const uint32_t *lds, F &&hook = F{}) {
     constexpr Grp q = sched(I);
     // weight fragment of the group two ahead
     if constexpr (I + 2 < kNG && sched(I + 2).mk != 0) st.frag[(I + 2) % 3] = frag_of<I + 2>(lds, st.lo);
@@ -723,12 +731,79 @@ struct HeadBF16 {
       // result is only needed at the end, is sunk below every MFMA
       asm volatile("" ::"v"(st.zacc[0]), "v"(st.zacc[1]), "v"(st.zacc[2]), "v"(st.zacc[3]));
     }
+    hook(std::integral_constant<int, I>{});
     fence();
   }
 
-  template <int... I>
-  __device__ static __forceinline__ void groups(S4 &st, const uint32_t *lds, std::integer_sequence<int, I...>) {
-    (group<I>(st, lds), ...);
+  template <class F, int... I>
+  __device__ static __forceinline__ void groups_h(S4 &st, const uint32_t *lds, F &hook,
+                                                  std::integer_sequence<int, I...>) {
+    (group<I>(st, lds, hook), ...);
+  }
+
+  // ---- the pieces of one spec's head (mlp4 runs them in order; the
+  // software-pipelined spec loop of k_eval spreads the last block's
+  // epilogue over the next spec's groups).  kPipe: the heads whose group
+  // schedule that loop knows.
+  static constexpr bool kPipe = MB == 4 && KC1 == 1;
+  __device__ static __forceinline__ void init_state(S4 &st) {
+    st.lane = threadIdx.x & 63;
+    st.g = st.lane >> 5;
+    st.lo[0] = st.lane * 4;
+    st.lo[1] = st.lo[0] + 16384;
+    st.lo[2] = st.lo[0] + 32768;
+    // opaque to the compiler, so it keeps the bases rather than forming
+    // each address beyond 64 KB anew
+    asm volatile("" : "+v"(st.lo[1]), "+v"(st.lo[2]));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) st.zacc[j] = 0.0f;
+  }
+  // before a spec's groups: its features, the first fragments and b2; the
+  // previous spec's partial layer-3 sums move to zp
+  __device__ static __forceinline__ void begin_spec(S4 &st, const u32x4 (&XB)[2][KC1], const uint32_t *lds,
+                                                    float (&zp)[4]) {
+#pragma unroll
+    for (int kc = 0; kc < KC1; ++kc) {
+      st.XB[0][kc] = XB[0][kc];
+      st.XB[1][kc] = XB[1][kc];
+    }
+    st.frag[0] = frag_of<0>(lds, st.lo);
+    st.frag[1] = frag_of<1>(lds, st.lo);
+    st.bias = *(const f32x16 *)(lds + OFF_B2 + st.g * 16);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      zp[j] = st.zacc[j];
+      st.zacc[j] = 0.0f;
+    }
+    fence();
+  }
+  template <class F>
+  __device__ static __forceinline__ void run_groups(S4 &st, const uint32_t *lds, F &hook) {
+    groups_h(st, lds, hook, std::make_integer_sequence<int, kNG>{});
+    // the last block's accumulators feed its epilogue in the next spec's groups
+    st.p0 = st.c0;
+    st.p1 = st.c1;
+  }
+  // register pairs [j0, j1) of the last block's epilogue into zp
+  __device__ static __forceinline__ void tail_pairs(const S4 &st, float (&zp)[4], int j0, int j1) {
+#pragma unroll
+    for (int j = j0; j < j1; ++j) {
+      const float *w = st.w3r[(MB - 1) & 1];
+      zp[j & 1] = fmaf(w[2 * j], relu_f(st.p0[2 * j]), zp[j & 1]);
+      zp[2 + (j & 1)] = fmaf(w[2 * j], relu_f(st.p1[2 * j]), zp[2 + (j & 1)]);
+      zp[j & 1] = fmaf(w[2 * j + 1], relu_f(st.p0[2 * j + 1]), zp[j & 1]);
+      zp[2 + (j & 1)] = fmaf(w[2 * j + 1], relu_f(st.p1[2 * j + 1]), zp[2 + (j & 1)]);
+    }
+  }
+  // z: lanes l and l ^ 32 hold the two halves of the same record's dot
+  // product; after the swap lane l < 32 adds block 0's halves of record l
+  // and lane l >= 32 block 1's halves of record l.
+  __device__ static __forceinline__ float tail_reduce(const float (&zp)[4], const uint32_t *lds) {
+    uint32_t u0 = __builtin_bit_cast(uint32_t, zp[0] + zp[1]);
+    uint32_t u1 = __builtin_bit_cast(uint32_t, zp[2] + zp[3]);
+    swap32(u0, u1);
+    return __builtin_bit_cast(float, u0) + __builtin_bit_cast(float, u1) +
+           __builtin_bit_cast(float, lds[OFF_B3]);
   }
 
   // x -> bf16 pairs; the swap turns "own record" into the B layout of the
@@ -749,47 +824,17 @@ struct HeadBF16 {
     }
   }
 
+  // one spec's head on the features XB: the groups, then the last block's
+  // epilogue and the reduction
   __device__ static __forceinline__ float mlp4(const u32x4 (&XB)[2][KC1], const uint32_t *lds) {
     S4 st;
-    st.lane = threadIdx.x & 63;
-    st.g = st.lane >> 5;
-#pragma unroll
-    for (int kc = 0; kc < KC1; ++kc) {
-      st.XB[0][kc] = XB[0][kc];
-      st.XB[1][kc] = XB[1][kc];
-    }
-    st.lo[0] = st.lane * 4;
-    st.lo[1] = st.lo[0] + 16384;
-    st.lo[2] = st.lo[0] + 32768;
-    // opaque to the compiler, so it keeps the bases rather than forming
-    // each address beyond 64 KB anew
-    asm volatile("" : "+v"(st.lo[1]), "+v"(st.lo[2]));
-    st.frag[0] = frag_of<0>(lds, st.lo);
-    st.frag[1] = frag_of<1>(lds, st.lo);
-    st.bias = *(const f32x16 *)(lds + OFF_B2 + st.g * 16);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) st.zacc[j] = 0.0f;
-    fence();
-    groups(st, lds, std::make_integer_sequence<int, kNG>{});
-    // the last block's epilogue: packing of four pairs ahead of their dots
-    st.p0 = st.c0;
-    st.p1 = st.c1;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const float *w = st.w3r[(MB - 1) & 1];
-      st.zacc[j & 1] = fmaf(w[2 * j], relu_f(st.p0[2 * j]), st.zacc[j & 1]);
-      st.zacc[2 + (j & 1)] = fmaf(w[2 * j], relu_f(st.p1[2 * j]), st.zacc[2 + (j & 1)]);
-      st.zacc[j & 1] = fmaf(w[2 * j + 1], relu_f(st.p0[2 * j + 1]), st.zacc[j & 1]);
-      st.zacc[2 + (j & 1)] = fmaf(w[2 * j + 1], relu_f(st.p1[2 * j + 1]), st.zacc[2 + (j & 1)]);
-    }
-    // lanes l and l ^ 32 hold the two halves of the same record's dot
-    // product; after the swap lane l < 32 adds block 0's halves of record
-    // l and lane l >= 32 block 1's halves of record l.
-    uint32_t u0 = __builtin_bit_cast(uint32_t, st.zacc[0] + st.zacc[1]);
-    uint32_t u1 = __builtin_bit_cast(uint32_t, st.zacc[2] + st.zacc[3]);
-    swap32(u0, u1);
-    return __builtin_bit_cast(float, u0) + __builtin_bit_cast(float, u1) +
-           __builtin_bit_cast(float, lds[OFF_B3]);
+    init_state(st);
+    float unused[4];
+    begin_spec(st, XB, lds, unused);
+    NoHook none;
+    run_groups(st, lds, none);
+    tail_pairs(st, st.zacc, 0, 8);
+    return tail_reduce(st.zacc, lds);
   }
 
   // z of the lane's own record; x: that record's features (fp32).
@@ -1195,6 +1240,30 @@ __device__ __forceinline__ void tile_edges(const Tile &t, const Fields &f, uint3
 // kVarMult weights each record's step-sum term by its multiplicity.
 enum : int { kVarGrid = 1, kVarMult = 2, kNumVars = 4 };
 
+// heads that take the software-pipelined spec loop
+template <class H, class = void> struct PipeOK : std::false_type {};
+template <class H> struct PipeOK<H, std::enable_if_t<H::kPipe>> : std::true_type {};
+
+// Spec s's per-pair outputs of the lane's record and its segmented step sum:
+// a tail lane stores its segment's sum to dst (the tile's carry slot or the
+// (spec, family, step) partial), a record of multiplicity m adding m t (one
+// fp32 rounding).
+template <bool MULT>
+__device__ __forceinline__ void spec_tail(const EvalParams &p, int s, float t_roof, float eta, float t, bool valid,
+                                          bool live, int64_t row, float tfac, const float (&fac)[6], double *dst,
+                                          size_t dst_stride) {
+  if (valid) {
+    const size_t i = (size_t)s * (size_t)p.fam_off[KS_NFAM] + (size_t)row;
+    if (p.o_troof) p.o_troof[i] = t_roof;
+    if (p.o_eta) p.o_eta[i] = eta;
+    if (p.o_t) p.o_t[i] = t;
+  }
+  if (p.partial) {
+    const float v = seg_scan(MULT ? t * tfac : (live ? t : 0.0f), fac);
+    if (dst) dst[(size_t)s * dst_stride] = (double)v;
+  }
+}
+
 template <int KIND, int VAR>
 __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalParams p) {
   constexpr bool GRID = (VAR & kVarGrid) != 0;
@@ -1314,6 +1383,77 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
       }
     }
 
+    if constexpr (PipeOK<H>::value && !GRID) {
+      if (!bnd) {
+        // Software-pipelined spec loop: spec s's MFMA groups carry, in their
+        // VALU slots, the last block's epilogue and the tail of spec s - 1
+        // (early groups) and the roofline and features of spec s + 1 (late
+        // groups), so that no VALU work of a spec stands outside the MFMA
+        // stream.  Spec s - 1's last-block accumulators and layer-3 partial
+        // sums live on in the head state (p0/p1, zp) until its epilogue
+        // has read them.
+        using S4 = typename H::S4;
+        S4 st;
+        H::init_state(st);
+        const int S = p.n_specs;
+        SpecC sc = spec_at(p.spec_c, 0);
+        Roof o = small ? roofline<true>(rc, sc) : roofline<false>(rc, sc);
+        u32x4 XB[2][1];
+        {
+          float x[IN];
+          features<IN, H::kRaw>(rc, sc, o, x);
+          H::pack_x(x, XB);
+        }
+        float zp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+        float tr_prev = 0.0f, t0_prev = 0.0f;
+        for (int s = 0; s < S; ++s) {
+          const SpecC sn = spec_at(p.spec_c, s + 1 < S ? s + 1 : s);
+          Roof on;
+          u32x4 XBn[2][1];
+          float eta_prev = 1.0f;
+          const float tr_cur = o.t_roof, t0_cur = sc.t0;
+          H::begin_spec(st, XB, lds, zp);
+          // group indices of the 36-group schedule of the 16-128 head:
+          // 0, 5, 6 and 11 carry no VALU work of their own
+          auto hook = [&](auto ic) {
+            constexpr int I = decltype(ic)::value;
+            if constexpr (I == 0) H::tail_pairs(st, zp, 0, 2);
+            if constexpr (I == 5) H::tail_pairs(st, zp, 2, 4);
+            if constexpr (I == 6) H::tail_pairs(st, zp, 4, 6);
+            if constexpr (I == 11) H::tail_pairs(st, zp, 6, 8);
+            if constexpr (I == 12) eta_prev = 1.0f + __expf(-H::tail_reduce(zp, lds));
+            if constexpr (I == 14) {
+              if (s > 0)
+                spec_tail<MULT>(p, s - 1, tr_prev, eta_prev, fmaxf(tr_prev * eta_prev, t0_prev), valid, live, row,
+                                tfac, fac, dst, dst_stride);
+            }
+            if constexpr (I == 20) on = small ? roofline<true>(rc, sn) : roofline<false>(rc, sn);
+            if constexpr (I == 26) {
+              float x[IN];
+              features<IN, H::kRaw>(rc, sn, on, x);
+              H::pack_x(x, XBn);
+            }
+          };
+          H::run_groups(st, lds, hook);
+          tr_prev = tr_cur;
+          t0_prev = t0_cur;
+          o = on;
+          sc = sn;
+          XB[0][0] = XBn[0][0];
+          XB[1][0] = XBn[1][0];
+        }
+        // the last spec's epilogue and tail
+        float zl[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) zl[j] = st.zacc[j];
+        H::tail_pairs(st, zl, 0, 4);
+        H::tail_pairs(st, zl, 4, 8);
+        const float eta = 1.0f + __expf(-H::tail_reduce(zl, lds));
+        spec_tail<MULT>(p, S - 1, tr_prev, eta, fmaxf(tr_prev * eta, t0_prev), valid, live, row, tfac, fac, dst,
+                        dst_stride);
+        continue;
+      }
+    }
     for (int s = 0; s < p.n_specs; ++s) {
       const SpecC sc = spec_at(p.spec_c, s);
       const Roof o = small ? roofline<true>(rc, sc) : roofline<false>(rc, sc);
@@ -1342,22 +1482,12 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
       }
       if (routed) eta = eta_g;
       const float t = fmaxf(o.t_roof * eta, sc.t0);
-      if (valid) {
-        const size_t i = (size_t)s * (size_t)p.fam_off[KS_NFAM] + (size_t)row;
-        if (p.o_troof) p.o_troof[i] = o.t_roof;
-        if (p.o_eta) p.o_eta[i] = eta;
-        if (p.o_t) p.o_t[i] = t;
-        // (without a grid the source is a per-family constant, written by
-        // k_fill_source instead, so the plain kernels keep their registers)
-        if constexpr (GRID) {
-          if (p.o_src) p.o_src[i] = routed ? 2 : (bnd ? 1 : 0);
-        }
+      // (without a grid the source is a per-family constant, written by
+      // k_fill_source instead, so the plain kernels keep their registers)
+      if constexpr (GRID) {
+        if (valid && p.o_src) p.o_src[(size_t)s * (size_t)p.fam_off[KS_NFAM] + (size_t)row] = routed ? 2 : (bnd ? 1 : 0);
       }
-      if (p.partial) {
-        // a record of multiplicity m adds m t (one fp32 rounding)
-        const float v = seg_scan(MULT ? t * tfac : (live ? t : 0.0f), fac);
-        if (dst) dst[(size_t)s * dst_stride] = (double)v;
-      }
+      spec_tail<MULT>(p, s, o.t_roof, eta, t, valid, live, row, tfac, fac, dst, dst_stride);
     }
   }
 }
