@@ -1410,11 +1410,13 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
           const SpecC sn = spec_at(p.spec_c, s + 1 < S ? s + 1 : s);
           Roof on;
           u32x4 XBn[2][1];
+          float xn[IN];
           float eta_prev = 1.0f;
           const float tr_cur = o.t_roof, t0_cur = sc.t0;
           H::begin_spec(st, XB, lds, zp);
-          // group indices of the 36-group schedule of the 16-128 head:
-          // 0, 5, 6 and 11 carry no VALU work of their own
+          // group indices of the 36-group schedule of the 16-128 head: 0, 5,
+          // 6 and 11 carry no VALU work of their own, nor do 20 and 28; the
+          // next spec's features are spread over three groups
           auto hook = [&](auto ic) {
             constexpr int I = decltype(ic)::value;
             if constexpr (I == 0) H::tail_pairs(st, zp, 0, 2);
@@ -1428,10 +1430,19 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
                                 tfac, fac, dst, dst_stride);
             }
             if constexpr (I == 20) on = small ? roofline<true>(rc, sn) : roofline<false>(rc, sn);
-            if constexpr (I == 26) {
-              float x[IN];
-              features<IN, H::kRaw>(rc, sn, on, x);
-              H::pack_x(x, XBn);
+            if constexpr (I == 22) {
+#pragma unroll
+              for (int i = 1; i < 4; ++i) xn[i] = feature<H::kRaw>(i, rc, sn, on);
+            }
+            if constexpr (I == 24) {
+#pragma unroll
+              for (int i = 4; i < 8; ++i) xn[i] = feature<H::kRaw>(i, rc, sn, on);
+            }
+            if constexpr (I == 28) {
+              xn[0] = feature<H::kRaw>(0, rc, sn, on);
+#pragma unroll
+              for (int i = 8; i < 16; ++i) xn[i] = feature<H::kRaw>(i, rc, sn, on);
+              H::pack_x(xn, XBn);
             }
           };
           H::run_groups(st, lds, hook);
