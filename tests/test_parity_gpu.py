@@ -159,6 +159,22 @@ def test_c4_subset_bf16_16_128():
     _bf16_case(gen.config4(n_specs=24, grid_steps=25, c1_steps=40))
 
 
+@pytest.mark.parametrize("n_specs", [1, 2, 3, 7])
+def test_spec_loop_counts_for_the_16_128_head(n_specs):
+    """The 16-128 head evaluates its spec loop software-pipelined (each
+    spec's epilogue and tail ride in the next spec's groups, its features in
+    the previous one's): any number of spec vectors against the oracle, and
+    every spec's outputs bit-identical to those of a call with only the
+    spec vectors up to it (a spec's results do not depend on its neighbours
+    in the loop)."""
+    wl = gen.config4(n_specs=8, grid_steps=12, c1_steps=20)
+    gpu, ref = _bf16_case(wl, n_specs=n_specs)
+    if n_specs > 1:
+        fewer = g.eval_steps(wl, n_specs=n_specs - 1)
+        for k in ("t_roof", "eta", "t_kernel", "t_body", "t_step"):
+            np.testing.assert_array_equal(gpu[k][:n_specs - 1], fewer[k], err_msg=k)
+
+
 def test_c3_moe_subset():
     _bf16_case(gen.config3(0, 30))
 
