@@ -1503,6 +1503,286 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
   }
 }
 
+// ------------------------------------------------------------ eta = 1 stream
+// The pure-roofline step sums (eta = 1, Eq. 2 and the segmented sum of
+// Sec. 5.6) when no per-pair output is asked for.  A wave takes a workgroup
+// tile on its own (256 consecutive records of one family: four 64-record
+// tiles) and each lane four consecutive records of it, so that each 16-lane
+// DPP row holds exactly one 64-record tile.  The fields arrive by coalesced
+// loads and are transposed through a wave-private LDS slot.  Per spec a lane
+// sums its records' t in runs of equal step (one FMA each); one segmented
+// scan per row then joins the lanes' last runs, and each run's tail record
+// adds the carry-in of the lanes before it.  The cross-lane work is thus per
+// four records instead of per record.  Runs are split at the 64-record tile
+// boundaries as in k_eval, and the partial sums, carries and record ranges
+// are the ones k_eval writes, so k_finish reads either alike.
+constexpr int kStreamR = 4;                       // records per lane
+constexpr int kStreamSlots = 6;                   // step, m, n, k, a, b
+static_assert(kWave * kStreamR == kWgRows, "a wave of the stream takes one workgroup tile");
+static_assert(kTileRows == 16 * kStreamR, "a 64-record tile is one 16-lane row");
+
+// orders a wave's LDS writes before its later reads (lanes read what other
+// lanes of the same wave wrote)
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// fields a family's counts read besides step and n
+constexpr bool uses_m(int fam) {
+  return fam != KS_GROUPED_GEMM && fam != KS_ATTN_PREFILL && fam != KS_ATTN_DECODE;
+}
+constexpr bool uses_k(int fam) { return fam != KS_RMSNORM && fam != KS_SILU_MUL && fam != KS_EMBED; }
+constexpr bool uses_a(int fam) {
+  return fam == KS_GROUPED_GEMM || fam == KS_ATTN_PREFILL || fam == KS_ATTN_DECODE;
+}
+constexpr bool uses_b(int fam) { return fam == KS_GROUPED_GEMM; }
+constexpr bool uses_field(int fam, int f) {
+  return f == 0 || f == 2 || (f == 1 && uses_m(fam)) || (f == 3 && uses_k(fam)) || (f == 4 && uses_a(fam)) ||
+         (f == 5 && uses_b(fam));
+}
+
+// a workgroup tile of the stream: family, first row, valid rows, first tile id
+struct STile {
+  int fam, nvalid, tile0;
+  int64_t row0;
+  bool hp, hn;   // a record of the family exists just before / after it
+};
+
+__device__ __forceinline__ STile stream_locate(const EvalParams &p, int wt, int fam0) {
+  STile t;
+  int fam = fam0;
+  while (wt >= p.wgt_off[fam + 1]) ++fam;
+  const int in_fam = wt - p.wgt_off[fam];
+  const int64_t lo = p.fam_off[fam], hi = p.fam_off[fam + 1];
+  t.fam = fam;
+  t.row0 = lo + (int64_t)in_fam * kWgRows;
+  const int64_t left = hi - t.row0;
+  t.nvalid = left < kWgRows ? (int)left : kWgRows;
+  t.tile0 = p.tile_off[fam] + in_fam * kWgWaves;
+  t.hp = in_fam > 0;
+  t.hn = left > kWgRows;
+  return t;
+}
+
+// Inclusive segmented scan within each 16-lane row (row_shr 1, 2, 4, 8):
+// v += g[i] * v[lane - 2^i], g[i] = 1 where that lane's key is this lane's
+// (keys sorted, so the lanes between share it too).  Lanes without a source
+// in the row read 0 (bound_ctrl) or are left out by the bank mask.
+__device__ __forceinline__ float row_scan(float v, const float (&g)[4]) {
+  asm volatile(
+      "s_nop 1\n"
+      "v_fmac_f32_dpp %0, %0, %1 row_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "s_nop 1\n"
+      "v_fmac_f32_dpp %0, %0, %2 row_shr:2 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "s_nop 1\n"
+      "v_fmac_f32_dpp %0, %0, %3 row_shr:4 row_mask:0xf bank_mask:0xe\n"
+      "s_nop 1\n"
+      "v_fmac_f32_dpp %0, %0, %4 row_shr:8 row_mask:0xf bank_mask:0xc\n"
+      : "+v"(v)
+      : "v"(g[0]), "v"(g[1]), "v"(g[2]), "v"(g[3]));
+  return v;
+}
+
+// What the spec loop needs of a lane's four records.  Runs never mix live
+// and other records (those carry key kNoKey), so the t of a record that is
+// not live never reaches a stored sum and needs no masking.
+struct SRec {
+  float Bf[kStreamR], frb[kStreamR], Btf[kStreamR], rcp_b[kStreamR], Ff[kStreamR];
+  uint64_t B[kStreamR];
+  uint32_t key[kStreamR];
+  float fj[kStreamR], ff[kStreamR];   // run continues from record j - 1; record j is in the lane's first run
+  bool ptail[kStreamR], to_carry[kStreamR];
+  float g[4], fc;                     // row-scan factors; the lane's first run continues the lane before
+  int tile;
+};
+
+// Spec loop.  Block counts below 2^23 (SMALL): the wave count in fp32 as in
+// roofline<true>, and F u / P as W (F / B) (N / P), the first factor per
+// record and the second per spec.  Otherwise the exact path of
+// roofline<false>.
+template <bool SMALL>
+__device__ __forceinline__ void stream_specs(const EvalParams &p, const SRec &r, int fam, bool any_tail) {
+  const size_t part_stride = (size_t)KS_NFAM * (size_t)p.n_steps;
+  for (int s = 0; s < p.n_specs; ++s) {
+    const SpecC sc = spec_at(p.spec_c, s);
+    const float np = sc.n_f * sc.rcp_p;
+    float acc[kStreamR];
+#pragma unroll
+    for (int j = 0; j < kStreamR; ++j) {
+      float t;
+      if constexpr (SMALL) {
+        const float W0 = ceilf(r.Bf[j] * sc.rcp_n);
+        const float W = (W0 - 1.0f) * sc.n_f >= r.Bf[j] ? W0 - 1.0f : W0;
+        t = fmaxf(fmaxf(W * (r.frb[j] * np), r.Btf[j] * sc.rcp_bw), sc.t0);
+      } else {
+        RowC rc;
+        rc.B = r.B[j];
+        rc.Ff = r.Ff[j];
+        rc.Btf = r.Btf[j];
+        rc.Bf = r.Bf[j];
+        rc.rcp_b = r.rcp_b[j];
+        t = fmaxf(roofline<false>(rc, sc).t_roof, sc.t0);
+      }
+      acc[j] = j == 0 ? t : fmaf(r.fj[j], acc[j - 1], t);
+    }
+    // the run ending at this lane's last record, over the row's lanes so far
+    const float x = row_scan(acc[kStreamR - 1], r.g);
+    // what the lanes before add to this lane's first run (0 at a row start)
+    const float cin = r.fc * __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+                                                         0, __builtin_bit_cast(int, x), 0x111, 0xf, 0xf, true));
+    if (any_tail) {
+#pragma unroll
+      for (int j = 0; j < kStreamR; ++j) {
+        if (r.ptail[j]) {
+          const double v = (double)fmaf(r.ff[j], cin, acc[j]);
+          double *d = r.to_carry[j] ? p.carry + (size_t)s * (size_t)p.n_tiles + r.tile
+                                    : p.partial + (size_t)s * part_stride + (size_t)fam * p.n_steps + r.key[j];
+          *d = v;
+        }
+      }
+    }
+  }
+}
+
+// One workgroup tile of family FAM.
+template <int FAM>
+__device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc, uint32_t (*ws)[kWgRows],
+                                            int lane) {
+  // coalesced loads (lane l: records 64 j + l), then the transpose through
+  // the wave's LDS slot (lane l: records 4 l + j)
+  {
+    uint32_t raw[kStreamSlots][kStreamR];
+    const uint32_t *src[kStreamSlots] = {p.step, p.m, p.n, p.k, p.a, p.b};
+#pragma unroll
+    for (int j = 0; j < kStreamR; ++j) {
+      const int i = kWave * j + lane;
+      const uint32_t off = (uint32_t)(i < tc.nvalid ? i : 0);
+#pragma unroll
+      for (int f = 0; f < kStreamSlots; ++f)
+        if (uses_field(FAM, f)) raw[f][j] = (src[f] + tc.row0)[off];
+    }
+#pragma unroll
+    for (int f = 0; f < kStreamSlots; ++f) {
+      if (uses_field(FAM, f)) {
+#pragma unroll
+        for (int j = 0; j < kStreamR; ++j) ws[f][kWave * j + lane] = raw[f][j];
+      }
+    }
+  }
+  // the steps just before and after the tile: lane 0 and lane 1 of one load
+  // (each address inside the family: the tile's first row where a
+  // neighbour does not exist)
+  const int pn_off = lane == 0 ? (tc.hp ? -1 : 0) : (tc.hn ? kWgRows : 0);
+  const uint32_t pn = (p.step + tc.row0)[pn_off];
+  wave_lds_sync();
+  uint32_t v[kStreamSlots][kStreamR];
+#pragma unroll
+  for (int f = 0; f < kStreamSlots; ++f) {
+    u32x4 q = {0, 0, 0, 0};
+    if (uses_field(FAM, f)) q = *reinterpret_cast<const u32x4 *>(&ws[f][kStreamR * lane]);
+#pragma unroll
+    for (int j = 0; j < kStreamR; ++j) v[f][j] = q[j];
+  }
+  const uint32_t prev = tc.hp ? __builtin_amdgcn_readlane(pn, 0) : kNoKey;
+  const uint32_t next = tc.hn ? __builtin_amdgcn_readlane(pn, 1) : kNoKey;
+
+  // per record: counts and the spec-independent roofline operands
+  SRec r;
+  uint32_t bad = 0;
+  bool live[kStreamR];
+  bool big = false;
+#pragma unroll
+  for (int j = 0; j < kStreamR; ++j) {
+    const bool valid = kStreamR * lane + j < tc.nvalid;
+    uint32_t b = 0;
+    if ((int64_t)v[0][j] >= p.n_steps) b |= kErrStep;
+    const CntF cf = record_counts_f(FAM, v[1][j], v[2][j], v[3][j], v[4][j], v[5][j], v[0][j], p, b);
+    if (valid) bad |= b;
+    live[j] = valid && !(b & kErrStep);
+    r.key[j] = live[j] ? v[0][j] : kNoKey;
+    r.B[j] = cf.B;
+    r.Ff[j] = cf.F;
+    r.Btf[j] = cf.Bt;
+    big |= cf.B >= kSmallB;
+  }
+  if (bad) atomicOr(p.err, bad);
+  const bool small = __ballot(big) == 0;   // wave-uniform
+#pragma unroll
+  for (int j = 0; j < kStreamR; ++j) {
+    r.Bf[j] = small ? (float)(uint32_t)r.B[j] : (float)r.B[j];
+    r.rcp_b[j] = rcpf(fmaxf(r.Bf[j], 1.0f));
+    r.frb[j] = r.Ff[j] * r.rcp_b[j];
+  }
+
+  // neighbours: the record before this lane's first (lane 0: the tile
+  // edge) and after its last (lane 63: the tile edge)
+  const uint32_t kp = (uint32_t)__builtin_amdgcn_update_dpp((int)prev, (int)r.key[kStreamR - 1], 0x138, 0xf, 0xf, false);
+  const uint32_t kn = (uint32_t)__builtin_amdgcn_update_dpp((int)next, (int)r.key[0], 0x130, 0xf, 0xf, false);
+  const int row_lane = lane & 15;
+  r.tile = tc.tile0 + (lane >> 4);
+  // the key of the row's first record and of the record before the row
+  // (row_newbcast:0 gives each row its lane 0)
+  const uint32_t rk0 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)r.key[0], 0x150, 0xf, 0xf, false);
+  const uint32_t rkp = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)kp, 0x150, 0xf, 0xf, false);
+  bool any = false;
+#pragma unroll
+  for (int j = 0; j < kStreamR; ++j) {
+    const uint32_t key = r.key[j];
+    const uint32_t before = j == 0 ? kp : r.key[j - 1];
+    const uint32_t after = j == kStreamR - 1 ? kn : r.key[j + 1];
+    r.fj[j] = j > 0 && key == before ? 1.0f : 0.0f;
+    r.ff[j] = key == r.key[0] ? 1.0f : 0.0f;
+    // the (family, step) record range, written where its global first and
+    // last records are
+    const uint32_t row = (uint32_t)(tc.row0 + kStreamR * lane + j);
+    if (live[j] && before != key) p.range[2 * ((size_t)FAM * p.n_steps + key)] = row;
+    if (live[j] && after != key) p.range[2 * ((size_t)FAM * p.n_steps + key) + 1] = row + 1;
+    // a run's last record within its 64-record tile
+    r.ptail[j] = live[j] && (after != key || (j == kStreamR - 1 && row_lane == 15));
+    r.to_carry[j] = key == rk0 && rkp == rk0;
+    any |= r.ptail[j];
+  }
+  const bool any_tail = __ballot(any) != 0;
+  r.fc = row_lane != 0 && kp == r.key[0] ? 1.0f : 0.0f;
+  // row-scan factors on the lanes' last keys
+  const uint32_t kl = r.key[kStreamR - 1];
+  r.g[0] = dpp_key<0x111, 0xf, 0xf>(kl) == kl ? 1.0f : 0.0f;
+  r.g[1] = dpp_key<0x112, 0xf, 0xf>(kl) == kl ? 1.0f : 0.0f;
+  r.g[2] = dpp_key<0x114, 0xf, 0xe>(kl) == kl ? 1.0f : 0.0f;
+  r.g[3] = dpp_key<0x118, 0xf, 0xc>(kl) == kl ? 1.0f : 0.0f;
+  if (small)
+    stream_specs<true>(p, r, FAM, any_tail);
+  else
+    stream_specs<false>(p, r, FAM, any_tail);
+}
+
+__global__ __launch_bounds__(kWgThreads) void k_stream(EvalParams p) {
+  __shared__ __attribute__((aligned(16))) uint32_t slot[kWgWaves][kStreamSlots][kWgRows];
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int n_wgt = p.wgt_off[KS_NFAM];
+  const int stride = (int)gridDim.x * kWgWaves;
+  uint32_t(*ws)[kWgRows] = slot[wave];
+  int fam = 0;
+  for (int wt = (int)blockIdx.x * kWgWaves + wave; wt < n_wgt; wt += stride) {
+    const STile tc = stream_locate(p, wt, fam);
+    fam = tc.fam;
+    switch (fam) {
+      case KS_GEMM: stream_tile<KS_GEMM>(p, tc, ws, lane); break;
+      case KS_LM_HEAD: stream_tile<KS_LM_HEAD>(p, tc, ws, lane); break;
+      case KS_GROUPED_GEMM: stream_tile<KS_GROUPED_GEMM>(p, tc, ws, lane); break;
+      case KS_ATTN_PREFILL: stream_tile<KS_ATTN_PREFILL>(p, tc, ws, lane); break;
+      case KS_ATTN_DECODE: stream_tile<KS_ATTN_DECODE>(p, tc, ws, lane); break;
+      case KS_RMSNORM: stream_tile<KS_RMSNORM>(p, tc, ws, lane); break;
+      case KS_ROPE: stream_tile<KS_ROPE>(p, tc, ws, lane); break;
+      case KS_SILU_MUL: stream_tile<KS_SILU_MUL>(p, tc, ws, lane); break;
+      case KS_KV_WRITE: stream_tile<KS_KV_WRITE>(p, tc, ws, lane); break;
+      default: stream_tile<KS_EMBED>(p, tc, ws, lane); break;
+    }
+  }
+}
+
 // ------------------------------------------------------------ eta source
 // Per pair, where eta came from when no grid routes any pair: 1 for the
 // families on the bounded head, 0 (the head of the mode) for the others.
@@ -1669,6 +1949,31 @@ static hipError_t launch_grid(const EvalParams &p, hipStream_t s) {
   return hipGetLastError();
 }
 
+// k_stream: the step sums of the eta = 1 stream without multiplicities or
+// per-pair outputs; grid-stride over workgroup tiles, one per wave
+static std::atomic<int> g_stream_resident[kMaxDevices];
+
+static hipError_t launch_stream(const EvalParams &p, hipStream_t s) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::atomic<int> *slot = dev < kMaxDevices ? &g_stream_resident[dev] : nullptr;
+  int cap = slot ? slot->load(std::memory_order_relaxed) : 0;
+  if (cap == 0) {
+    int per_cu = 0, n_cu = 0;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_stream, kWgThreads, 0);
+    if (e != hipSuccess) return e;
+    e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    cap = (per_cu < 1 ? 1 : per_cu) * (n_cu < 1 ? 1 : n_cu);
+    if (slot) slot->store(cap, std::memory_order_relaxed);
+  }
+  const int n_wgt = p.wgt_off[KS_NFAM];
+  const int need = (n_wgt + kWgWaves - 1) / kWgWaves;
+  hipLaunchKernelGGL(k_stream, dim3(need < cap ? need : cap), dim3(kWgThreads), 0, s, p);
+  return hipGetLastError();
+}
+
 // the eta = 1 stream has no Tier B instantiation (a grid selects the
 // head-less kind)
 template <int KIND>
@@ -1677,6 +1982,8 @@ static hipError_t launch_kind(const EvalParams &p, hipStream_t s) {
   const bool mult = p.mult && p.partial;
   if constexpr (KIND == kEtaOne) {
     if (p.grid_mask) return hipErrorInvalidValue;
+    const bool per_pair = p.o_flops || p.o_bytes || p.o_blocks || p.o_troof || p.o_eta || p.o_t;
+    if (!mult && !per_pair && p.partial && p.range) return launch_stream(p, s);
     return mult ? launch_grid<KIND, kVarMult>(p, s) : launch_grid<KIND, 0>(p, s);
   } else {
     if (p.grid_mask)

@@ -329,6 +329,51 @@ def test_eta_one_without_count_outputs():
     _eta1_case(gen.config3(0, 40), counts=False)
 
 
+def _run_workload(seed, n_steps, max_run, n_specs):
+    """Per family, each step's records in one run of U{1..max_run} records
+    (some families skip steps), so that runs start and end at every one of
+    a lane's four records, at 16-lane row (64-record tile) edges and at
+    256-record workgroup-tile edges; family sizes are not multiples of 4."""
+    rng = np.random.default_rng(seed)
+    rows, reqs = [], []
+    for j in range(n_steps):
+        reqs.append([(int(rng.integers(1, 40)), int(rng.integers(0, 5000)))
+                     for _ in range(int(rng.integers(1, 4)))])
+    shape = {gen.GEMM: lambda: (int(rng.integers(1, 3000)), int(rng.integers(64, 9000)), int(rng.integers(64, 9000)), 0, 0),
+             gen.ATTN_DECODE: lambda: (0, 8 * int(rng.integers(1, 9)), 128, int(rng.integers(1, 9)), 0),
+             gen.RMSNORM: lambda: (int(rng.integers(1, 3000)), 4096, 0, 0, 0),
+             gen.SILU_MUL: lambda: (int(rng.integers(1, 3000)), int(rng.integers(1, 30000)), 0, 0, 0),
+             gen.EMBED: lambda: (int(rng.integers(1, 3000)), 8192, 0, 0, 0)}
+    for f, mk in shape.items():
+        for j in range(n_steps):
+            if rng.uniform() < 0.1:
+                continue
+            run = int(rng.integers(1, max_run + 1)) if rng.uniform() < 0.7 else int(rng.integers(1, 6))
+            rows += [(f, j) + mk() for _ in range(run)]
+    sp = gen.specs_grid(n_specs, 7) if n_specs > 1 else spec(P=1e15, BW=4e12, n_cu=132, t0=2e-6)
+    return _wl(make_desc(rows, reqs), n_steps, specs=sp)
+
+
+@pytest.mark.parametrize("seed,n_steps,max_run,n_specs", [(1, 40, 9, 1), (2, 60, 70, 3), (3, 30, 300, 5),
+                                                           (4, 400, 200, 2)])
+def test_eta_one_step_sums_runs_at_every_offset(seed, n_steps, max_run, n_specs):
+    """The eta = 1 step sums without per-pair outputs (each lane sums four
+    consecutive records, a row scan joins the lanes) against the oracle, and
+    against the same call with per-pair outputs (one record per lane)."""
+    wl = _run_workload(seed, n_steps, max_run, n_specs)
+    ref = o.eval_kernels(wl.desc, wl.specs, eta_one=True)
+    rs = o.eval_steps(wl.desc, wl.steps, wl.specs, wl.host, eta_one=True, kern=ref)
+    steps_only = g.eval_steps(wl, eta_one=True, per_pair=False)
+    _check_steps(wl, steps_only, rs, bf16=False, n_specs=wl.n_specs)
+    per_pair = g.eval_steps(wl, eta_one=True, counts=False)
+    _check_kernels(wl, per_pair, ref, bf16=False, eta_one=True)
+    for key in ("t_body", "t_gpu", "t_step"):
+        assert g.rel_err(steps_only[key], per_pair[key]).max() <= 2 * REL
+    again = g.eval_steps(wl, eta_one=True, per_pair=False)
+    for key in ("t_body", "t_gpu", "t_step"):
+        np.testing.assert_array_equal(again[key], steps_only[key])
+
+
 def _multi_spec(n_cus):
     n = len(n_cus)
     rng = np.random.default_rng(11)
