@@ -1585,12 +1585,18 @@ __device__ __forceinline__ float row_scan(float v, const float (&g)[4]) {
   return v;
 }
 
-// What the spec loop needs of a lane's four records.  Runs never mix live
-// and other records (those carry key kNoKey), so the t of a record that is
-// not live never reaches a stored sum and needs no masking.
+// Block counts below 2^22: the wave count W = ceil(B / N) in fp32 as the
+// ceiling of (B - 1/2) fl(1/N).  B - 1/2 is exact, and the two roundings
+// move the quotient by at most (B/N) (2^-23 + 2^-48) < 1/(2N), while
+// (B - 1/2)/N lies at least 1/(2N) away from every integer (B and N are
+// integers), so the ceiling is exact.
+constexpr uint32_t kStreamSmallB = 1u << 22;
+
+// What the spec loop needs of a lane's four records besides their roofline
+// operands.  Runs never mix live and other records (those carry key
+// kNoKey), so the t of a record that is not live never reaches a stored
+// sum and needs no masking.
 struct SRec {
-  float Bf[kStreamR], frb[kStreamR], Btf[kStreamR], rcp_b[kStreamR], Ff[kStreamR];
-  uint64_t B[kStreamR];
   uint32_t key[kStreamR];
   float fj[kStreamR], ff[kStreamR];   // run continues from record j - 1; record j is in the lane's first run
   bool ptail[kStreamR], to_carry[kStreamR];
@@ -1598,12 +1604,16 @@ struct SRec {
   int tile;
 };
 
-// Spec loop.  Block counts below 2^23 (SMALL): the wave count in fp32 as in
-// roofline<true>, and F u / P as W (F / B) (N / P), the first factor per
-// record and the second per spec.  Otherwise the exact path of
-// roofline<false>.
-template <bool SMALL>
-__device__ __forceinline__ void stream_specs(const EvalParams &p, const SRec &r, int fam, bool any_tail) {
+// Spec loop.  W = ceil(B / N) as the ceiling of (B - 1/2) / N: in fp32 for
+// block counts below 2^22 (as above), else in fp64, exact by the same
+// argument below 2^51 (the exact path of k_eval assumes B < 2^52); then
+// F u / P = W (F / B) (N / P), the first factor per record and the second
+// per spec.  BH: B - 1/2 per record, as float or double; frb, btf: F / B
+// and Bt per record.  part: the spec-0 partials of the tile's family.
+template <class BH>
+__device__ __forceinline__ void stream_specs(const EvalParams &p, const SRec &r, const BH (&bh)[kStreamR],
+                                             const float (&frb)[kStreamR], const float (&btf)[kStreamR],
+                                             double *part, bool any_tail) {
   const size_t part_stride = (size_t)KS_NFAM * (size_t)p.n_steps;
   for (int s = 0; s < p.n_specs; ++s) {
     const SpecC sc = spec_at(p.spec_c, s);
@@ -1611,20 +1621,12 @@ __device__ __forceinline__ void stream_specs(const EvalParams &p, const SRec &r,
     float acc[kStreamR];
 #pragma unroll
     for (int j = 0; j < kStreamR; ++j) {
-      float t;
-      if constexpr (SMALL) {
-        const float W0 = ceilf(r.Bf[j] * sc.rcp_n);
-        const float W = (W0 - 1.0f) * sc.n_f >= r.Bf[j] ? W0 - 1.0f : W0;
-        t = fmaxf(fmaxf(W * (r.frb[j] * np), r.Btf[j] * sc.rcp_bw), sc.t0);
-      } else {
-        RowC rc;
-        rc.B = r.B[j];
-        rc.Ff = r.Ff[j];
-        rc.Btf = r.Btf[j];
-        rc.Bf = r.Bf[j];
-        rc.rcp_b = r.rcp_b[j];
-        t = fmaxf(roofline<false>(rc, sc).t_roof, sc.t0);
-      }
+      float W;
+      if constexpr (sizeof(BH) == sizeof(float))
+        W = ceilf(bh[j] * sc.rcp_n);
+      else
+        W = (float)ceil(bh[j] * sc.rcp_nd);
+      const float t = fmaxf(fmaxf(W * (frb[j] * np), btf[j] * sc.rcp_bw), sc.t0);
       acc[j] = j == 0 ? t : fmaf(r.fj[j], acc[j - 1], t);
     }
     // the run ending at this lane's last record, over the row's lanes so far
@@ -1638,7 +1640,7 @@ __device__ __forceinline__ void stream_specs(const EvalParams &p, const SRec &r,
         if (r.ptail[j]) {
           const double v = (double)fmaf(r.ff[j], cin, acc[j]);
           double *d = r.to_carry[j] ? p.carry + (size_t)s * (size_t)p.n_tiles + r.tile
-                                    : p.partial + (size_t)s * part_stride + (size_t)fam * p.n_steps + r.key[j];
+                                    : part + (size_t)s * part_stride + r.key[j];
           *d = v;
         }
       }
@@ -1646,10 +1648,17 @@ __device__ __forceinline__ void stream_specs(const EvalParams &p, const SRec &r,
   }
 }
 
-// One workgroup tile of family FAM.
+// One workgroup tile of family FAM; rng and part: the family's range table
+// and spec-0 partials (formed before the family is dispatched on, so that
+// each family's code does not hold its own copy of them).
+// One workgroup tile of family FAM; rng and part: the family's range table
+// and spec-0 partials (formed before the family is dispatched on, so that
+// each family's code does not hold its own copy of them).
 template <int FAM>
 __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc, uint32_t (*ws)[kWgRows],
-                                            int lane) {
+                                            int lane, uint32_t *rng, double *part) {
+  uint64_t B[kStreamR];
+  float Ff[kStreamR], Btf[kStreamR];
   // coalesced loads (lane l: records 64 j + l), then the transpose through
   // the wave's LDS slot (lane l: records 4 l + j)
   {
@@ -1693,28 +1702,25 @@ __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc
   uint32_t bad = 0;
   bool live[kStreamR];
   bool big = false;
+  // a step at or past n_steps (none can be when n_steps >= 2^32)
+  const bool lim = p.n_steps <= (int64_t)UINT32_MAX;
+  const uint32_t n_steps32 = (uint32_t)p.n_steps;
 #pragma unroll
   for (int j = 0; j < kStreamR; ++j) {
     const bool valid = kStreamR * lane + j < tc.nvalid;
     uint32_t b = 0;
-    if ((int64_t)v[0][j] >= p.n_steps) b |= kErrStep;
+    if (lim && v[0][j] >= n_steps32) b |= kErrStep;
     const CntF cf = record_counts_f(FAM, v[1][j], v[2][j], v[3][j], v[4][j], v[5][j], v[0][j], p, b);
     if (valid) bad |= b;
     live[j] = valid && !(b & kErrStep);
     r.key[j] = live[j] ? v[0][j] : kNoKey;
-    r.B[j] = cf.B;
-    r.Ff[j] = cf.F;
-    r.Btf[j] = cf.Bt;
-    big |= cf.B >= kSmallB;
+    B[j] = cf.B;
+    Ff[j] = cf.F;
+    Btf[j] = cf.Bt;
+    big |= cf.B >= kStreamSmallB;
   }
   if (bad) atomicOr(p.err, bad);
   const bool small = __ballot(big) == 0;   // wave-uniform
-#pragma unroll
-  for (int j = 0; j < kStreamR; ++j) {
-    r.Bf[j] = small ? (float)(uint32_t)r.B[j] : (float)r.B[j];
-    r.rcp_b[j] = rcpf(fmaxf(r.Bf[j], 1.0f));
-    r.frb[j] = r.Ff[j] * r.rcp_b[j];
-  }
 
   // neighbours: the record before this lane's first (lane 0: the tile
   // edge) and after its last (lane 63: the tile edge)
@@ -1737,8 +1743,8 @@ __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc
     // the (family, step) record range, written where its global first and
     // last records are
     const uint32_t row = (uint32_t)(tc.row0 + kStreamR * lane + j);
-    if (live[j] && before != key) p.range[2 * ((size_t)FAM * p.n_steps + key)] = row;
-    if (live[j] && after != key) p.range[2 * ((size_t)FAM * p.n_steps + key) + 1] = row + 1;
+    if (live[j] && before != key) rng[2 * (size_t)key] = row;
+    if (live[j] && after != key) rng[2 * (size_t)key + 1] = row + 1;
     // a run's last record within its 64-record tile
     r.ptail[j] = live[j] && (after != key || (j == kStreamR - 1 && row_lane == 15));
     r.to_carry[j] = key == rk0 && rkp == rk0;
@@ -1752,13 +1758,30 @@ __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc
   r.g[1] = dpp_key<0x112, 0xf, 0xf>(kl) == kl ? 1.0f : 0.0f;
   r.g[2] = dpp_key<0x114, 0xf, 0xe>(kl) == kl ? 1.0f : 0.0f;
   r.g[3] = dpp_key<0x118, 0xf, 0xc>(kl) == kl ? 1.0f : 0.0f;
-  if (small)
-    stream_specs<true>(p, r, FAM, any_tail);
-  else
-    stream_specs<false>(p, r, FAM, any_tail);
+  float frb[kStreamR];
+  if (small) {
+    float bh[kStreamR];
+#pragma unroll
+    for (int j = 0; j < kStreamR; ++j) {
+      const float Bf = (float)(uint32_t)B[j];
+      bh[j] = Bf - 0.5f;
+      frb[j] = Ff[j] * rcpf(fmaxf(Bf, 1.0f));
+    }
+    stream_specs(p, r, bh, frb, Btf, part, any_tail);
+  } else {
+    double bh[kStreamR];
+#pragma unroll
+    for (int j = 0; j < kStreamR; ++j) {
+      bh[j] = (double)B[j] - 0.5;
+      frb[j] = Ff[j] * rcpf(fmaxf((float)B[j], 1.0f));
+    }
+    stream_specs(p, r, bh, frb, Btf, part, any_tail);
+  }
 }
 
-__global__ __launch_bounds__(kWgThreads) void k_stream(EvalParams p) {
+// 80 registers (six waves per SIMD) measured faster than the 83 the
+// compiler picks by itself
+__global__ __launch_bounds__(kWgThreads) __attribute__((amdgpu_waves_per_eu(6))) void k_stream(EvalParams p) {
   __shared__ __attribute__((aligned(16))) uint32_t slot[kWgWaves][kStreamSlots][kWgRows];
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int n_wgt = p.wgt_off[KS_NFAM];
@@ -1768,17 +1791,19 @@ __global__ __launch_bounds__(kWgThreads) void k_stream(EvalParams p) {
   for (int wt = (int)blockIdx.x * kWgWaves + wave; wt < n_wgt; wt += stride) {
     const STile tc = stream_locate(p, wt, fam);
     fam = tc.fam;
+    uint32_t *rng = p.range + 2 * (size_t)fam * (size_t)p.n_steps;
+    double *part = p.partial + (size_t)fam * (size_t)p.n_steps;
     switch (fam) {
-      case KS_GEMM: stream_tile<KS_GEMM>(p, tc, ws, lane); break;
-      case KS_LM_HEAD: stream_tile<KS_LM_HEAD>(p, tc, ws, lane); break;
-      case KS_GROUPED_GEMM: stream_tile<KS_GROUPED_GEMM>(p, tc, ws, lane); break;
-      case KS_ATTN_PREFILL: stream_tile<KS_ATTN_PREFILL>(p, tc, ws, lane); break;
-      case KS_ATTN_DECODE: stream_tile<KS_ATTN_DECODE>(p, tc, ws, lane); break;
-      case KS_RMSNORM: stream_tile<KS_RMSNORM>(p, tc, ws, lane); break;
-      case KS_ROPE: stream_tile<KS_ROPE>(p, tc, ws, lane); break;
-      case KS_SILU_MUL: stream_tile<KS_SILU_MUL>(p, tc, ws, lane); break;
-      case KS_KV_WRITE: stream_tile<KS_KV_WRITE>(p, tc, ws, lane); break;
-      default: stream_tile<KS_EMBED>(p, tc, ws, lane); break;
+      case KS_GEMM: stream_tile<KS_GEMM>(p, tc, ws, lane, rng, part); break;
+      case KS_LM_HEAD: stream_tile<KS_LM_HEAD>(p, tc, ws, lane, rng, part); break;
+      case KS_GROUPED_GEMM: stream_tile<KS_GROUPED_GEMM>(p, tc, ws, lane, rng, part); break;
+      case KS_ATTN_PREFILL: stream_tile<KS_ATTN_PREFILL>(p, tc, ws, lane, rng, part); break;
+      case KS_ATTN_DECODE: stream_tile<KS_ATTN_DECODE>(p, tc, ws, lane, rng, part); break;
+      case KS_RMSNORM: stream_tile<KS_RMSNORM>(p, tc, ws, lane, rng, part); break;
+      case KS_ROPE: stream_tile<KS_ROPE>(p, tc, ws, lane, rng, part); break;
+      case KS_SILU_MUL: stream_tile<KS_SILU_MUL>(p, tc, ws, lane, rng, part); break;
+      case KS_KV_WRITE: stream_tile<KS_KV_WRITE>(p, tc, ws, lane, rng, part); break;
+      default: stream_tile<KS_EMBED>(p, tc, ws, lane, rng, part); break;
     }
   }
 }
