@@ -44,6 +44,34 @@ def _eval_status(wl):
     return st, abi.ks_last_error(), {k: v.cpu().numpy() for k, v in so_t.items()}
 
 
+def _eval_status_eta_one(wl):
+    """eta = 1 step sums without per-pair outputs (the streaming kernel)."""
+    import torch
+    di = abi.DeviceInputs(wl)
+    heads = di.make_heads(wl.heads.precision, wl.heads.in_dim, wl.heads.hidden, abi.KS_ETA_ONE)
+    so_t, so = abi.step_outputs(wl.desc.n_steps, di.n_specs)
+    abi.ks_eval_steps(di.desc, di.steps, di.specs_ptr, di.n_specs, heads, di.host, so, None,
+                      di.ws_ptr, di.ws_bytes, abi.current_stream())
+    st = abi.ks_device_status(di.ws_ptr, di.ws_bytes, abi.current_stream(), check=False)
+    torch.cuda.synchronize()
+    return st, abi.ks_last_error(), {k: v.cpu().numpy() for k, v in so_t.items()}
+
+
+def test_eta_one_stream_flags_and_skips_bad_records():
+    """A record whose step is out of range, and a grouped GEMM whose expert
+    offsets run past the table, are flagged by the eta = 1 stream; the other
+    records' step sums are those of the input without the bad records."""
+    good = GOOD_ROWS[:2] + [(gen.ATTN_DECODE, 0, 0, 8, 128, 2, 0)]
+    st, msg, ref = _eval_status_eta_one(_wl(good, GOOD_REQS))
+    assert st == abi.KS_OK, msg
+    st, msg, out = _eval_status_eta_one(_wl(good + [(gen.GEMM, 7, 4, 64, 64, 0, 0)], GOOD_REQS))
+    assert st == abi.KS_EINVAL and "step" in msg
+    np.testing.assert_array_equal(out["t_body"], ref["t_body"])
+    st, msg, _ = _eval_status_eta_one(_wl([(gen.GROUPED_GEMM, 0, 0, 64, 64, 4, 3)], [[(1, 1)]],
+                                          experts=[1, 2, 3, 4]))
+    assert st == abi.KS_EINVAL and "expert" in msg
+
+
 def test_good_input_validates():
     st, msg = _validate(_wl(GOOD_ROWS, GOOD_REQS, experts=[3, 0]))
     assert st == abi.KS_OK, msg
