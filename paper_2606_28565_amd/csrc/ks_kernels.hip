@@ -10,6 +10,9 @@
 //                on MFMA (Sec. 5.3), t = max(t_roof eta, t0) (Eq. 2), a
 //                wavefront segmented sum of t by step, and each (family,
 //                step) record range
+//   k_stream     instead of k_eval for the eta = 1 step sums without
+//                per-pair outputs: the same per 256 records and wave, four
+//                consecutive records per lane
 //   k_finish     per (spec, step): body sum, all-reduce (Eq. 3), assembly (Eq. 4)
 #include <hip/hip_runtime.h>
 
