@@ -512,8 +512,20 @@ def test_max_size_batch_sampled():
         torch.cuda.synchronize()
         abi.ks_device_status(di.ws_ptr, di.ws_bytes, abi.current_stream())
         gpu = {key: ko_t[key][:, rows_t].cpu().numpy() for key in ("t_roof", "eta", "t_kernel")}
-        body = so_t["t_body"].cpu().numpy()[:, steps]
-        del di, ko_t, so_t
+        body_all = so_t["t_body"].cpu().numpy()
+        body = body_all[:, steps]
+        del ko_t
+        stream = None
+        if eta_one:
+            # the same call without per-pair outputs: the eta = 1 streaming
+            # kernel, in the launch configuration the benchmark times
+            abi.ks_eval_steps(di.desc, di.steps, di.specs_ptr, di.n_specs, heads, di.host, so, None,
+                              di.ws_ptr, di.ws_bytes, abi.current_stream())
+            torch.cuda.synchronize()
+            abi.ks_device_status(di.ws_ptr, di.ws_bytes, abi.current_stream())
+            stream = so_t["t_body"].cpu().numpy()
+            assert g.rel_err(stream, body_all).max() <= 2 * REL
+        del di, so_t
         torch.cuda.empty_cache()
         ref = o.eval_kernels(_sub_desc(d, rows), wl.specs, None if eta_one else wl.heads, eta_one=eta_one)
         assert g.rel_err(gpu["t_roof"], ref["t_roof"]).max() <= REL
@@ -527,6 +539,8 @@ def test_max_size_batch_sampled():
         for s in range(wl.n_specs):
             ref_body = np.bincount(d.step[rows], weights=t_ge[s], minlength=d.n_steps)[steps]
             assert g.rel_err(body[s], ref_body).max() <= REL
+            if stream is not None:
+                assert g.rel_err(stream[s, steps], ref_body).max() <= REL
 
 
 # -------------------------------------------------- bounded analytical head --
