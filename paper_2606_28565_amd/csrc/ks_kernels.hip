@@ -1508,7 +1508,7 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
 
 // ------------------------------------------------------------ eta = 1 stream
 // The pure-roofline step sums (eta = 1, Eq. 2 and the segmented sum of
-// Sec. 5.6) when no per-pair output is asked for.  A wave takes a workgroup
+// Sec. 5.7) when no per-pair output is asked for.  A wave takes a workgroup
 // tile on its own (256 consecutive records of one family: four 64-record
 // tiles) and each lane four consecutive records of it, so that each 16-lane
 // DPP row holds exactly one 64-record tile.  The fields arrive by coalesced
