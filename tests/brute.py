@@ -131,3 +131,92 @@ def bf16_scalar(v):
     else:
         r = lo if int(round(lo / ulp)) % 2 == 0 else hi
     return math.copysign(r, v)
+
+
+# ---------------------------------------------------------------------------
+# elementwise and memory kernels: each kernel written out as the loop it runs
+# over its elements, counting the arithmetic operations of every element's
+# expression and collecting the distinct elements it reads and writes, and
+# the thread blocks its grid mapping touches.  Returns (F, Bt, B).
+
+def rmsnorm_work(T, D, dt):
+    """y[t, i] = x[t, i] * rsqrt(mean_i x[t, i]^2) * w[i], one block per token
+    row: per element a square and an accumulate (the mean), the scale by the
+    row's reciprocal root and the weight multiply."""
+    ops = 0
+    x_rd, w_rd, y_wr, blocks = set(), set(), set(), set()
+    for t in range(T):
+        for i in range(D):                       # pass 1: sum of squares
+            ops += 2                             # x * x, acc += .
+            x_rd.add((t, i))
+        for i in range(D):                       # pass 2: normalise, weight
+            ops += 2                             # * r, * w[i]
+            x_rd.add((t, i))
+            w_rd.add(i)
+            y_wr.add((t, i))
+        blocks.add(t)
+    return ops, dt * (len(x_rd) + len(w_rd) + len(y_wr)), len(blocks)
+
+
+def rope_work(T, heads, d, dt):
+    """x'[t, h, c] = x[t, h, c] cos[t, c] + rot(x)[t, h, c] sin[t, c] in place
+    over the rotated heads, one block per token: per element two multiplies
+    and one add; the position's cos/sin table holds d values (cos for one half
+    of the rotation pairs' slots, sin for the other)."""
+    ops = 0
+    x_rd, x_wr, tab, blocks = set(), set(), set(), set()
+    for t in range(T):
+        for h in range(heads):
+            for c in range(d):
+                ops += 3
+                x_rd.add((t, h, c))
+                x_wr.add((t, h, c))
+                tab.add((t, c))
+        blocks.add(t)
+    return ops, dt * (len(x_rd) + len(x_wr) + len(tab)), len(blocks)
+
+
+def silu_mul_work(T, I, dt, block=1024):
+    """out[t, i] = g / (1 + exp(-g)) * u with g = gate[t, i], u = up[t, i]:
+    negate, exponentiate, add one, divide, multiply by u (five operations);
+    flat blocks of `block` elements."""
+    ops = 0
+    g_rd, u_rd, o_wr, blocks = set(), set(), set(), set()
+    for t in range(T):
+        for i in range(I):
+            ops += 5
+            g_rd.add((t, i))
+            u_rd.add((t, i))
+            o_wr.add((t, i))
+            blocks.add((t * I + i) // block)
+    return ops, dt * (len(g_rd) + len(u_rd) + len(o_wr)), len(blocks)
+
+
+def kv_write_work(T, Hkv, d, dt):
+    """cache_k[slot(t), h, c] = k[t, h, c] and the same for v: a copy, no
+    arithmetic; one block per token."""
+    k_rd, v_rd, ck_wr, cv_wr, blocks = set(), set(), set(), set(), set()
+    for t in range(T):
+        for h in range(Hkv):
+            for c in range(d):
+                k_rd.add((t, h, c))
+                v_rd.add((t, h, c))
+                ck_wr.add((t, h, c))
+                cv_wr.add((t, h, c))
+        blocks.add(t)
+    return 0, dt * (len(k_rd) + len(v_rd) + len(ck_wr) + len(cv_wr)), len(blocks)
+
+
+def embed_work(T, D, dt, id_bytes=4):
+    """out[t, i] = table[id[t], i]: read the token's id (a 4-byte integer),
+    gather its table row and write the output row; no arithmetic; one block
+    per token.  Token ids are taken distinct (the gathered rows do not
+    repeat: the bytes a kernel moves, not a cache's hits)."""
+    ids, tab, out, blocks = set(), set(), set(), set()
+    for t in range(T):
+        ids.add(t)
+        for i in range(D):
+            tab.add((t, i))                      # row id[t] = t (distinct ids)
+            out.add((t, i))
+        blocks.add(t)
+    return 0, id_bytes * len(ids) + dt * (len(tab) + len(out)), len(blocks)

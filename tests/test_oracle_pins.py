@@ -117,28 +117,63 @@ def test_grouped_gemm_counts_brute():
     assert int(c["M"][0]) == sum(experts)
 
 
-def _elementwise_brute(fam, m, n, k, dt=2):
-    """Enumerate the elements each elementwise kernel reads/writes."""
-    if fam == gen.RMSNORM:     # read x, write y, read weight; square, sum, scale, weight
-        return 4 * m * n, dt * (m * n + m * n + n), m
-    if fam == gen.ROPE:        # rotate heads*d per token, cos/sin table d per token
-        return 3 * m * n * k, dt * (2 * m * n * k + m * k), m
-    if fam == gen.SILU_MUL:    # read gate and up, write out
-        return 5 * m * n, dt * (m * n + m * n + m * n), math.ceil(m * n / 1024)
-    if fam == gen.KV_WRITE:    # read k, v; write k, v into the cache
-        return 0, dt * 4 * m * n * k, m
-    if fam == gen.EMBED:       # read token id (4 B), gather row, write row
-        return 0, dt * m * n + dt * m * n + 4 * m, m
-    raise ValueError(fam)
+_ELEMENTWISE_BRUTE = {
+    gen.RMSNORM: lambda m, n, k: brute.rmsnorm_work(m, n, 2),
+    gen.ROPE: lambda m, n, k: brute.rope_work(m, n, k, 2),
+    gen.SILU_MUL: lambda m, n, k: brute.silu_mul_work(m, n, 2),
+    gen.KV_WRITE: lambda m, n, k: brute.kv_write_work(m, n, k, 2),
+    gen.EMBED: lambda m, n, k: brute.embed_work(m, n, 2),
+}
 
 
 @pytest.mark.parametrize("fam", [gen.RMSNORM, gen.ROPE, gen.SILU_MUL, gen.KV_WRITE, gen.EMBED])
-@pytest.mark.parametrize("m,n,k", [(1, 1, 1), (7, 3, 2), (1000, 3, 5)])
-def test_elementwise_counts(fam, m, n, k):
+@pytest.mark.parametrize("m,n,k", [(1, 1, 1), (7, 3, 2), (300, 5, 3), (37, 29, 4)])
+def test_elementwise_counts_brute(fam, m, n, k):
+    """F, Bt and B of the norm, rotary, activation, KV-write and embedding
+    records against their kernels enumerated element by element (the
+    operations of each element's expression, the distinct elements read and
+    written, the blocks the grid mapping touches).  (300, 5) and (37, 29)
+    span several 1024-element SiLU blocks with a ragged last one."""
     d = make_desc([(fam, 0, m, n, k, 0, 0)], [[(1, 0)]])
     c = o.kernel_counts(d)
-    F, Bt, B = _elementwise_brute(fam, m, n, k)
+    F, Bt, B = _ELEMENTWISE_BRUTE[fam](m, n, k)
     assert (int(c["F"][0]), int(c["Bt"][0]), int(c["B"][0])) == (F, Bt, B)
+
+
+def test_unused_k_is_ignored_by_the_features():
+    """Norm, activation and embedding records carry no K: whatever their k
+    field holds, feature x12 (the K shape feature) is 0 and their latency is
+    the same as with k = 0; the families that have a K (GEMM, LM head,
+    grouped GEMM, attention, RoPE, KV write) take log2(1 + k) / 24 from it
+    (Sec. 5.3: shape features per family)."""
+    k = 77
+    rows = [(gen.GEMM, 0, 5, 9, k, 0, 0), (gen.LM_HEAD, 0, 2, 9, k, 0, 0),
+            (gen.GROUPED_GEMM, 0, 0, 9, k, 2, 0), (gen.ATTN_DECODE, 0, 0, 4, k, 2, 0),
+            (gen.RMSNORM, 0, 5, 64, k, 0, 0), (gen.ROPE, 0, 5, 6, k, 0, 0),
+            (gen.SILU_MUL, 0, 5, 64, k, 0, 0), (gen.KV_WRITE, 0, 5, 2, k, 0, 0),
+            (gen.EMBED, 0, 5, 64, k, 0, 0)]
+    d = make_desc(rows, [[(1, 30), (1, 4)]], expert_rows=[3, 2])
+    heads = gen.make_heads(16, 8, "f32")
+    sp = spec()
+    r = o.eval_kernels(d, sp, heads, keep_features=True)
+    fam = d.family()
+    unused = np.isin(fam, [gen.RMSNORM, gen.SILU_MUL, gen.EMBED])
+    assert unused.sum() == 3 and (~unused).sum() == 6
+    x12 = r["x"][0, :, 12]
+    assert (x12[unused] == 0.0).all()
+    np.testing.assert_allclose(x12[~unused], math.log2(1 + k) / 24, rtol=1e-15)
+    # the same records with k = 0 where it is unused: identical predictions
+    rows0 = [rw if rw[0] not in (gen.RMSNORM, gen.SILU_MUL, gen.EMBED) else rw[:4] + (0,) + rw[5:]
+             for rw in rows]
+    r0 = o.eval_kernels(make_desc(rows0, [[(1, 30), (1, 4)]], expert_rows=[3, 2]), sp, heads)
+    np.testing.assert_array_equal(r["z"], r0["z"])
+    np.testing.assert_array_equal(r["t"], r0["t"])
+    # and a K that the family has does change its prediction
+    rows1 = [rw if rw[0] != gen.ROPE else rw[:4] + (3,) + rw[5:] for rw in rows]
+    r1 = o.eval_kernels(make_desc(rows1, [[(1, 30), (1, 4)]], expert_rows=[3, 2]), sp, heads)
+    rope = fam == gen.ROPE
+    assert (r1["z"][:, rope] != r["z"][:, rope]).all()
+    np.testing.assert_array_equal(r1["z"][:, ~rope], r["z"][:, ~rope])
 
 
 # ---------------------------------------------------------------- roofline -
