@@ -433,52 +433,7 @@ def test_n_cu_above_limit_flagged():
 
 
 # ------------------------------------------------------------ maximum size --
-def _max_batch(n_steps=88_640, seed=5):
-    """A 64M-record batch of the 70B shape (80 layers x 9 kernels + 2 per
-    step = 722 records per step, as one C5 batch), built vectorized: decode
-    steps of U{1..64} requests with Pareto-like histories up to 131072.
-    Same record count, families and shapes as the benchmark's C5 batch."""
-    rng = np.random.default_rng(seed)
-    S, L, D, F, V = n_steps, 80, 8192, 28672, 32000
-    nreq = rng.integers(1, 65, S)
-    req_off = np.zeros(S + 1, np.int64)
-    req_off[1:] = np.cumsum(nreq)
-    req_h = np.minimum(131072, (512 * rng.uniform(size=int(req_off[-1])) ** (-1 / 1.2))).astype(np.uint32)
-    T = nreq.astype(np.uint32)                      # one query token per request
-    st = np.arange(S, dtype=np.uint32)
-    fams = []
-
-    def fam(f, per_step, m_of_step, n, k=None, a=None):
-        cnt = len(n)
-        k = [0] * cnt if k is None else k
-        a = [0] * cnt if a is None else a
-        fams.append((f, np.repeat(st, cnt), np.repeat(m_of_step, cnt),
-                     np.tile(np.asarray(n, np.uint32), S), np.tile(np.asarray(k, np.uint32), S),
-                     np.tile(np.asarray(a, np.uint32), S)))
-        assert per_step == cnt
-    gemm_n = [(64 + 16) * 128, D, 2 * F, D] * L
-    gemm_k = [D, D, D, F] * L
-    fam(gen.GEMM, 4 * L, T, gemm_n, gemm_k)
-    fam(gen.LM_HEAD, 1, nreq.astype(np.uint32), [V], [D])
-    fam(gen.ATTN_DECODE, L, np.zeros(S, np.uint32), [64] * L, [128] * L, [8] * L)
-    fam(gen.RMSNORM, 2 * L, T, [D] * (2 * L))
-    fam(gen.ROPE, L, T, [72] * L, [128] * L)
-    fam(gen.SILU_MUL, L, T, [F] * L)
-    fam(gen.EMBED, 1, T, [D])
-    fam_off = np.zeros(gen.NFAM + 1, np.int64)
-    cols = [[] for _ in range(5)]
-    for f in range(gen.NFAM):
-        for (ff, *c) in fams:
-            if ff == f:
-                for dst, src in zip(cols, c):
-                    dst.append(src)
-                fam_off[f + 1] += len(c[0])
-    fam_off = np.cumsum(fam_off)
-    step, m, n, k, a = (np.concatenate(c) for c in cols)
-    desc = gen.Desc(fam_off, step, m, n, k, a, np.zeros_like(a), req_off.astype(np.uint32),
-                    np.ones(int(req_off[-1]), np.uint32), req_h, np.zeros(0, np.uint32))
-    return gen.Workload("max", desc, steprec(S, layers=L, hidden=D, n_launch=0), gen.specs_datasheet(),
-                        gen.make_heads(32, 256, "bf16"), gen.HostConsts())
+C5_BATCH_STEPS = 88_640      # steps 0 .. 88,640 of the 70B trace: 63,998,080 records
 
 
 def _sub_desc(d, rows):
@@ -492,17 +447,30 @@ def _sub_desc(d, rows):
 
 
 def test_max_size_batch_sampled():
-    """One 64M-record batch (the largest single call of the C5 workload), bf16
-    32-256 heads and eta = 1: sampled records and steps against the oracle."""
+    """The benchmark's 70B batch (the largest single call of that workload:
+    88,640 steps of the prefix-cache trace, 63,998,080 records, prefill steps
+    with prefix-shortened chunks and decode steps) in the launch
+    configuration the benchmark times, bf16 32-256 heads and eta = 1:
+    sampled prefill and decode steps against the oracle, bf16 eta also
+    against the plain fp64 definition (no bf16 rounding points); the eta = 1
+    step sums of the streaming kernel against the per-pair path on every
+    step."""
     import torch
-    wl = _max_batch()
+    wl = gen.config5(0, C5_BATCH_STEPS)
     d = wl.desc
-    assert d.n_rows == 88_640 * 722
+    assert d.n_rows == 63_998_080
+    fam = d.family()
+    pre_steps = np.unique(d.step[fam == gen.ATTN_PREFILL])
+    dec_steps = np.unique(d.step[fam == gen.ATTN_DECODE])
+    assert len(pre_steps) > 0 and len(dec_steps) > 0
     rng = np.random.default_rng(3)
-    steps = np.unique(np.concatenate([[0, d.n_steps - 1], rng.integers(0, d.n_steps, 5)]))
+    steps = np.unique(np.concatenate([[0, d.n_steps - 1], rng.choice(pre_steps, 4), rng.choice(dec_steps, 4)]))
     rows = np.nonzero(np.isin(d.step, steps))[0]
+    assert (fam[rows] == gen.ATTN_PREFILL).any() and (fam[rows] == gen.ATTN_DECODE).any()
     rows_t = torch.as_tensor(rows, device="cuda")
+    sub = _sub_desc(d, rows)
     for eta_one in (False, True):
+        print(f"[max batch] eta_one={eta_one}", flush=True)
         di = abi.DeviceInputs(wl)
         heads = di.make_heads("bf16", 32, 256, abi.KS_ETA_ONE if eta_one else abi.KS_ETA_MLP)
         so_t, so = abi.step_outputs(d.n_steps, di.n_specs)
@@ -527,13 +495,19 @@ def test_max_size_batch_sampled():
             assert g.rel_err(stream, body_all).max() <= 2 * REL
         del di, so_t
         torch.cuda.empty_cache()
-        ref = o.eval_kernels(_sub_desc(d, rows), wl.specs, None if eta_one else wl.heads, eta_one=eta_one)
+        ref = o.eval_kernels(sub, wl.specs, None if eta_one else wl.heads, eta_one=eta_one)
         assert g.rel_err(gpu["t_roof"], ref["t_roof"]).max() <= REL
         if eta_one:
             assert (gpu["eta"] == 1.0).all()
             assert g.rel_err(gpu["t_kernel"], ref["t"]).max() <= REL
         else:
             assert g.rel_err(gpu["eta"], ref["eta"]).max() <= REL_BF16
+            dz = np.abs(_z_from_eta(gpu["eta"]) - ref["z"])
+            assert dz.max() <= ZTOL, dz.max()
+            assert g.rel_err(gpu["t_kernel"], ref["t"]).max() <= REL_BF16
+            pure = o.eval_kernels(sub, wl.specs, wl.heads, emulate_bf16=False)
+            assert g.rel_err(gpu["eta"], pure["eta"]).max() <= REL_BF16
+            assert g.rel_err(gpu["t_kernel"], pure["t"]).max() <= REL_BF16
         t_ge = np.maximum(ref["t_roof"] * gpu["eta"], wl.specs["t0"][:, None])
         assert g.rel_err(gpu["t_kernel"], t_ge).max() <= REL
         for s in range(wl.n_specs):
@@ -541,6 +515,48 @@ def test_max_size_batch_sampled():
             assert g.rel_err(body[s], ref_body).max() <= REL
             if stream is not None:
                 assert g.rel_err(stream[s, steps], ref_body).max() <= REL
+
+
+# ------------------------------------------ bf16 heads vs the plain definition --
+@pytest.mark.parametrize("which", ["c4", "c5"])
+def test_bf16_heads_against_the_unrounded_definition(which):
+    """bf16 heads against the model's plain fp64 definition (no bf16 rounding
+    points at all, the oracle's emulate_bf16=False), not only against the
+    emulation of the kernel's rounding: eta, t_kernel and the step outputs
+    within the 1e-2 bar."""
+    wl = (gen.config4(n_specs=24, grid_steps=25, c1_steps=40) if which == "c4" else gen.config5(0, 24))
+    gpu = g.eval_steps(wl)
+    pure = o.eval_kernels(wl.desc, wl.specs, wl.heads, emulate_bf16=False)
+    assert g.rel_err(gpu["eta"], pure["eta"]).max() <= REL_BF16
+    assert g.rel_err(gpu["t_kernel"], pure["t"]).max() <= REL_BF16
+    rs = o.eval_steps(wl.desc, wl.steps, wl.specs, wl.host, wl.heads, kern=pure)
+    _check_steps(wl, gpu, rs, bf16=True, n_specs=wl.n_specs)
+
+
+# ------------------------------------------------- K fields the model ignores --
+@pytest.mark.parametrize("precision,in_dim,hidden", [("f32", 16, 64), ("bf16", 16, 128)])
+def test_unused_k_fields_are_ignored(precision, in_dim, hidden):
+    """Norm, activation and embedding records carry no K: garbage in their k
+    field changes nothing (their K feature is 0 on both sides), while the
+    other families' k still counts."""
+    wl = gen.config1(0, 40).with_heads(gen.make_heads(in_dim, hidden, precision))
+    d = wl.desc
+    fam = d.family()
+    unused = np.isin(fam, [gen.RMSNORM, gen.SILU_MUL, gen.EMBED])
+    k = d.k.copy()
+    k[unused] = np.random.default_rng(9).integers(1, 1 << 17, int(unused.sum())).astype(np.uint32)
+    dk = gen.Desc(d.fam_off, d.step, d.m, d.n, k, d.a, d.b, d.req_off, d.req_q, d.req_h, d.expert_rows,
+                  d.elem_bytes)
+    wk = gen.Workload(wl.name, dk, wl.steps, wl.specs, wl.heads, wl.host)
+    ref = o.eval_kernels(dk, wl.specs, wl.heads)
+    gpu = g.eval_steps(wk)
+    _check_kernels(wk, gpu, ref, bf16=precision == "bf16")
+    base = g.eval_steps(wl)
+    for key in ("eta", "t_kernel", "t_body", "t_step"):
+        np.testing.assert_array_equal(gpu[key], base[key], err_msg=key)
+    eta1 = g.eval_steps(wk, eta_one=True, per_pair=False)
+    eta1_base = g.eval_steps(wl, eta_one=True, per_pair=False)
+    np.testing.assert_array_equal(eta1["t_body"], eta1_base["t_body"])
 
 
 # -------------------------------------------------- bounded analytical head --
