@@ -403,6 +403,29 @@ ks_status ks_eval_steps(const ks_desc* desc, const ks_steps* steps,
                         const ks_step_out* out, const ks_kernel_out* kout,
                         void* ws, size_t ws_bytes, hipStream_t stream);
 
+/*
+ * Allocation-free ks_eval_steps, for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  Same arguments, checks and results as ks_eval_steps,
+ * without the workspace: the library uses a fixed device array of
+ * KS_STATIC_SCRATCH_BYTES on each GPU instead (held from the library's load
+ * on that GPU until the process ends).  A call whose ks_workspace_bytes()
+ * exceeds it fails with KS_ERANGE before any launch.  Every call on one GPU
+ * shares that GPU's array and leaves its contents behind: calls that
+ * overlap on one GPU (other streams, other threads) race.  flags: a device
+ * uint32 or NULL; if set, the call's bad-data flag word is copied there on
+ * the stream after the evaluation (0: no record was skipped; nonzero: the
+ * evaluation skipped bad device data, which ks_validate names).  The call
+ * issues no hipMalloc, hipFree or hipMemset.
+ */
+enum { KS_STATIC_SCRATCH_BYTES = 64 << 20 };
+
+ks_status ks_eval_steps_static(const ks_desc* desc, const ks_steps* steps,
+                               const ks_spec* specs, int32_t n_specs,
+                               const ks_heads* heads, const ks_host* host,
+                               const ks_step_out* out, const ks_kernel_out* kout,
+                               uint32_t* flags, hipStream_t stream);
+
 /* Synchronous device-side check of the inputs: step order within families,
  * field limits, request and expert offsets, spec sanity.  Synchronizes the
  * stream.  Returns KS_OK, KS_EINVAL or KS_ERANGE with a message. */

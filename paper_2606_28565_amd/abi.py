@@ -18,6 +18,7 @@ NFAM = 10
 KS_OK, KS_EINVAL, KS_ERANGE, KS_EHIP, KS_EWORKSPACE = range(5)
 KS_F32, KS_BF16 = 0, 1
 KS_ETA_MLP, KS_ETA_ONE = 0, 1
+KS_STATIC_SCRATCH_BYTES = 64 << 20   # the allocation-free entry point's device array
 STATUS_NAMES = {0: "KS_OK", 1: "KS_EINVAL", 2: "KS_ERANGE", 3: "KS_EHIP", 4: "KS_EWORKSPACE"}
 
 P = C.c_void_p
@@ -133,6 +134,8 @@ def load(path: str = LIB_PATH) -> C.CDLL:
     lib.ks_eval_kernels.restype = C.c_int
     lib.ks_eval_steps.argtypes = [pd, pst, psp, C.c_int32, ph, phost, pso, pko, P, C.c_size_t, P]
     lib.ks_eval_steps.restype = C.c_int
+    lib.ks_eval_steps_static.argtypes = [pd, pst, psp, C.c_int32, ph, phost, pso, pko, P, P]
+    lib.ks_eval_steps_static.restype = C.c_int
     lib.ks_validate.argtypes = [pd, pst, psp, C.c_int32, P, C.c_size_t, P]
     lib.ks_validate.restype = C.c_int
     lib.ks_device_status.argtypes = [P, C.c_size_t, P]
@@ -187,6 +190,14 @@ def ks_eval_steps(desc, steps, specs_ptr, n_specs, heads, host, out, kout, ws_pt
                               C.byref(host), C.byref(out),
                               C.byref(kout) if kout is not None else None,
                               ws_ptr, ws_bytes, stream)
+    return _check(st) if check else st
+
+
+def ks_eval_steps_static(desc, steps, specs_ptr, n_specs, heads, host, out, kout, flags_ptr, stream,
+                         check=True):
+    st = load().ks_eval_steps_static(C.byref(desc), C.byref(steps), specs_ptr, n_specs, C.byref(heads),
+                                     C.byref(host), C.byref(out),
+                                     C.byref(kout) if kout is not None else None, flags_ptr, stream)
     return _check(st) if check else st
 
 

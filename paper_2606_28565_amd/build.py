@@ -48,12 +48,14 @@ def build(verbose: bool = False) -> str:
     expand = os.path.join(tmp, "ks_expand.o")
     _run([HIPCC, *DEVICE_FLAGS, *common, "-c", os.path.join(CSRC, "ks_kernels.hip"), "-o", kern])
     _run([HIPCC, *DEVICE_FLAGS, *common, "-c", os.path.join(CSRC, "ks_expand.hip"), "-o", expand])
+    static = os.path.join(tmp, "ks_static.o")
+    _run([HIPCC, *DEVICE_FLAGS, *common, "-c", os.path.join(CSRC, "ks_static.hip"), "-o", static])
     _run([HIPCC, *HOST_FLAGS, *common, "-D__HIP_PLATFORM_AMD__", "-c",
           os.path.join(CSRC, "ks_api.cpp"), "-o", api])
     simo = os.path.join(tmp, "ks_sim.o")
     _run([HIPCC, *HOST_FLAGS, *common, "-D__HIP_PLATFORM_AMD__", "-c",
           os.path.join(CSRC, "ks_sim.cpp"), "-o", simo])
-    objs = [kern, expand, api, simo]
+    objs = [kern, expand, static, api, simo]
     tmp_lib = LIB + ".tmp"
     _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp_lib])
     os.replace(tmp_lib, LIB)
