@@ -55,8 +55,8 @@ constexpr size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 //   specc   : n_specs * 64 B               per-spec loop constants
 //   agg     : 4 * n_steps uint64           per-step attention work
 //   range   : KS_NFAM * n_steps * 2 uint32 per (family, step) record range
-//   partial : n_specs * KS_NFAM * n_steps double
-//   carry   : n_specs * n_tiles double
+//   partial : KS_NFAM * n_steps * n_specs double (spec-minor)
+//   carry   : n_tiles * n_specs double (spec-minor)
 struct Layout {
   size_t specc, agg, range, partial, carry, total;
 };

@@ -73,8 +73,8 @@ struct EvalParams {
   uint64_t *o_flops, *o_bytes, *o_blocks;
   float *o_troof, *o_eta, *o_t;
   // per-step partial sums (nullable: no step sums)
-  double *partial;   // [n_specs][KS_NFAM][n_steps]
-  double *carry;     // [n_specs][n_tiles]
+  double *partial;   // [KS_NFAM][n_steps][n_specs] (spec-minor)
+  double *carry;     // [n_tiles][n_specs]
   uint32_t *range;   // [KS_NFAM][n_steps][2] record range of each (family, step); nullable
   uint32_t *err;
   uint8_t *o_src;    // per pair: 0 head of the mode, 1 bounded head, 2 grid (nullable)
@@ -89,7 +89,7 @@ struct FinishParams {
   const ks_spec *specs;
   int64_t fam_off[KS_NFAM + 1];
   int32_t tile_off[KS_NFAM + 1];
-  const double *partial, *carry;
+  const double *partial, *carry;       // [KS_NFAM][n_steps][n_specs], [n_tiles][n_specs]
   int32_t n_tiles;
   const uint32_t *range;               // [KS_NFAM][n_steps][2]
   ks_host host;

@@ -1248,13 +1248,12 @@ template <class H, class = void> struct PipeOK : std::false_type {};
 template <class H> struct PipeOK<H, std::enable_if_t<H::kPipe>> : std::true_type {};
 
 // Spec s's per-pair outputs of the lane's record and its segmented step sum:
-// a tail lane stores its segment's sum to dst (the tile's carry slot or the
-// (spec, family, step) partial), a record of multiplicity m adding m t (one
-// fp32 rounding).
+// a tail lane stores its segment's sum to dst[s] (dst: the tile's carry
+// slots or the (family, step) partials, one per spec, contiguous), a record
+// of multiplicity m adding m t (one fp32 rounding).
 template <bool MULT>
 __device__ __forceinline__ void spec_tail(const EvalParams &p, int s, float t_roof, float eta, float t, bool valid,
-                                          bool live, int64_t row, float tfac, const float (&fac)[6], double *dst,
-                                          size_t dst_stride) {
+                                          bool live, int64_t row, float tfac, const float (&fac)[6], double *dst) {
   if (valid) {
     const size_t i = (size_t)s * (size_t)p.fam_off[KS_NFAM] + (size_t)row;
     if (p.o_troof) p.o_troof[i] = t_roof;
@@ -1263,7 +1262,7 @@ __device__ __forceinline__ void spec_tail(const EvalParams &p, int s, float t_ro
   }
   if (p.partial) {
     const float v = seg_scan(MULT ? t * tfac : (live ? t : 0.0f), fac);
-    if (dst) dst[(size_t)s * dst_stride] = (double)v;
+    if (dst) dst[s] = (double)v;
   }
 }
 
@@ -1374,16 +1373,14 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
     // is flagged bad data; both sit at or after the wave's last live lane or
     // carry a flagged record, so the scan of every live segment is unchanged.
     const float tfac = MULT ? (live ? fc.mult : 0.0f) : 0.0f;
+    // (spec-minor layout: a tail lane's sums for all specs are one
+    // contiguous run, so its stores fill whole cache lines)
     double *dst = nullptr;
-    size_t dst_stride = 0;
     if (p.partial && is_tail) {
-      if (to_carry) {
-        dst = p.carry + tile_id;
-        dst_stride = (size_t)p.n_tiles;
-      } else {
-        dst = p.partial + (size_t)fam * p.n_steps + key;
-        dst_stride = (size_t)KS_NFAM * p.n_steps;
-      }
+      if (to_carry)
+        dst = p.carry + (size_t)tile_id * (size_t)p.n_specs;
+      else
+        dst = p.partial + ((size_t)fam * (size_t)p.n_steps + key) * (size_t)p.n_specs;
     }
 
     if constexpr (PipeOK<H>::value && !GRID) {
@@ -1430,7 +1427,7 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
             if constexpr (I == 14) {
               if (s > 0)
                 spec_tail<MULT>(p, s - 1, tr_prev, eta_prev, fmaxf(tr_prev * eta_prev, t0_prev), valid, live, row,
-                                tfac, fac, dst, dst_stride);
+                                tfac, fac, dst);
             }
             if constexpr (I == 20) on = small ? roofline<true>(rc, sn) : roofline<false>(rc, sn);
             if constexpr (I == 22) {
@@ -1463,8 +1460,7 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
         H::tail_pairs(st, zl, 0, 4);
         H::tail_pairs(st, zl, 4, 8);
         const float eta = 1.0f + __expf(-H::tail_reduce(zl, lds));
-        spec_tail<MULT>(p, S - 1, tr_prev, eta, fmaxf(tr_prev * eta, t0_prev), valid, live, row, tfac, fac, dst,
-                        dst_stride);
+        spec_tail<MULT>(p, S - 1, tr_prev, eta, fmaxf(tr_prev * eta, t0_prev), valid, live, row, tfac, fac, dst);
         continue;
       }
     }
@@ -1501,7 +1497,7 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
       if constexpr (GRID) {
         if (valid && p.o_src) p.o_src[(size_t)s * (size_t)p.fam_off[KS_NFAM] + (size_t)row] = routed ? 2 : (bnd ? 1 : 0);
       }
-      spec_tail<MULT>(p, s, o.t_roof, eta, t, valid, live, row, tfac, fac, dst, dst_stride);
+      spec_tail<MULT>(p, s, o.t_roof, eta, t, valid, live, row, tfac, fac, dst);
     }
   }
 }
@@ -1612,12 +1608,12 @@ struct SRec {
 // argument below 2^51 (the exact path of k_eval assumes B < 2^52); then
 // F u / P = W (F / B) (N / P), the first factor per record and the second
 // per spec.  BH: B - 1/2 per record, as float or double; frb, btf: F / B
-// and Bt per record.  part: the spec-0 partials of the tile's family.
+// and Bt per record.  part: the partials of the tile's family ([step][spec]).
 template <class BH>
 __device__ __forceinline__ void stream_specs(const EvalParams &p, const SRec &r, const BH (&bh)[kStreamR],
                                              const float (&frb)[kStreamR], const float (&btf)[kStreamR],
                                              double *part, bool any_tail) {
-  const size_t part_stride = (size_t)KS_NFAM * (size_t)p.n_steps;
+  const size_t S = (size_t)p.n_specs;
   for (int s = 0; s < p.n_specs; ++s) {
     const SpecC sc = spec_at(p.spec_c, s);
     const float np = sc.n_f * sc.rcp_p;
@@ -1642,8 +1638,7 @@ __device__ __forceinline__ void stream_specs(const EvalParams &p, const SRec &r,
       for (int j = 0; j < kStreamR; ++j) {
         if (r.ptail[j]) {
           const double v = (double)fmaf(r.ff[j], cin, acc[j]);
-          double *d = r.to_carry[j] ? p.carry + (size_t)s * (size_t)p.n_tiles + r.tile
-                                    : part + (size_t)s * part_stride + r.key[j];
+          double *d = r.to_carry[j] ? p.carry + (size_t)r.tile * S + s : part + (size_t)r.key[j] * S + s;
           *d = v;
         }
       }
@@ -1652,11 +1647,8 @@ __device__ __forceinline__ void stream_specs(const EvalParams &p, const SRec &r,
 }
 
 // One workgroup tile of family FAM; rng and part: the family's range table
-// and spec-0 partials (formed before the family is dispatched on, so that
-// each family's code does not hold its own copy of them).
-// One workgroup tile of family FAM; rng and part: the family's range table
-// and spec-0 partials (formed before the family is dispatched on, so that
-// each family's code does not hold its own copy of them).
+// and partials (formed before the family is dispatched on, so that each
+// family's code does not hold its own copy of them).
 template <int FAM>
 __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc, uint32_t (*ws)[kWgRows],
                                             int lane, uint32_t *rng, double *part) {
@@ -1795,7 +1787,7 @@ __global__ __launch_bounds__(kWgThreads) __attribute__((amdgpu_waves_per_eu(6)))
     const STile tc = stream_locate(p, wt, fam);
     fam = tc.fam;
     uint32_t *rng = p.range + 2 * (size_t)fam * (size_t)p.n_steps;
-    double *part = p.partial + (size_t)fam * (size_t)p.n_steps;
+    double *part = p.partial + (size_t)fam * (size_t)p.n_steps * (size_t)p.n_specs;
     switch (fam) {
       case KS_GEMM: stream_tile<KS_GEMM>(p, tc, ws, lane, rng, part); break;
       case KS_LM_HEAD: stream_tile<KS_LM_HEAD>(p, tc, ws, lane, rng, part); break;
@@ -1828,41 +1820,75 @@ __global__ void k_fill_source(uint8_t *src, EvalParams p) {
 
 // ------------------------------------------------------------ step finish
 // per (spec, step): t_body, t_comm (Eq. 3, two all-reduces per layer),
-// t_gpu and t_step (Eq. 4)
-__global__ void k_finish(FinishParams p) {
-  const int64_t total = (int64_t)p.n_specs * p.n_steps;
-  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
-       idx += (int64_t)gridDim.x * blockDim.x) {
-    const int s = (int)(idx / p.n_steps);
-    const int64_t j = idx - (int64_t)s * p.n_steps;
-    double body = 0.0;
-    for (int f = 0; f < KS_NFAM; ++f) {
-      // clamped to the family's rows: a range left half-written by unsorted
-      // input (reported by ks_validate) still indexes only this family's tiles
-      const int64_t base = p.fam_off[f], top = p.fam_off[f + 1];
-      int64_t r0 = p.range[2 * (f * p.n_steps + j)];
-      int64_t r1 = p.range[2 * (f * p.n_steps + j) + 1];
-      r0 = r0 < base ? base : (r0 > top ? top : r0);
-      r1 = r1 < base ? base : (r1 > top ? top : r1);
-      if (r0 >= r1) continue;
-      body += p.partial[((size_t)s * KS_NFAM + f) * p.n_steps + j];
-      const int t_first = p.tile_off[f] + (int)((r0 - base) / kTileRows);
-      const int t_last = p.tile_off[f] + (int)((r1 - 1 - base) / kTileRows);
-      for (int t = t_first + 1; t <= t_last; ++t) body += p.carry[(size_t)s * p.n_tiles + t];
+// t_gpu and t_step (Eq. 4).  The partial sums are spec-minor and the
+// outputs step-minor, so a workgroup takes a tile of kFinSteps steps x
+// kFinSpecs specs (kFinSpecs a power of two, at least the spec count or
+// 16): it reads with the spec fastest, passes the three results through
+// LDS, and writes with the step fastest.
+constexpr int kFinThreads = 256;
+
+__global__ __launch_bounds__(kFinThreads) void k_finish(FinishParams p, int spec_bits) {
+  __shared__ double res[3][kFinThreads];
+  const int tps = 1 << spec_bits;                 // specs per tile
+  const int tst = kFinThreads >> spec_bits;        // steps per tile
+  const int64_t n_st = (p.n_steps + tst - 1) / tst;
+  const int64_t n_sp = (p.n_specs + tps - 1) / tps;
+  const int tid = threadIdx.x;
+  for (int64_t tile = blockIdx.x; tile < n_st * n_sp; tile += gridDim.x) {
+    const int64_t j0 = (tile % n_st) * tst;
+    const int s0 = (int)(tile / n_st) * tps;
+    // phase 1: thread (step jj, spec ss), spec fastest
+    {
+      const int ss = tid & (tps - 1), jj = tid >> spec_bits;
+      const int s = s0 + ss;
+      const int64_t j = j0 + jj;
+      if (s < p.n_specs && j < p.n_steps) {
+        const size_t S = (size_t)p.n_specs;
+        double body = 0.0;
+        for (int f = 0; f < KS_NFAM; ++f) {
+          // clamped to the family's rows: a range left half-written by
+          // unsorted input (reported by ks_validate) still indexes only this
+          // family's tiles
+          const int64_t base = p.fam_off[f], top = p.fam_off[f + 1];
+          int64_t r0 = p.range[2 * (f * p.n_steps + j)];
+          int64_t r1 = p.range[2 * (f * p.n_steps + j) + 1];
+          r0 = r0 < base ? base : (r0 > top ? top : r0);
+          r1 = r1 < base ? base : (r1 > top ? top : r1);
+          if (r0 >= r1) continue;
+          body += p.partial[((size_t)f * (size_t)p.n_steps + (size_t)j) * S + s];
+          const int t_first = p.tile_off[f] + (int)((r0 - base) / kTileRows);
+          const int t_last = p.tile_off[f] + (int)((r1 - 1 - base) / kTileRows);
+          for (int t = t_first + 1; t <= t_last; ++t) body += p.carry[(size_t)t * S + s];
+        }
+        const ks_spec sp = p.specs[s];
+        const double P = (double)p.tp[j];
+        const double Sb = (double)p.agg[j] * (double)p.hidden[j] * (double)p.elem_bytes;
+        double t_ar = 0.0;
+        if (P > 1.0)
+          t_ar = sp.ar_alpha0 + sp.ar_alpha_log2p * log2(P) + 2.0 * (P - 1.0) / P * Sb / sp.ar_beta;
+        const double comm = 2.0 * (double)p.layers[j] * t_ar;
+        const double gpu = p.host.body_scale * body + comm;
+        const double step = fmax(gpu + (double)p.n_launch[j] * p.host.c_disp, p.host.ell) +
+                            fmax(0.0, p.host.c_ovl - gpu) + p.host.c_tail;
+        res[0][ss * tst + jj] = body;
+        res[1][ss * tst + jj] = gpu;
+        res[2][ss * tst + jj] = step;
+      }
     }
-    const ks_spec sp = p.specs[s];
-    const double P = (double)p.tp[j];
-    const double S = (double)p.agg[j] * (double)p.hidden[j] * (double)p.elem_bytes;
-    double t_ar = 0.0;
-    if (P > 1.0)
-      t_ar = sp.ar_alpha0 + sp.ar_alpha_log2p * log2(P) + 2.0 * (P - 1.0) / P * S / sp.ar_beta;
-    const double comm = 2.0 * (double)p.layers[j] * t_ar;
-    const double gpu = p.host.body_scale * body + comm;
-    const double step = fmax(gpu + (double)p.n_launch[j] * p.host.c_disp, p.host.ell) +
-                        fmax(0.0, p.host.c_ovl - gpu) + p.host.c_tail;
-    p.t_body[idx] = body;
-    p.t_gpu[idx] = gpu;
-    p.t_step[idx] = step;
+    __syncthreads();
+    // phase 2: thread (spec ss, step jj), step fastest
+    {
+      const int jj = tid % tst, ss = tid / tst;
+      const int s = s0 + ss;
+      const int64_t j = j0 + jj;
+      if (s < p.n_specs && j < p.n_steps) {
+        const size_t o = (size_t)s * (size_t)p.n_steps + (size_t)j;
+        p.t_body[o] = res[0][ss * tst + jj];
+        p.t_gpu[o] = res[1][ss * tst + jj];
+        p.t_step[o] = res[2][ss * tst + jj];
+      }
+    }
+    __syncthreads();
   }
 }
 
@@ -2048,7 +2074,11 @@ hipError_t launch_fill_source(const EvalParams &p, hipStream_t s) {
 
 hipError_t launch_finish(const FinishParams &p, hipStream_t s) {
   if (p.n_steps == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_finish, dim3(grid_for((int64_t)p.n_specs * p.n_steps, 256, 8192)), dim3(256), 0, s, p);
+  int bits = 0;   // specs per tile: the spec count rounded up to a power of two, at most 16
+  while (bits < 4 && (1 << bits) < p.n_specs) ++bits;
+  const int64_t tiles = ((p.n_steps + (kFinThreads >> bits) - 1) / (kFinThreads >> bits)) *
+                        (((int64_t)p.n_specs + (1 << bits) - 1) >> bits);
+  hipLaunchKernelGGL(k_finish, dim3(grid_for(tiles, 1, 8192)), dim3(kFinThreads), 0, s, p, bits);
   return hipGetLastError();
 }
 
