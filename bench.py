@@ -102,12 +102,12 @@ def copy_calibration(nbytes: int, reps: int) -> None:
 FIELDS_USED = {0: 4, 1: 4, 2: 5, 3: 4, 4: 4, 5: 3, 6: 4, 7: 3, 8: 4, 9: 3}
 
 
-def stream_bytes(wl, n_specs: int) -> float:
+def stream_bytes(wl, n_specs: int, sums: bool = True, pair_outputs: int = 0) -> float:
     """Algorithmic HBM bytes of one evaluation-kernel launch: the record
     fields each family uses, the per-expert row counts of grouped records,
-    the per-step attention work (4 x u64 per step), and the writes: one
-    range (2 x u32) per (family, step) and one fp64 partial per (spec,
-    family, step)."""
+    the per-step attention work (4 x u64 per step), and the writes: with
+    step sums one range (2 x u32) per (family, step) and one fp64 partial
+    per (spec, family, step); pair_outputs fp32 values per (spec, record)."""
     import numpy as np
     d = wl.desc
     rows = np.diff(d.fam_off)
@@ -115,8 +115,10 @@ def stream_bytes(wl, n_specs: int) -> float:
     g0, g1 = int(d.fam_off[2]), int(d.fam_off[3])
     b += 4.0 * float(d.a[g0:g1].astype(np.int64).sum())
     b += 32.0 * d.n_steps
-    segs = sum(len(np.unique(d.step[d.fam_off[f]:d.fam_off[f + 1]])) for f in range(len(rows)))
-    b += segs * (8.0 + 8.0 * n_specs)
+    if sums:
+        segs = sum(len(np.unique(d.step[d.fam_off[f]:d.fam_off[f + 1]])) for f in range(len(rows)))
+        b += segs * (8.0 + 8.0 * n_specs)
+    b += 4.0 * pair_outputs * d.n_rows * n_specs
     return b
 
 
@@ -316,7 +318,10 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=15)
     ap.add_argument("--workload", default="c4", choices=["c4", "c1", "c5-batch"])
     ap.add_argument("--eta-one", action="store_true", help="eta = 1 (pure roofline) mode")
-    ap.add_argument("--per-pair", action="store_true", help="also write per-pair t_roof/eta/t_kernel")
+    ap.add_argument("--per-pair", action="store_true",
+                    help="also write each pair's latency t_kernel (ks_eval_steps with per-pair outputs)")
+    ap.add_argument("--kernels", action="store_true",
+                    help="per-kernel latencies only: ks_eval_kernels writing t_kernel for every pair, no step sums")
     ap.add_argument("--bounded", default="none", choices=["none", "mixed", "all"],
                     help="families on the bounded analytical head: none; the GEMMs, embedding and "
                          "KV writes (mixed, the rest on the MLP or eta = 1); or all")
@@ -386,8 +391,8 @@ def main() -> int:
         routed_frac = float((src_t["source"] == 2).float().mean().item())
         del src_t, so0_t
     so_t, so = abi.step_outputs(wl.desc.n_steps, di.n_specs)
-    if args.per_pair:
-        ko_t, ko = abi.kernel_outputs(wl.desc.n_rows, di.n_specs, counts=False)
+    if args.per_pair or args.kernels:
+        ko_t, ko = abi.kernel_outputs(wl.desc.n_rows, di.n_specs, counts=False, t_roof=False, eta=False)
     else:
         ko = None
     stream = abi.current_stream()
@@ -411,6 +416,9 @@ def main() -> int:
                 return
             abi.ks_eval_steps(db.desc, db.steps, di.specs_ptr, di.n_specs, heads, di.host, so, ko,
                               ews_ptr, ews_bytes, stream)
+            return
+        if args.kernels:
+            abi.ks_eval_kernels(di.desc, di.specs_ptr, di.n_specs, heads, ko, di.ws_ptr, di.ws_bytes, stream)
             return
         abi.ks_eval_steps(di.desc, di.steps, di.specs_ptr, di.n_specs, heads, di.host, so, ko,
                           di.ws_ptr, di.ws_bytes, stream)
@@ -502,7 +510,9 @@ def main() -> int:
         on_mlp_n = int(np.count_nonzero(on_mlp))
     mlp_pairs = on_mlp_n * di.n_specs if head_pairs is None else head_pairs
     if args.eta_one or bmask == gen.BOUNDED_ALL:
-        alg = stream_bytes(wl, di.n_specs) if eval_desc is None or args.expand != "homogeneous" else None
+        alg = (stream_bytes(wl, di.n_specs, sums=not args.kernels,
+                            pair_outputs=1 if (args.per_pair or args.kernels) else 0)
+               if eval_desc is None or args.expand != "homogeneous" else None)
         bound, unit, peak = "hbm", "GB/s", PEAK["hbm"] / 1e9
         achieved = alg / (k_ms * 1e-3) / 1e9 if alg is not None else None
         dtype = "f32"
@@ -527,13 +537,15 @@ def main() -> int:
                            + ("" if not bmask else f"; bounded head on families 0x{bmask:03x}")
                            + ("" if grid is None else f"; Tier B grid on every family, {100 * routed_frac:.1f}% of "
                                                       f"the pairs routed to it"),
-                   "per_pair_outputs": bool(args.per_pair),
+                   "per_pair_outputs": bool(args.per_pair or args.kernels),
+                   "step_sums": not args.kernels,
                    "input": ("batch descriptors, expanded on the GPU every step ("
                              + args.expand + " records)") if db is not None else "kernel records"},
         "step_evals_per_s": step_evals,
         "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
                      "frac": achieved / peak if achieved is not None else None,
-                     "traffic": (recorded_traffic(f"{args.workload}{'-eta1' if args.eta_one else ''}")
+                     "traffic": (recorded_traffic(f"{args.workload}{'-eta1' if args.eta_one else ''}"
+                                                  f"{'-kernels' if args.kernels else ('-pair' if args.per_pair else '')}")
                                  if not bmask and db is None and grid is None else None),
                      "kernel_ms": k_ms, "evaluated_records": n_eval,
                      "note": "achieved = algorithmic work of one evaluation-kernel launch (FLOPs of the "

@@ -1503,22 +1503,27 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
 }
 
 // ------------------------------------------------------------ eta = 1 stream
-// The pure-roofline step sums (eta = 1, Eq. 2 and the segmented sum of
-// Sec. 5.7) when no per-pair output is asked for.  A wave takes a workgroup
-// tile on its own (256 consecutive records of one family: four 64-record
-// tiles) and each lane four consecutive records of it, so that each 16-lane
-// DPP row holds exactly one 64-record tile.  The fields arrive by coalesced
-// loads and are transposed through a wave-private LDS slot.  Per spec a lane
-// sums its records' t in runs of equal step (one FMA each); one segmented
-// scan per row then joins the lanes' last runs, and each run's tail record
-// adds the carry-in of the lanes before it.  The cross-lane work is thus per
-// four records instead of per record.  Runs are split at the 64-record tile
-// boundaries as in k_eval, and the partial sums, carries and record ranges
-// are the ones k_eval writes, so k_finish reads either alike.
+// The pure roofline (eta = 1, Eq. 2) of every (spec, record) pair: its
+// per-pair outputs and/or the step sums (Sec. 5.7).  A wave takes a
+// workgroup tile on its own (256 consecutive records of one family: four
+// 64-record tiles) and each lane four consecutive records of it, so that
+// each 16-lane DPP row holds exactly one 64-record tile.  The fields arrive
+// by coalesced loads and are transposed through a wave-private LDS slot.
+// Per spec a lane writes its four records' per-pair outputs as one vector
+// store each, and sums their t in runs of equal step (one FMA each); one
+// segmented scan per row then joins the lanes' last runs, and each run's
+// tail record adds the carry-in of the lanes before it.  The cross-lane
+// work is thus per four records instead of per record.  Runs are split at
+// the 64-record tile boundaries as in k_eval, and the partial sums, carries
+// and record ranges are the ones k_eval writes, so k_finish reads either
+// alike.
 constexpr int kStreamR = 4;                       // records per lane
-constexpr int kStreamSlots = 6;                   // step, m, n, k, a, b
 static_assert(kWave * kStreamR == kWgRows, "a wave of the stream takes one workgroup tile");
 static_assert(kTileRows == 16 * kStreamR, "a 64-record tile is one 16-lane row");
+
+// what a launch of the stream computes: step sums, per-pair outputs, and
+// whether records carry multiplicities (step sums only)
+enum : int { kStrSums = 1, kStrPair = 2, kStrMult = 4 };
 
 // orders a wave's LDS writes before its later reads (lanes read what other
 // lanes of the same wave wrote)
@@ -1541,6 +1546,17 @@ constexpr bool uses_field(int fam, int f) {
   return f == 0 || f == 2 || (f == 1 && uses_m(fam)) || (f == 3 && uses_k(fam)) || (f == 4 && uses_a(fam)) ||
          (f == 5 && uses_b(fam));
 }
+// LDS slot of field f (0 .. 5: step, m, n, k, a, b) for the family: the
+// used fields in order (at most five per family); the multiplicity, when
+// present, takes slot 5
+constexpr int slot_of(int fam, int f) {
+  int n = 0;
+  for (int i = 0; i < f; ++i) n += uses_field(fam, i) ? 1 : 0;
+  return n;
+}
+constexpr int kStreamFieldSlots = 5;
+static_assert(slot_of(KS_GROUPED_GEMM, 6) <= kStreamFieldSlots && slot_of(KS_GEMM, 6) <= kStreamFieldSlots,
+              "at most five fields per family");
 
 // a workgroup tile of the stream: family, first row, valid rows, first tile id
 struct STile {
@@ -1594,14 +1610,32 @@ constexpr uint32_t kStreamSmallB = 1u << 22;
 // What the spec loop needs of a lane's four records besides their roofline
 // operands.  Runs never mix live and other records (those carry key
 // kNoKey), so the t of a record that is not live never reaches a stored
-// sum and needs no masking.
+// sum and needs no masking.  Per-record flags are bits of one word (bit j:
+// record j) so that they take one register rather than a lane mask each.
 struct SRec {
   uint32_t key[kStreamR];
-  float fj[kStreamR], ff[kStreamR];   // run continues from record j - 1; record j is in the lane's first run
-  bool ptail[kStreamR], to_carry[kStreamR];
-  float g[4], fc;                     // row-scan factors; the lane's first run continues the lane before
+  float fj[kStreamR];      // 1: record j continues the run of record j - 1
+  float mf[kStreamR];      // the record's multiplicity (step sums with multiplicities)
+  uint32_t ptail;          // bit j: record j ends a run within its 64-record tile
+  uint32_t to_carry;       // bit j: ... and that run continues from the previous tile
+  uint32_t first;          // bit j: record j is in the lane's first run
+  float g[4], fc;          // row-scan factors; the lane's first run continues the lane before
   int tile;
 };
+
+// four consecutive per-pair values of a lane (records 4 lane .. 4 lane + 3
+// of the tile) at q: one 16-byte store when all four are valid and q is
+// 16-byte aligned, else one store per valid record
+__device__ __forceinline__ void store_quad(float *q, int lane, int nvalid, const float (&v)[kStreamR]) {
+  typedef float f32x4 __attribute__((ext_vector_type(4)));
+  if (kStreamR * lane + kStreamR - 1 < nvalid && (reinterpret_cast<uintptr_t>(q) & 15) == 0) {
+    *reinterpret_cast<f32x4 *>(q) = f32x4{v[0], v[1], v[2], v[3]};
+  } else {
+#pragma unroll
+    for (int j = 0; j < kStreamR; ++j)
+      if (kStreamR * lane + j < nvalid) q[j] = v[j];
+  }
+}
 
 // Spec loop.  W = ceil(B / N) as the ceiling of (B - 1/2) / N: in fp32 for
 // block counts below 2^22 (as above), else in fp64, exact by the same
@@ -1609,15 +1643,17 @@ struct SRec {
 // F u / P = W (F / B) (N / P), the first factor per record and the second
 // per spec.  BH: B - 1/2 per record, as float or double; frb, btf: F / B
 // and Bt per record.  part: the partials of the tile's family ([step][spec]).
-template <class BH>
-__device__ __forceinline__ void stream_specs(const EvalParams &p, const SRec &r, const BH (&bh)[kStreamR],
-                                             const float (&frb)[kStreamR], const float (&btf)[kStreamR],
-                                             double *part, bool any_tail) {
+template <int VAR, class BH>
+__device__ __forceinline__ void stream_specs(const EvalParams &p, const STile &tc, int lane, const SRec &r,
+                                             const BH (&bh)[kStreamR], const float (&frb)[kStreamR],
+                                             const float (&btf)[kStreamR], double *part, bool any_tail) {
+  constexpr bool SUMS = (VAR & kStrSums) != 0, PAIR = (VAR & kStrPair) != 0, MULT = (VAR & kStrMult) != 0;
   const size_t S = (size_t)p.n_specs;
+  const size_t n_rows = (size_t)p.fam_off[KS_NFAM];
   for (int s = 0; s < p.n_specs; ++s) {
     const SpecC sc = spec_at(p.spec_c, s);
     const float np = sc.n_f * sc.rcp_p;
-    float acc[kStreamR];
+    float t[kStreamR], tr[kStreamR];
 #pragma unroll
     for (int j = 0; j < kStreamR; ++j) {
       float W;
@@ -1625,21 +1661,38 @@ __device__ __forceinline__ void stream_specs(const EvalParams &p, const SRec &r,
         W = ceilf(bh[j] * sc.rcp_n);
       else
         W = (float)ceil(bh[j] * sc.rcp_nd);
-      const float t = fmaxf(fmaxf(W * (frb[j] * np), btf[j] * sc.rcp_bw), sc.t0);
-      acc[j] = j == 0 ? t : fmaf(r.fj[j], acc[j - 1], t);
+      tr[j] = fmaxf(W * (frb[j] * np), btf[j] * sc.rcp_bw);
+      t[j] = fmaxf(tr[j], sc.t0);
     }
-    // the run ending at this lane's last record, over the row's lanes so far
-    const float x = row_scan(acc[kStreamR - 1], r.g);
-    // what the lanes before add to this lane's first run (0 at a row start)
-    const float cin = r.fc * __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
-                                                         0, __builtin_bit_cast(int, x), 0x111, 0xf, 0xf, true));
-    if (any_tail) {
+    if constexpr (PAIR) {
+      const size_t i0 = (size_t)s * n_rows + (size_t)tc.row0 + (size_t)(kStreamR * lane);
+      if (p.o_troof) store_quad(p.o_troof + i0, lane, tc.nvalid, tr);
+      if (p.o_eta) {
+        const float one[kStreamR] = {1.0f, 1.0f, 1.0f, 1.0f};
+        store_quad(p.o_eta + i0, lane, tc.nvalid, one);
+      }
+      if (p.o_t) store_quad(p.o_t + i0, lane, tc.nvalid, t);
+    }
+    if constexpr (SUMS) {
+      float acc[kStreamR];
 #pragma unroll
       for (int j = 0; j < kStreamR; ++j) {
-        if (r.ptail[j]) {
-          const double v = (double)fmaf(r.ff[j], cin, acc[j]);
-          double *d = r.to_carry[j] ? p.carry + (size_t)r.tile * S + s : part + (size_t)r.key[j] * S + s;
-          *d = v;
+        const float v = MULT ? t[j] * r.mf[j] : t[j];
+        acc[j] = j == 0 ? v : fmaf(r.fj[j], acc[j - 1], v);
+      }
+      // the run ending at this lane's last record, over the row's lanes so far
+      const float x = row_scan(acc[kStreamR - 1], r.g);
+      // what the lanes before add to this lane's first run (0 at a row start)
+      const float cin = r.fc * __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+                                                           0, __builtin_bit_cast(int, x), 0x111, 0xf, 0xf, true));
+      if (any_tail) {
+#pragma unroll
+        for (int j = 0; j < kStreamR; ++j) {
+          if ((r.ptail >> j) & 1u) {
+            const double v = (double)(((r.first >> j) & 1u) ? acc[j] + cin : acc[j]);
+            double *d = ((r.to_carry >> j) & 1u) ? p.carry + (size_t)r.tile * S + s : part + (size_t)r.key[j] * S + s;
+            *d = v;
+          }
         }
       }
     }
@@ -1649,110 +1702,143 @@ __device__ __forceinline__ void stream_specs(const EvalParams &p, const SRec &r,
 // One workgroup tile of family FAM; rng and part: the family's range table
 // and partials (formed before the family is dispatched on, so that each
 // family's code does not hold its own copy of them).
-template <int FAM>
+template <int FAM, int VAR>
 __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc, uint32_t (*ws)[kWgRows],
                                             int lane, uint32_t *rng, double *part) {
-  uint64_t B[kStreamR];
-  float Ff[kStreamR], Btf[kStreamR];
+  constexpr bool SUMS = (VAR & kStrSums) != 0, PAIR = (VAR & kStrPair) != 0, MULT = (VAR & kStrMult) != 0;
   // coalesced loads (lane l: records 64 j + l), then the transpose through
   // the wave's LDS slot (lane l: records 4 l + j)
   {
-    uint32_t raw[kStreamSlots][kStreamR];
-    const uint32_t *src[kStreamSlots] = {p.step, p.m, p.n, p.k, p.a, p.b};
+    uint32_t raw[6][kStreamR], rawm[kStreamR];
+    const uint32_t *src[6] = {p.step, p.m, p.n, p.k, p.a, p.b};
 #pragma unroll
     for (int j = 0; j < kStreamR; ++j) {
       const int i = kWave * j + lane;
       const uint32_t off = (uint32_t)(i < tc.nvalid ? i : 0);
 #pragma unroll
-      for (int f = 0; f < kStreamSlots; ++f)
+      for (int f = 0; f < 6; ++f)
         if (uses_field(FAM, f)) raw[f][j] = (src[f] + tc.row0)[off];
+      if constexpr (MULT) rawm[j] = (p.mult + tc.row0)[off];
     }
 #pragma unroll
-    for (int f = 0; f < kStreamSlots; ++f) {
+    for (int f = 0; f < 6; ++f) {
       if (uses_field(FAM, f)) {
 #pragma unroll
-        for (int j = 0; j < kStreamR; ++j) ws[f][kWave * j + lane] = raw[f][j];
+        for (int j = 0; j < kStreamR; ++j) ws[slot_of(FAM, f)][kWave * j + lane] = raw[f][j];
       }
+    }
+    if constexpr (MULT) {
+#pragma unroll
+      for (int j = 0; j < kStreamR; ++j) ws[kStreamFieldSlots][kWave * j + lane] = rawm[j];
     }
   }
   // the steps just before and after the tile: lane 0 and lane 1 of one load
   // (each address inside the family: the tile's first row where a
   // neighbour does not exist)
-  const int pn_off = lane == 0 ? (tc.hp ? -1 : 0) : (tc.hn ? kWgRows : 0);
-  const uint32_t pn = (p.step + tc.row0)[pn_off];
+  uint32_t pn = 0;
+  if constexpr (SUMS) {
+    const int pn_off = lane == 0 ? (tc.hp ? -1 : 0) : (tc.hn ? kWgRows : 0);
+    pn = (p.step + tc.row0)[pn_off];
+  }
   wave_lds_sync();
-  uint32_t v[kStreamSlots][kStreamR];
+  uint32_t v[6][kStreamR];
 #pragma unroll
-  for (int f = 0; f < kStreamSlots; ++f) {
+  for (int f = 0; f < 6; ++f) {
     u32x4 q = {0, 0, 0, 0};
-    if (uses_field(FAM, f)) q = *reinterpret_cast<const u32x4 *>(&ws[f][kStreamR * lane]);
+    if (uses_field(FAM, f)) q = *reinterpret_cast<const u32x4 *>(&ws[slot_of(FAM, f)][kStreamR * lane]);
 #pragma unroll
     for (int j = 0; j < kStreamR; ++j) v[f][j] = q[j];
   }
-  const uint32_t prev = tc.hp ? __builtin_amdgcn_readlane(pn, 0) : kNoKey;
-  const uint32_t next = tc.hn ? __builtin_amdgcn_readlane(pn, 1) : kNoKey;
-
-  // per record: counts and the spec-independent roofline operands
   SRec r;
+  if constexpr (MULT) {
+    const u32x4 q = *reinterpret_cast<const u32x4 *>(&ws[kStreamFieldSlots][kStreamR * lane]);
+#pragma unroll
+    for (int j = 0; j < kStreamR; ++j) r.mf[j] = (float)q[j];   // exact below 2^24
+  }
+
+  // per record: counts and the spec-independent roofline operands; exact
+  // (u64) when the per-record counts are written, else in fp32
   uint32_t bad = 0;
   bool live[kStreamR];
   bool big = false;
+  uint64_t B[kStreamR];
+  float Ff[kStreamR], Btf[kStreamR];
   // a step at or past n_steps (none can be when n_steps >= 2^32)
   const bool lim = p.n_steps <= (int64_t)UINT32_MAX;
   const uint32_t n_steps32 = (uint32_t)p.n_steps;
+  const bool exact = PAIR && (p.o_flops || p.o_bytes || p.o_blocks);   // wave-uniform
 #pragma unroll
   for (int j = 0; j < kStreamR; ++j) {
     const bool valid = kStreamR * lane + j < tc.nvalid;
     uint32_t b = 0;
     if (lim && v[0][j] >= n_steps32) b |= kErrStep;
-    const CntF cf = record_counts_f(FAM, v[1][j], v[2][j], v[3][j], v[4][j], v[5][j], v[0][j], p, b);
+    if (PAIR && exact) {
+      const Cnt c = record_counts(FAM, v[1][j], v[2][j], v[3][j], v[4][j], v[5][j], v[0][j], p, b);
+      if (valid) {
+        const size_t row = (size_t)tc.row0 + (size_t)(kStreamR * lane + j);
+        if (p.o_flops) p.o_flops[row] = c.F;
+        if (p.o_bytes) p.o_bytes[row] = c.Bt;
+        if (p.o_blocks) p.o_blocks[row] = c.B;
+      }
+      B[j] = c.B;
+      Ff[j] = (float)c.F;
+      Btf[j] = (float)c.Bt;
+    } else {
+      const CntF cf = record_counts_f(FAM, v[1][j], v[2][j], v[3][j], v[4][j], v[5][j], v[0][j], p, b);
+      B[j] = cf.B;
+      Ff[j] = cf.F;
+      Btf[j] = cf.Bt;
+    }
     if (valid) bad |= b;
     live[j] = valid && !(b & kErrStep);
     r.key[j] = live[j] ? v[0][j] : kNoKey;
-    B[j] = cf.B;
-    Ff[j] = cf.F;
-    Btf[j] = cf.Bt;
-    big |= cf.B >= kStreamSmallB;
+    big |= B[j] >= kStreamSmallB;
   }
   if (bad) atomicOr(p.err, bad);
   const bool small = __ballot(big) == 0;   // wave-uniform
 
-  // neighbours: the record before this lane's first (lane 0: the tile
-  // edge) and after its last (lane 63: the tile edge)
-  const uint32_t kp = (uint32_t)__builtin_amdgcn_update_dpp((int)prev, (int)r.key[kStreamR - 1], 0x138, 0xf, 0xf, false);
-  const uint32_t kn = (uint32_t)__builtin_amdgcn_update_dpp((int)next, (int)r.key[0], 0x130, 0xf, 0xf, false);
-  const int row_lane = lane & 15;
-  r.tile = tc.tile0 + (lane >> 4);
-  // the key of the row's first record and of the record before the row
-  // (row_newbcast:0 gives each row its lane 0)
-  const uint32_t rk0 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)r.key[0], 0x150, 0xf, 0xf, false);
-  const uint32_t rkp = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)kp, 0x150, 0xf, 0xf, false);
-  bool any = false;
+  bool any_tail = false;
+  if constexpr (SUMS) {
+    const uint32_t prev = tc.hp ? __builtin_amdgcn_readlane(pn, 0) : kNoKey;
+    const uint32_t next = tc.hn ? __builtin_amdgcn_readlane(pn, 1) : kNoKey;
+    // neighbours: the record before this lane's first (lane 0: the tile
+    // edge) and after its last (lane 63: the tile edge)
+    const uint32_t kp =
+        (uint32_t)__builtin_amdgcn_update_dpp((int)prev, (int)r.key[kStreamR - 1], 0x138, 0xf, 0xf, false);
+    const uint32_t kn = (uint32_t)__builtin_amdgcn_update_dpp((int)next, (int)r.key[0], 0x130, 0xf, 0xf, false);
+    const int row_lane = lane & 15;
+    r.tile = tc.tile0 + (lane >> 4);
+    // the key of the row's first record and of the record before the row
+    // (row_newbcast:0 gives each row its lane 0)
+    const uint32_t rk0 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)r.key[0], 0x150, 0xf, 0xf, false);
+    const uint32_t rkp = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)kp, 0x150, 0xf, 0xf, false);
+    r.ptail = r.to_carry = r.first = 0;
 #pragma unroll
-  for (int j = 0; j < kStreamR; ++j) {
-    const uint32_t key = r.key[j];
-    const uint32_t before = j == 0 ? kp : r.key[j - 1];
-    const uint32_t after = j == kStreamR - 1 ? kn : r.key[j + 1];
-    r.fj[j] = j > 0 && key == before ? 1.0f : 0.0f;
-    r.ff[j] = key == r.key[0] ? 1.0f : 0.0f;
-    // the (family, step) record range, written where its global first and
-    // last records are
-    const uint32_t row = (uint32_t)(tc.row0 + kStreamR * lane + j);
-    if (live[j] && before != key) rng[2 * (size_t)key] = row;
-    if (live[j] && after != key) rng[2 * (size_t)key + 1] = row + 1;
-    // a run's last record within its 64-record tile
-    r.ptail[j] = live[j] && (after != key || (j == kStreamR - 1 && row_lane == 15));
-    r.to_carry[j] = key == rk0 && rkp == rk0;
-    any |= r.ptail[j];
+    for (int j = 0; j < kStreamR; ++j) {
+      const uint32_t key = r.key[j];
+      const uint32_t before = j == 0 ? kp : r.key[j - 1];
+      const uint32_t after = j == kStreamR - 1 ? kn : r.key[j + 1];
+      r.fj[j] = j > 0 && key == before ? 1.0f : 0.0f;
+      // the (family, step) record range, written where its global first and
+      // last records are
+      const uint32_t row = (uint32_t)(tc.row0 + kStreamR * lane + j);
+      if (live[j] && before != key) rng[2 * (size_t)key] = row;
+      if (live[j] && after != key) rng[2 * (size_t)key + 1] = row + 1;
+      // a run's last record within its 64-record tile
+      const bool pt = live[j] && (after != key || (j == kStreamR - 1 && row_lane == 15));
+      r.ptail |= (pt ? 1u : 0u) << j;
+      r.to_carry |= (key == rk0 && rkp == rk0 ? 1u : 0u) << j;
+      r.first |= (key == r.key[0] ? 1u : 0u) << j;
+    }
+    any_tail = __ballot(r.ptail != 0) != 0;
+    r.fc = row_lane != 0 && kp == r.key[0] ? 1.0f : 0.0f;
+    // row-scan factors on the lanes' last keys
+    const uint32_t kl = r.key[kStreamR - 1];
+    r.g[0] = dpp_key<0x111, 0xf, 0xf>(kl) == kl ? 1.0f : 0.0f;
+    r.g[1] = dpp_key<0x112, 0xf, 0xf>(kl) == kl ? 1.0f : 0.0f;
+    r.g[2] = dpp_key<0x114, 0xf, 0xe>(kl) == kl ? 1.0f : 0.0f;
+    r.g[3] = dpp_key<0x118, 0xf, 0xc>(kl) == kl ? 1.0f : 0.0f;
   }
-  const bool any_tail = __ballot(any) != 0;
-  r.fc = row_lane != 0 && kp == r.key[0] ? 1.0f : 0.0f;
-  // row-scan factors on the lanes' last keys
-  const uint32_t kl = r.key[kStreamR - 1];
-  r.g[0] = dpp_key<0x111, 0xf, 0xf>(kl) == kl ? 1.0f : 0.0f;
-  r.g[1] = dpp_key<0x112, 0xf, 0xf>(kl) == kl ? 1.0f : 0.0f;
-  r.g[2] = dpp_key<0x114, 0xf, 0xe>(kl) == kl ? 1.0f : 0.0f;
-  r.g[3] = dpp_key<0x118, 0xf, 0xc>(kl) == kl ? 1.0f : 0.0f;
   float frb[kStreamR];
   if (small) {
     float bh[kStreamR];
@@ -1762,7 +1848,7 @@ __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc
       bh[j] = Bf - 0.5f;
       frb[j] = Ff[j] * rcpf(fmaxf(Bf, 1.0f));
     }
-    stream_specs(p, r, bh, frb, Btf, part, any_tail);
+    stream_specs<VAR>(p, tc, lane, r, bh, frb, Btf, part, any_tail);
   } else {
     double bh[kStreamR];
 #pragma unroll
@@ -1770,14 +1856,18 @@ __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc
       bh[j] = (double)B[j] - 0.5;
       frb[j] = Ff[j] * rcpf(fmaxf((float)B[j], 1.0f));
     }
-    stream_specs(p, r, bh, frb, Btf, part, any_tail);
+    stream_specs<VAR>(p, tc, lane, r, bh, frb, Btf, part, any_tail);
   }
 }
 
-// 80 registers (six waves per SIMD) measured faster than the 83 the
-// compiler picks by itself
-__global__ __launch_bounds__(kWgThreads) __attribute__((amdgpu_waves_per_eu(6))) void k_stream(EvalParams p) {
-  __shared__ __attribute__((aligned(16))) uint32_t slot[kWgWaves][kStreamSlots][kWgRows];
+// Six waves per SIMD for the plain step sums (80 registers).
+template <int VAR> struct StreamOcc { static constexpr int value = VAR == kStrSums ? 6 : 4; };
+
+template <int VAR>
+__global__ __launch_bounds__(kWgThreads) __attribute__((amdgpu_waves_per_eu(StreamOcc<VAR>::value)))
+void k_stream(EvalParams p) {
+  constexpr int NSLOT = kStreamFieldSlots + ((VAR & kStrMult) ? 1 : 0);
+  __shared__ __attribute__((aligned(16))) uint32_t slot[kWgWaves][NSLOT][kWgRows];
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int n_wgt = p.wgt_off[KS_NFAM];
   const int stride = (int)gridDim.x * kWgWaves;
@@ -1786,19 +1876,23 @@ __global__ __launch_bounds__(kWgThreads) __attribute__((amdgpu_waves_per_eu(6)))
   for (int wt = (int)blockIdx.x * kWgWaves + wave; wt < n_wgt; wt += stride) {
     const STile tc = stream_locate(p, wt, fam);
     fam = tc.fam;
-    uint32_t *rng = p.range + 2 * (size_t)fam * (size_t)p.n_steps;
-    double *part = p.partial + (size_t)fam * (size_t)p.n_steps * (size_t)p.n_specs;
+    uint32_t *rng = nullptr;
+    double *part = nullptr;
+    if constexpr ((VAR & kStrSums) != 0) {
+      rng = p.range + 2 * (size_t)fam * (size_t)p.n_steps;
+      part = p.partial + (size_t)fam * (size_t)p.n_steps * (size_t)p.n_specs;
+    }
     switch (fam) {
-      case KS_GEMM: stream_tile<KS_GEMM>(p, tc, ws, lane, rng, part); break;
-      case KS_LM_HEAD: stream_tile<KS_LM_HEAD>(p, tc, ws, lane, rng, part); break;
-      case KS_GROUPED_GEMM: stream_tile<KS_GROUPED_GEMM>(p, tc, ws, lane, rng, part); break;
-      case KS_ATTN_PREFILL: stream_tile<KS_ATTN_PREFILL>(p, tc, ws, lane, rng, part); break;
-      case KS_ATTN_DECODE: stream_tile<KS_ATTN_DECODE>(p, tc, ws, lane, rng, part); break;
-      case KS_RMSNORM: stream_tile<KS_RMSNORM>(p, tc, ws, lane, rng, part); break;
-      case KS_ROPE: stream_tile<KS_ROPE>(p, tc, ws, lane, rng, part); break;
-      case KS_SILU_MUL: stream_tile<KS_SILU_MUL>(p, tc, ws, lane, rng, part); break;
-      case KS_KV_WRITE: stream_tile<KS_KV_WRITE>(p, tc, ws, lane, rng, part); break;
-      default: stream_tile<KS_EMBED>(p, tc, ws, lane, rng, part); break;
+      case KS_GEMM: stream_tile<KS_GEMM, VAR>(p, tc, ws, lane, rng, part); break;
+      case KS_LM_HEAD: stream_tile<KS_LM_HEAD, VAR>(p, tc, ws, lane, rng, part); break;
+      case KS_GROUPED_GEMM: stream_tile<KS_GROUPED_GEMM, VAR>(p, tc, ws, lane, rng, part); break;
+      case KS_ATTN_PREFILL: stream_tile<KS_ATTN_PREFILL, VAR>(p, tc, ws, lane, rng, part); break;
+      case KS_ATTN_DECODE: stream_tile<KS_ATTN_DECODE, VAR>(p, tc, ws, lane, rng, part); break;
+      case KS_RMSNORM: stream_tile<KS_RMSNORM, VAR>(p, tc, ws, lane, rng, part); break;
+      case KS_ROPE: stream_tile<KS_ROPE, VAR>(p, tc, ws, lane, rng, part); break;
+      case KS_SILU_MUL: stream_tile<KS_SILU_MUL, VAR>(p, tc, ws, lane, rng, part); break;
+      case KS_KV_WRITE: stream_tile<KS_KV_WRITE, VAR>(p, tc, ws, lane, rng, part); break;
+      default: stream_tile<KS_EMBED, VAR>(p, tc, ws, lane, rng, part); break;
     }
   }
 }
@@ -1982,9 +2076,6 @@ static hipError_t resident_wgs(int *out) {
     if (e != hipSuccess) return e;
     e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
-    // the eta = 1 stream is latency-bound: one workgroup per CU beyond the
-    // resident ones measured faster (the extra ones start as others retire)
-    if (KIND == kEtaOne) per_cu += 1;
     r = (per_cu < 1 ? 1 : per_cu) * (n_cu < 1 ? 1 : n_cu);
     if (slot) slot->store(r, std::memory_order_relaxed);
   }
@@ -2003,19 +2094,23 @@ static hipError_t launch_grid(const EvalParams &p, hipStream_t s) {
   return hipGetLastError();
 }
 
-// k_stream: the step sums of the eta = 1 stream without multiplicities or
-// per-pair outputs; grid-stride over workgroup tiles, one per wave
-static std::atomic<int> g_stream_resident[kMaxDevices];
+// k_stream: every eta = 1 evaluation (per-pair outputs and/or step sums,
+// with or without multiplicities); grid-stride over workgroup tiles, one
+// per wave.  As many workgroups as are resident, cached per device and
+// variant.
+constexpr int kNumStreamVars = 8;
+static std::atomic<int> g_stream_resident[kMaxDevices][kNumStreamVars];
 
+template <int VAR>
 static hipError_t launch_stream(const EvalParams &p, hipStream_t s) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
-  std::atomic<int> *slot = dev < kMaxDevices ? &g_stream_resident[dev] : nullptr;
+  std::atomic<int> *slot = dev < kMaxDevices ? &g_stream_resident[dev][VAR] : nullptr;
   int cap = slot ? slot->load(std::memory_order_relaxed) : 0;
   if (cap == 0) {
     int per_cu = 0, n_cu = 0;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_stream, kWgThreads, 0);
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_stream<VAR>, kWgThreads, 0);
     if (e != hipSuccess) return e;
     e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
@@ -2024,32 +2119,35 @@ static hipError_t launch_stream(const EvalParams &p, hipStream_t s) {
   }
   const int n_wgt = p.wgt_off[KS_NFAM];
   const int need = (n_wgt + kWgWaves - 1) / kWgWaves;
-  hipLaunchKernelGGL(k_stream, dim3(need < cap ? need : cap), dim3(kWgThreads), 0, s, p);
+  hipLaunchKernelGGL((k_stream<VAR>), dim3(need < cap ? need : cap), dim3(kWgThreads), 0, s, p);
   return hipGetLastError();
 }
 
-// the eta = 1 stream has no Tier B instantiation (a grid selects the
-// head-less kind)
+// eta = 1 (no bounded or grid family: those select the head-less kind)
+static hipError_t launch_eta_one(const EvalParams &p, hipStream_t s) {
+  if (p.grid_mask || p.bounded_mask) return hipErrorInvalidValue;
+  const bool sums = p.partial && p.range;
+  const bool pair = p.o_flops || p.o_bytes || p.o_blocks || p.o_troof || p.o_eta || p.o_t;
+  // multiplicities matter only for the step sums
+  const bool mult = sums && p.mult;
+  if (!sums) return launch_stream<kStrPair>(p, s);
+  if (mult) return pair ? launch_stream<kStrSums | kStrPair | kStrMult>(p, s) : launch_stream<kStrSums | kStrMult>(p, s);
+  return pair ? launch_stream<kStrSums | kStrPair>(p, s) : launch_stream<kStrSums>(p, s);
+}
+
 template <int KIND>
 static hipError_t launch_kind(const EvalParams &p, hipStream_t s) {
   // multiplicities matter only for the step sums
   const bool mult = p.mult && p.partial;
-  if constexpr (KIND == kEtaOne) {
-    if (p.grid_mask) return hipErrorInvalidValue;
-    const bool per_pair = p.o_flops || p.o_bytes || p.o_blocks || p.o_troof || p.o_eta || p.o_t;
-    if (!mult && !per_pair && p.partial && p.range) return launch_stream(p, s);
-    return mult ? launch_grid<KIND, kVarMult>(p, s) : launch_grid<KIND, 0>(p, s);
-  } else {
-    if (p.grid_mask)
-      return mult ? launch_grid<KIND, kVarGrid | kVarMult>(p, s) : launch_grid<KIND, kVarGrid>(p, s);
-    return mult ? launch_grid<KIND, kVarMult>(p, s) : launch_grid<KIND, 0>(p, s);
-  }
+  if (p.grid_mask)
+    return mult ? launch_grid<KIND, kVarGrid | kVarMult>(p, s) : launch_grid<KIND, kVarGrid>(p, s);
+  return mult ? launch_grid<KIND, kVarMult>(p, s) : launch_grid<KIND, 0>(p, s);
 }
 
 hipError_t launch_eval(int kind, const EvalParams &p, hipStream_t s) {
   if (p.wgt_off[KS_NFAM] == 0) return hipSuccess;
   switch (kind) {
-    case kEtaOne: return launch_kind<kEtaOne>(p, s);
+    case kEtaOne: return launch_eta_one(p, s);
     case kBoundedOnly: return launch_kind<kBoundedOnly>(p, s);
     case kF32_16_64: return launch_kind<kF32_16_64>(p, s);
     case kF32_16_128: return launch_kind<kF32_16_128>(p, s);
