@@ -1507,9 +1507,9 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
 // per-pair outputs and/or the step sums (Sec. 5.7).  A wave takes a
 // workgroup tile on its own (256 consecutive records of one family: four
 // 64-record tiles) and each lane four consecutive records of it, so that
-// each 16-lane DPP row holds exactly one 64-record tile.  The fields arrive
-// by coalesced loads and are transposed through a wave-private LDS slot.
-// Per spec a lane writes its four records' per-pair outputs as one vector
+// each 16-lane DPP row holds exactly one 64-record tile.  A lane loads its
+// four records of a field with one 16-byte load, so the wave's load of a
+// field covers the tile's 1 KB contiguously.  Per spec a lane writes its four records' per-pair outputs as one vector
 // store each, and sums their t in runs of equal step (one FMA each); one
 // segmented scan per row then joins the lanes' last runs, and each run's
 // tail record adds the carry-in of the lanes before it.  The cross-lane
@@ -1525,14 +1525,6 @@ static_assert(kTileRows == 16 * kStreamR, "a 64-record tile is one 16-lane row")
 // whether records carry multiplicities (step sums only)
 enum : int { kStrSums = 1, kStrPair = 2, kStrMult = 4 };
 
-// orders a wave's LDS writes before its later reads (lanes read what other
-// lanes of the same wave wrote)
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
 // fields a family's counts read besides step and n
 constexpr bool uses_m(int fam) {
   return fam != KS_GROUPED_GEMM && fam != KS_ATTN_PREFILL && fam != KS_ATTN_DECODE;
@@ -1546,18 +1538,6 @@ constexpr bool uses_field(int fam, int f) {
   return f == 0 || f == 2 || (f == 1 && uses_m(fam)) || (f == 3 && uses_k(fam)) || (f == 4 && uses_a(fam)) ||
          (f == 5 && uses_b(fam));
 }
-// LDS slot of field f (0 .. 5: step, m, n, k, a, b) for the family: the
-// used fields in order (at most five per family); the multiplicity, when
-// present, takes slot 5
-constexpr int slot_of(int fam, int f) {
-  int n = 0;
-  for (int i = 0; i < f; ++i) n += uses_field(fam, i) ? 1 : 0;
-  return n;
-}
-constexpr int kStreamFieldSlots = 5;
-static_assert(slot_of(KS_GROUPED_GEMM, 6) <= kStreamFieldSlots && slot_of(KS_GEMM, 6) <= kStreamFieldSlots,
-              "at most five fields per family");
-
 // a workgroup tile of the stream: family, first row, valid rows, first tile id
 struct STile {
   int fam, nvalid, tile0;
@@ -1616,6 +1596,7 @@ struct SRec {
   uint32_t key[kStreamR];
   float fj[kStreamR];      // 1: record j continues the run of record j - 1
   float mf[kStreamR];      // the record's multiplicity (step sums with multiplicities)
+  uint32_t off[kStreamR];  // with 32-bit offsets: byte offset of record j's sum slot from the spec-0 partial
   uint32_t ptail;          // bit j: record j ends a run within its 64-record tile
   uint32_t to_carry;       // bit j: ... and that run continues from the previous tile
   uint32_t first;          // bit j: record j is in the lane's first run
@@ -1623,11 +1604,32 @@ struct SRec {
   int tile;
 };
 
+// a lane's four consecutive records (4 lane .. 4 lane + 3 of the tile) of
+// one field array, base: the tile's first record: one 16-byte load when the
+// four are valid and the address is 16-byte aligned, else one load per
+// record with its index clamped to the tile's valid rows (nvalid >= 1)
+__device__ __forceinline__ u32x4 load_quad(const uint32_t *base, int lane, int nvalid) {
+  const uint32_t *q = reinterpret_cast<const uint32_t *>(reinterpret_cast<const char *>(base) +
+                                                         (uint32_t)(16 * lane));
+  if (kStreamR * lane + kStreamR - 1 < nvalid && (reinterpret_cast<uintptr_t>(q) & 15) == 0)
+    return *reinterpret_cast<const u32x4 *>(q);
+  u32x4 r;
+#pragma unroll
+  for (int j = 0; j < kStreamR; ++j) {
+    const int i = kStreamR * lane + j;
+    r[j] = base[i < nvalid ? i : nvalid - 1];
+  }
+  return r;
+}
+
 // four consecutive per-pair values of a lane (records 4 lane .. 4 lane + 3
-// of the tile) at q: one 16-byte store when all four are valid and q is
-// 16-byte aligned, else one store per valid record
-__device__ __forceinline__ void store_quad(float *q, int lane, int nvalid, const float (&v)[kStreamR]) {
+// of the tile) at base + 4 lane (base: the tile's first record, the same
+// for the whole wave, so the lane's part is a 32-bit offset): one 16-byte
+// store when all four are valid and the address is 16-byte aligned, else
+// one store per valid record
+__device__ __forceinline__ void store_quad(float *base, int lane, int nvalid, const float (&v)[kStreamR]) {
   typedef float f32x4 __attribute__((ext_vector_type(4)));
+  float *q = reinterpret_cast<float *>(reinterpret_cast<char *>(base) + (uint32_t)(16 * lane));
   if (kStreamR * lane + kStreamR - 1 < nvalid && (reinterpret_cast<uintptr_t>(q) & 15) == 0) {
     *reinterpret_cast<f32x4 *>(q) = f32x4{v[0], v[1], v[2], v[3]};
   } else {
@@ -1643,6 +1645,10 @@ __device__ __forceinline__ void store_quad(float *q, int lane, int nvalid, const
 // F u / P = W (F / B) (N / P), the first factor per record and the second
 // per spec.  BH: B - 1/2 per record, as float or double; frb, btf: F / B
 // and Bt per record.  part: the partials of the tile's family ([step][spec]).
+// The sum slots are addressed as the spec's uniform base plus the records'
+// 32-bit byte offsets r.off (the launcher takes this kernel for step sums
+// only when the partial and carry regions span less than 4 GiB), so a spec
+// costs no per-lane address arithmetic.
 template <int VAR, class BH>
 __device__ __forceinline__ void stream_specs(const EvalParams &p, const STile &tc, int lane, const SRec &r,
                                              const BH (&bh)[kStreamR], const float (&frb)[kStreamR],
@@ -1665,7 +1671,7 @@ __device__ __forceinline__ void stream_specs(const EvalParams &p, const STile &t
       t[j] = fmaxf(tr[j], sc.t0);
     }
     if constexpr (PAIR) {
-      const size_t i0 = (size_t)s * n_rows + (size_t)tc.row0 + (size_t)(kStreamR * lane);
+      const size_t i0 = (size_t)s * n_rows + (size_t)tc.row0;
       if (p.o_troof) store_quad(p.o_troof + i0, lane, tc.nvalid, tr);
       if (p.o_eta) {
         const float one[kStreamR] = {1.0f, 1.0f, 1.0f, 1.0f};
@@ -1690,8 +1696,7 @@ __device__ __forceinline__ void stream_specs(const EvalParams &p, const STile &t
         for (int j = 0; j < kStreamR; ++j) {
           if ((r.ptail >> j) & 1u) {
             const double v = (double)(((r.first >> j) & 1u) ? acc[j] + cin : acc[j]);
-            double *d = ((r.to_carry >> j) & 1u) ? p.carry + (size_t)r.tile * S + s : part + (size_t)r.key[j] * S + s;
-            *d = v;
+            *reinterpret_cast<double *>(reinterpret_cast<char *>(part + s) + r.off[j]) = v;
           }
         }
       }
@@ -1703,34 +1708,27 @@ __device__ __forceinline__ void stream_specs(const EvalParams &p, const STile &t
 // and partials (formed before the family is dispatched on, so that each
 // family's code does not hold its own copy of them).
 template <int FAM, int VAR>
-__device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc, uint32_t (*ws)[kWgRows],
-                                            int lane, uint32_t *rng, double *part) {
+__device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc, int lane, uint32_t *rng,
+                                            double *part) {
   constexpr bool SUMS = (VAR & kStrSums) != 0, PAIR = (VAR & kStrPair) != 0, MULT = (VAR & kStrMult) != 0;
-  // coalesced loads (lane l: records 64 j + l), then the transpose through
-  // the wave's LDS slot (lane l: records 4 l + j)
+  // the lane's four records of each field the family uses, 16 bytes per
+  // lane and field (the wave's loads of a field cover the tile contiguously)
+  uint32_t v[6][kStreamR];
   {
-    uint32_t raw[6][kStreamR], rawm[kStreamR];
     const uint32_t *src[6] = {p.step, p.m, p.n, p.k, p.a, p.b};
 #pragma unroll
-    for (int j = 0; j < kStreamR; ++j) {
-      const int i = kWave * j + lane;
-      const uint32_t off = (uint32_t)(i < tc.nvalid ? i : 0);
-#pragma unroll
-      for (int f = 0; f < 6; ++f)
-        if (uses_field(FAM, f)) raw[f][j] = (src[f] + tc.row0)[off];
-      if constexpr (MULT) rawm[j] = (p.mult + tc.row0)[off];
-    }
-#pragma unroll
     for (int f = 0; f < 6; ++f) {
-      if (uses_field(FAM, f)) {
+      u32x4 q = {0, 0, 0, 0};
+      if (uses_field(FAM, f)) q = load_quad(src[f] + tc.row0, lane, tc.nvalid);
 #pragma unroll
-        for (int j = 0; j < kStreamR; ++j) ws[slot_of(FAM, f)][kWave * j + lane] = raw[f][j];
-      }
+      for (int j = 0; j < kStreamR; ++j) v[f][j] = q[j];
     }
-    if constexpr (MULT) {
+  }
+  SRec r;
+  if constexpr (MULT) {
+    const u32x4 q = load_quad(p.mult + tc.row0, lane, tc.nvalid);
 #pragma unroll
-      for (int j = 0; j < kStreamR; ++j) ws[kStreamFieldSlots][kWave * j + lane] = rawm[j];
-    }
+    for (int j = 0; j < kStreamR; ++j) r.mf[j] = (float)q[j];   // exact below 2^24
   }
   // the steps just before and after the tile: lane 0 and lane 1 of one load
   // (each address inside the family: the tile's first row where a
@@ -1739,21 +1737,6 @@ __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc
   if constexpr (SUMS) {
     const int pn_off = lane == 0 ? (tc.hp ? -1 : 0) : (tc.hn ? kWgRows : 0);
     pn = (p.step + tc.row0)[pn_off];
-  }
-  wave_lds_sync();
-  uint32_t v[6][kStreamR];
-#pragma unroll
-  for (int f = 0; f < 6; ++f) {
-    u32x4 q = {0, 0, 0, 0};
-    if (uses_field(FAM, f)) q = *reinterpret_cast<const u32x4 *>(&ws[slot_of(FAM, f)][kStreamR * lane]);
-#pragma unroll
-    for (int j = 0; j < kStreamR; ++j) v[f][j] = q[j];
-  }
-  SRec r;
-  if constexpr (MULT) {
-    const u32x4 q = *reinterpret_cast<const u32x4 *>(&ws[kStreamFieldSlots][kStreamR * lane]);
-#pragma unroll
-    for (int j = 0; j < kStreamR; ++j) r.mf[j] = (float)q[j];   // exact below 2^24
   }
 
   // per record: counts and the spec-independent roofline operands; exact
@@ -1831,6 +1814,14 @@ __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc
       r.first |= (key == r.key[0] ? 1u : 0u) << j;
     }
     any_tail = __ballot(r.ptail != 0) != 0;
+    {
+      // carries lie after the partials: their offset from this family's
+      // partials is (carry - part) + tile S 8
+      const uint32_t S8 = (uint32_t)p.n_specs * 8u;
+      const uint32_t cbase = (uint32_t)((const char *)p.carry - (const char *)part) + (uint32_t)r.tile * S8;
+#pragma unroll
+      for (int j = 0; j < kStreamR; ++j) r.off[j] = ((r.to_carry >> j) & 1u) ? cbase : r.key[j] * S8;
+    }
     r.fc = row_lane != 0 && kp == r.key[0] ? 1.0f : 0.0f;
     // row-scan factors on the lanes' last keys
     const uint32_t kl = r.key[kStreamR - 1];
@@ -1860,18 +1851,20 @@ __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc
   }
 }
 
-// Six waves per SIMD for the plain step sums (80 registers).
-template <int VAR> struct StreamOcc { static constexpr int value = VAR == kStrSums ? 6 : 4; };
+// Waves per SIMD the register allocator must fit: six for the plain step
+// sums (80 registers); the other variants take what their registers allow
+// (asking for seven with per-pair latencies alone spills and measured
+// slower).
+template <int VAR> struct StreamOcc {
+  static constexpr int value = VAR == kStrSums ? 6 : 4;
+};
 
 template <int VAR>
 __global__ __launch_bounds__(kWgThreads) __attribute__((amdgpu_waves_per_eu(StreamOcc<VAR>::value)))
 void k_stream(EvalParams p) {
-  constexpr int NSLOT = kStreamFieldSlots + ((VAR & kStrMult) ? 1 : 0);
-  __shared__ __attribute__((aligned(16))) uint32_t slot[kWgWaves][NSLOT][kWgRows];
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int n_wgt = p.wgt_off[KS_NFAM];
   const int stride = (int)gridDim.x * kWgWaves;
-  uint32_t(*ws)[kWgRows] = slot[wave];
   int fam = 0;
   for (int wt = (int)blockIdx.x * kWgWaves + wave; wt < n_wgt; wt += stride) {
     const STile tc = stream_locate(p, wt, fam);
@@ -1883,16 +1876,16 @@ void k_stream(EvalParams p) {
       part = p.partial + (size_t)fam * (size_t)p.n_steps * (size_t)p.n_specs;
     }
     switch (fam) {
-      case KS_GEMM: stream_tile<KS_GEMM, VAR>(p, tc, ws, lane, rng, part); break;
-      case KS_LM_HEAD: stream_tile<KS_LM_HEAD, VAR>(p, tc, ws, lane, rng, part); break;
-      case KS_GROUPED_GEMM: stream_tile<KS_GROUPED_GEMM, VAR>(p, tc, ws, lane, rng, part); break;
-      case KS_ATTN_PREFILL: stream_tile<KS_ATTN_PREFILL, VAR>(p, tc, ws, lane, rng, part); break;
-      case KS_ATTN_DECODE: stream_tile<KS_ATTN_DECODE, VAR>(p, tc, ws, lane, rng, part); break;
-      case KS_RMSNORM: stream_tile<KS_RMSNORM, VAR>(p, tc, ws, lane, rng, part); break;
-      case KS_ROPE: stream_tile<KS_ROPE, VAR>(p, tc, ws, lane, rng, part); break;
-      case KS_SILU_MUL: stream_tile<KS_SILU_MUL, VAR>(p, tc, ws, lane, rng, part); break;
-      case KS_KV_WRITE: stream_tile<KS_KV_WRITE, VAR>(p, tc, ws, lane, rng, part); break;
-      default: stream_tile<KS_EMBED, VAR>(p, tc, ws, lane, rng, part); break;
+      case KS_GEMM: stream_tile<KS_GEMM, VAR>(p, tc, lane, rng, part); break;
+      case KS_LM_HEAD: stream_tile<KS_LM_HEAD, VAR>(p, tc, lane, rng, part); break;
+      case KS_GROUPED_GEMM: stream_tile<KS_GROUPED_GEMM, VAR>(p, tc, lane, rng, part); break;
+      case KS_ATTN_PREFILL: stream_tile<KS_ATTN_PREFILL, VAR>(p, tc, lane, rng, part); break;
+      case KS_ATTN_DECODE: stream_tile<KS_ATTN_DECODE, VAR>(p, tc, lane, rng, part); break;
+      case KS_RMSNORM: stream_tile<KS_RMSNORM, VAR>(p, tc, lane, rng, part); break;
+      case KS_ROPE: stream_tile<KS_ROPE, VAR>(p, tc, lane, rng, part); break;
+      case KS_SILU_MUL: stream_tile<KS_SILU_MUL, VAR>(p, tc, lane, rng, part); break;
+      case KS_KV_WRITE: stream_tile<KS_KV_WRITE, VAR>(p, tc, lane, rng, part); break;
+      default: stream_tile<KS_EMBED, VAR>(p, tc, lane, rng, part); break;
     }
   }
 }
@@ -2124,8 +2117,22 @@ static hipError_t launch_stream(const EvalParams &p, hipStream_t s) {
 }
 
 // eta = 1 (no bounded or grid family: those select the head-less kind)
+template <int KIND>
+static hipError_t launch_kind(const EvalParams &p, hipStream_t s);
+
 static hipError_t launch_eta_one(const EvalParams &p, hipStream_t s) {
   if (p.grid_mask || p.bounded_mask) return hipErrorInvalidValue;
+  // the stream addresses the sum slots by 32-bit offsets from the partials:
+  // step sums whose partial and carry regions (carries after partials) span
+  // 4 GiB or more take the one-record-per-lane kernel instead (its
+  // head-less kind without bounded or grid families is eta = 1)
+  if (p.partial) {
+    const bool after = p.carry > p.partial;
+    const uint64_t span = after ? (uint64_t)((const char *)p.carry - (const char *)p.partial) +
+                                      (uint64_t)p.n_tiles * (uint64_t)p.n_specs * sizeof(double)
+                                : ~0ull;
+    if (span >= (1ull << 32)) return launch_kind<kBoundedOnly>(p, s);
+  }
   const bool sums = p.partial && p.range;
   const bool pair = p.o_flops || p.o_bytes || p.o_blocks || p.o_troof || p.o_eta || p.o_t;
   // multiplicities matter only for the step sums
