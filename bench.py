@@ -47,6 +47,11 @@ def _workload(name: str):
     if name == "c1":
         return (gen.config1(), "c1-llama7b: 1000 steps, 2 datasheet specs, fp32 heads", {"specs": 2, "steps": None},
                 [gen.trace_c1()])
+    if name == "c3":
+        wl = gen.config3()
+        return (wl, "c3-mixtral-moe: the whole 200k-step trace (8 experts top-2, Dirichlet(0.5) routing, ragged "
+                    "grouped GEMMs) in one call, 2 datasheet specs, bf16 16-128-128-1 heads",
+                {"specs": 2, "steps": 200}, [])
     if name == "c5-batch":
         wl = gen.config5(0, C5_BATCH_STEPS)
         return (wl, f"c5-70b-prefix: one 64M-record batch (steps 0..{C5_BATCH_STEPS}), 2 datasheet specs, "
@@ -127,6 +132,15 @@ def head_flops_per_pair(in_dim: int, hidden: int) -> int:
     return 2 * (in_dim * hidden + hidden * hidden + hidden)
 
 
+def host_threads() -> int:
+    """Host threads this process may run on (its CPU affinity), i.e. all the
+    host cores the box gives it."""
+    try:
+        return len(os.sched_getaffinity(0))
+    except AttributeError:
+        return os.cpu_count() or 1
+
+
 def cpu_baseline(wl, sample: dict, eta_one: bool, threads: int, bounded=None, grid=None):
     """The oracle as it stands, on a bounded sample of the same workload:
     the first sample["specs"] spec vectors and, if sample["steps"] is set,
@@ -149,6 +163,7 @@ def cpu_baseline(wl, sample: dict, eta_one: bool, threads: int, bounded=None, gr
     pairs = n * len(spec_ids)
     what = f"all {n} records" if rows is None else f"the {n} records of steps 0..{sample['steps']}"
     return {"value": pairs / dt, "unit": "predictions/s", "cores": threads, "kind": "oracle",
+            "os_cpu_count": os.cpu_count(), "pairs": pairs, "seconds": dt,
             "sample": f"{what} x {len(spec_ids)} of {wl.n_specs} spec vectors "
                       f"({pairs} predictions, {dt:.1f} s, fp64 numpy, {threads} BLAS threads)"}
 
@@ -311,12 +326,293 @@ def _sim_cpu_baseline(reqs, h, n):
                       "fp64 numpy latency model per step)"}
 
 
+
+# --------------------------------------------------------------------------
+# sweeps: several evaluation calls per benchmark step
+# --------------------------------------------------------------------------
+FAMILY_FIELDS_USED = FIELDS_USED
+
+
+def layout_stream_bytes(fam_off, n_steps: int, n_prefill: int, n_specs: int, with_mult: bool) -> float:
+    """stream_bytes for the records of a dense decoder's batch expansion,
+    from its family offsets alone: every non-attention family with records
+    has them in every step, the attention records of a step sit in one of
+    the two attention families."""
+    rows = [int(fam_off[f + 1] - fam_off[f]) for f in range(len(fam_off) - 1)]
+    b = float(sum(rows[f] * 4 * (FIELDS_USED[f] + (1 if with_mult else 0)) for f in range(len(rows))))
+    b += 32.0 * n_steps
+    segs = 0
+    for f, r in enumerate(rows):
+        if r == 0:
+            continue
+        segs += n_prefill if f == 3 else (n_steps - n_prefill if f == 4 else n_steps)
+    b += segs * (8.0 + 8.0 * n_specs)
+    return b
+
+
+def _bench_sweep(args) -> int:
+    """c2: the six dense shapes of the six-shape workload (TP 1 to 8), each
+    its whole 100k-step trace in one ks_eval_steps call; c5: the whole
+    500k-step 70B trace in 64M-record step-aligned batches, each expanded
+    on the GPU from its batch descriptors (ks_expand) and evaluated
+    (ks_eval_steps).  One benchmark step is the whole sweep; inputs (records
+    for c2, batch descriptors for c5) are resident in HBM before the timed
+    region.  For c5 a second measurement times the sweep with every batch's
+    descriptors uploaded from pinned host memory on a second stream, each
+    batch's upload overlapping the previous batch's work (not `value`)."""
+    import numpy as np
+    import torch
+    from paper_2606_28565_amd import abi
+    from workload import gen
+
+    stream = abi.current_stream()
+    mode = abi.KS_ETA_ONE if args.eta_one else abi.KS_ETA_MLP
+    parts, keep = [], []
+    if args.workload == "c2":
+        in_dim, hidden = 16, 128
+        for i in range(len(gen.DENSE_SHAPES)):
+            print(f"[bench] c2 shape {gen.DENSE_SHAPES[i].name}", file=sys.stderr, flush=True)
+            wl = gen.config2(i)
+            di = abi.DeviceInputs(wl)
+            heads = di.make_heads("bf16", in_dim, hidden, mode)
+            so_t, so = abi.step_outputs(wl.desc.n_steps, di.n_specs)
+            keep += [so_t]
+            parts.append({"name": gen.DENSE_SHAPES[i].name, "tp": gen.DENSE_SHAPES[i].tp, "di": di, "db": None,
+                          "desc": di.desc, "steps": di.steps, "heads": heads, "so": so, "ws_ptr": di.ws_ptr,
+                          "ws_bytes": di.ws_bytes, "rows": wl.desc.n_rows, "eval_rows": wl.desc.n_rows,
+                          "n_steps": wl.desc.n_steps,
+                          "bytes": stream_bytes(wl, di.n_specs) if args.eta_one else None})
+            del wl
+        n_specs = parts[0]["di"].n_specs
+        wdesc = ("c2-six-shapes: S1..S6 (hidden 2048..8192, 24..80 layers, GQA, TP 1..8), each shape's whole "
+                 "100k-step trace in one call, 2 datasheet specs, bf16 16-128-128-1 heads")
+        specs_ptr, host = None, None
+    else:
+        in_dim, hidden = 32, 256
+        expand_mode = abi.KS_EXPAND_HOMOGENEOUS if args.expand == "homogeneous" else abi.KS_EXPAND_PER_LAYER
+        tr = gen.trace_c5()
+        small = gen.config5(0, 2)
+        di0 = abi.DeviceInputs(small)
+        keep.append(di0)
+        heads = di0.make_heads("bf16", in_dim, hidden, mode)
+        n_specs = di0.n_specs
+        specs_ptr, host = di0.specs_ptr, di0.host
+        bounds = list(range(0, tr.n_steps, C5_BATCH_STEPS)) + [tr.n_steps]
+        per_layer_rows = 0
+        for lo, hi in zip(bounds[:-1], bounds[1:]):
+            print(f"[bench] c5 batch steps {lo}..{hi}", file=sys.stderr, flush=True)
+            sl = tr.slice(lo, hi)
+            db = abi.DeviceBatch(sl, expand_mode)
+            ws_bytes = abi.ks_workspace_bytes(db.desc, n_specs)
+            ws = torch.empty(ws_bytes + 256, dtype=torch.uint8, device="cuda")
+            so_t, so = abi.step_outputs(hi - lo, n_specs)
+            keep += [ws, so_t]
+            n_pre = int(np.count_nonzero(sl.prefill))
+            _, pl = abi.ks_expand_layout(db.model, hi - lo, n_pre, abi.KS_EXPAND_PER_LAYER)
+            per_layer_rows += pl[-1]
+            parts.append({"name": f"steps {lo}..{hi}", "di": None, "db": db, "desc": db.desc, "steps": db.steps,
+                          "heads": heads, "so": so, "ws_ptr": ws.data_ptr() + (-ws.data_ptr()) % 256,
+                          "ws_bytes": ws_bytes, "rows": pl[-1], "eval_rows": db.fam_off[-1], "n_steps": hi - lo,
+                          "bytes": (layout_stream_bytes(db.fam_off, hi - lo, n_pre, n_specs,
+                                                        expand_mode == abi.KS_EXPAND_HOMOGENEOUS)
+                                    if args.eta_one else None),
+                          "trace": sl})
+        del tr
+        wdesc = (f"c5-70b-prefix-full: the whole 500k-step trace in {len(parts)} step-aligned batches of "
+                 f"<= {C5_BATCH_STEPS} steps (64M records), each expanded on the GPU from its batch "
+                 f"descriptors ({'homogeneous' if expand_mode == abi.KS_EXPAND_HOMOGENEOUS else 'per-layer'} "
+                 "records) and evaluated, 2 datasheet specs, bf16 32-256-256-1 heads")
+
+    def run_part(pt, timed_ev=None):
+        if pt["db"] is not None:
+            pt["db"].expand(stream)
+        if timed_ev is not None:
+            abi.ks_set_timing_events(*timed_ev)
+        sp = specs_ptr if pt["di"] is None else pt["di"].specs_ptr
+        hs = host if pt["di"] is None else pt["di"].host
+        abi.ks_eval_steps(pt["desc"], pt["steps"], sp, n_specs, pt["heads"], hs, pt["so"], None,
+                          pt["ws_ptr"], pt["ws_bytes"], stream)
+        if timed_ev is not None:
+            abi.ks_set_timing_events(None, None)
+
+    def step():
+        for pt in parts:
+            run_part(pt)
+
+    print(f"[bench] {len(parts)} calls per step; warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    for pt in parts:
+        abi.ks_device_status(pt["ws_ptr"], pt["ws_bytes"], stream)
+        if pt["db"] is not None:
+            abi.ks_device_status(pt["db"].ws_ptr, pt["db"].ws_bytes, stream)
+    cs = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(cs)
+    for _ in range(args.steps):
+        step()
+    ev1.record(cs)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    print(f"[bench] {args.steps} steps: {ms:.3f} ms/step", file=sys.stderr, flush=True)
+
+    # each call's evaluation kernel (and record writer), from HIP events the
+    # library records around those launches on the stream
+    reps = max(3, min(args.steps, 10))
+    ev = abi.HipEvents(2 * reps * len(parts))
+    try:
+        k = 0
+        for _ in range(reps):
+            for pt in parts:
+                run_part(pt, (ev.ev[k], ev.ev[k + 1]))
+                k += 2
+        torch.cuda.synchronize()
+        for i, pt in enumerate(parts):
+            pt["kernel_ms"] = sum(ev.elapsed_ms(2 * (r * len(parts) + i), 2 * (r * len(parts) + i) + 1)
+                                  for r in range(reps)) / reps
+        if parts[0]["db"] is not None:
+            k = 0
+            for _ in range(reps):
+                for pt in parts:
+                    abi.ks_set_timing_events(ev.ev[k], ev.ev[k + 1])
+                    pt["db"].expand(stream)
+                    abi.ks_set_timing_events(None, None)
+                    k += 2
+            torch.cuda.synchronize()
+            for i, pt in enumerate(parts):
+                pt["expand_ms"] = sum(ev.elapsed_ms(2 * (r * len(parts) + i), 2 * (r * len(parts) + i) + 1)
+                                      for r in range(reps)) / reps
+    finally:
+        abi.ks_set_timing_events(None, None)
+        ev.close()
+    k_ms = sum(pt["kernel_ms"] for pt in parts)
+
+    pcie = None
+    if parts[0]["db"] is not None:
+        pcie = _c5_upload_sweep(parts, run_part, stream, reps)
+
+    dispatch_rows = sum(pt["rows"] for pt in parts)
+    eval_rows = sum(pt["eval_rows"] for pt in parts)
+    pairs = dispatch_rows * n_specs
+    n_steps_total = sum(pt["n_steps"] for pt in parts)
+    if args.eta_one:
+        alg = sum(pt["bytes"] for pt in parts)
+        bound, unit, peak, dtype = "hbm", "GB/s", PEAK["hbm"] / 1e9, "f32"
+        achieved = alg / (k_ms * 1e-3) / 1e9
+    else:
+        alg = float(eval_rows) * n_specs * head_flops_per_pair(in_dim, hidden)
+        bound, unit, peak, dtype = "mfma", "TFLOP/s", PEAK["bf16"] / 1e12, "bf16"
+        achieved = alg / (k_ms * 1e-3) / 1e12
+    out = {
+        "metric": METRIC, "value": pairs / (ms * 1e-3), "unit": "predictions/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": dtype, "data": "synthetic",
+        "config": {"workload": wdesc, "records": dispatch_rows, "evaluated_records": eval_rows,
+                   "spec_vectors": n_specs, "serving_steps": n_steps_total, "calls_per_step": len(parts),
+                   "predictions_per_step": pairs,
+                   "head": "eta=1" if args.eta_one else f"bf16 {in_dim}-{hidden}-{hidden}-1",
+                   "input": ("batch descriptors, expanded on the GPU every step" if parts[0]["db"] is not None
+                             else "kernel records")},
+        "step_evals_per_s": n_steps_total * n_specs / (ms * 1e-3),
+        "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
+                     "traffic": None, "kernel_ms": k_ms,
+                     "note": "achieved = algorithmic work of the sweep's evaluation-kernel launches (head "
+                             "FLOPs over the records evaluated, or the bytes the model reads and writes) / "
+                             "the sum of those kernels' mean durations from HIP events around each launch"},
+        "calls": [{"name": pt["name"], "records": pt["rows"], "kernel_ms": pt["kernel_ms"],
+                   **({"expand_ms": pt["expand_ms"]} if "expand_ms" in pt else {}),
+                   **({"tp": pt["tp"]} if "tp" in pt else {})} for pt in parts],
+    }
+    if pcie is not None:
+        out["pcie_inclusive"] = pcie
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = _sweep_cpu_baseline(args)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def _c5_upload_sweep(parts, run_part, stream, reps):
+    """The c5 sweep with every batch's descriptors (request offsets, query
+    and history tokens, prefill flags) copied from pinned host memory on a
+    second stream: all uploads are queued at once, and each batch's
+    expansion waits for its own upload (an event), so batch b + 1's upload
+    overlaps batch b's work.  Returns the whole-sweep time and the upload
+    bytes; the resident-input figure stays `value`."""
+    import numpy as np
+    import torch
+    host = []
+    nbytes = 0
+    for pt in parts:
+        tr = pt["trace"]
+        arrs = {"req_off": np.ascontiguousarray(tr.req_off, np.uint32).view(np.int32),
+                "req_q": np.ascontiguousarray(tr.req_q, np.uint32).view(np.int32),
+                "req_h": np.ascontiguousarray(tr.req_h, np.uint32).view(np.int32),
+                "prefill": np.ascontiguousarray(tr.prefill, np.uint8)}
+        pin = {k: torch.from_numpy(v).pin_memory() for k, v in arrs.items()}
+        nbytes += sum(v.numel() * v.element_size() for v in pin.values())
+        host.append(pin)
+    copy = torch.cuda.Stream()
+    comp = torch.cuda.current_stream()
+    times = []
+    for _ in range(reps):
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(comp)
+        copy.wait_event(e0)
+        done = []
+        with torch.cuda.stream(copy):
+            for pt, pin in zip(parts, host):
+                for k, v in pin.items():
+                    pt["db"].t[k].copy_(v, non_blocking=True)
+                ev = torch.cuda.Event()
+                ev.record(copy)
+                done.append(ev)
+        for pt, ev in zip(parts, done):
+            comp.wait_event(ev)
+            run_part(pt)
+        e1.record(comp)
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+    return {"ms_per_sweep": sum(times) / len(times), "upload_bytes": nbytes,
+            "note": "whole sweep with the batch descriptors uploaded from pinned host memory on a second "
+                    "stream, overlapped with the previous batch's expansion and evaluation; not `value` "
+                    "(value has the inputs resident in HBM)"}
+
+
+def _sweep_cpu_baseline(args):
+    """The oracle on a bounded sample of the sweep: c2, the records of the
+    first 40 steps of each of the six shapes; c5, those of the first 300
+    steps; every spec vector."""
+    from workload import gen
+    threads = args.cpu_threads or host_threads()
+    if args.workload == "c2":
+        wls = [gen.config2(i, 0, 40) for i in range(len(gen.DENSE_SHAPES))]
+        what = "the records of steps 0..40 of each of the six shapes"
+    else:
+        wls = [gen.config5(0, 300)]
+        what = "the records of steps 0..300"
+    pairs, secs = 0, 0.0
+    for wl in wls:
+        r = cpu_baseline(wl, {"specs": wl.n_specs, "steps": None}, args.eta_one, threads)
+        pairs += r["pairs"]
+        secs += r["seconds"]
+    return {"value": pairs / secs, "unit": "predictions/s", "cores": threads, "kind": "oracle",
+            "os_cpu_count": os.cpu_count(),
+            "sample": f"{what} x 2 spec vectors ({pairs} predictions, {secs:.1f} s, fp64 numpy, "
+                      f"{threads} BLAS threads)"}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=15)
-    ap.add_argument("--workload", default="c4", choices=["c4", "c1", "c5-batch"])
+    ap.add_argument("--workload", default="c4", choices=["c4", "c1", "c3", "c5-batch", "c2", "c5"],
+                    help="c4: the capacity grid (default); c1; c3: the whole MoE trace in one call; c5-batch: "
+                         "one 64M-record batch of the 70B trace; c2: the six dense shapes, each its whole "
+                         "100k-step trace in one call; c5: the whole 500k-step 70B trace in 64M-record "
+                         "batches, each expanded on the GPU from its batch descriptors and evaluated")
     ap.add_argument("--eta-one", action="store_true", help="eta = 1 (pure roofline) mode")
     ap.add_argument("--per-pair", action="store_true",
                     help="also write each pair's latency t_kernel (ks_eval_steps with per-pair outputs)")
@@ -367,6 +663,8 @@ def main() -> int:
 
     if args.simulate:
         return _bench_simulate(args)
+    if args.workload in ("c2", "c5"):
+        return _bench_sweep(args)
 
     print(f"[bench] generating workload {args.workload}", file=sys.stderr, flush=True)
     wl, wdesc, sample, traces = _workload(args.workload)
@@ -556,7 +854,7 @@ def main() -> int:
     if exp is not None:
         out["expand"] = exp
     if not args.no_cpu_baseline:
-        threads = args.cpu_threads or min(16, os.cpu_count() or 1)
+        threads = args.cpu_threads or host_threads()
         print(f"[bench] cpu baseline: oracle on {sample}, {threads} threads", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(wl, sample, args.eta_one, threads, bounded, grid)
         try:
