@@ -36,3 +36,14 @@ def spec(P=2.0 ** 50, BW=2.0 ** 40, n_cu=4, l2=2.0 ** 20, t0=2.0 ** -20,
 def steprec(n_steps, layers=1, hidden=64, tp=1, n_launch=0):
     full = lambda v: np.full(n_steps, v, np.uint32)
     return gen.StepRec(full(layers), full(hidden), full(tp), full(n_launch))
+
+
+def sub_desc(d, rows):
+    """The records `rows` (sorted) of d, with d's request lists and expert
+    table: the oracle then prices only those records."""
+    fam = d.family()[rows]
+    fam_off = np.zeros(gen.NFAM + 1, np.int64)
+    fam_off[1:] = np.cumsum(np.bincount(fam, minlength=gen.NFAM))
+    mult = None if getattr(d, "mult", None) is None else d.mult[rows]
+    return gen.Desc(fam_off, d.step[rows], d.m[rows], d.n[rows], d.k[rows], d.a[rows], d.b[rows],
+                    d.req_off, d.req_q, d.req_h, d.expert_rows, d.elem_bytes, mult)

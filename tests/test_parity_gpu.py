@@ -11,7 +11,7 @@ import torch  # noqa: F401  (runtime loads at collection, not inside a timed tes
 from oracle import ks_oracle as o
 from workload import gen
 from tests import gpu_helpers as g
-from tests.helpers import make_desc, spec, steprec
+from tests.helpers import make_desc, spec, steprec, sub_desc
 from paper_2606_28565_amd import abi
 
 pytestmark = pytest.mark.gpu
@@ -436,14 +436,7 @@ def test_n_cu_above_limit_flagged():
 C5_BATCH_STEPS = 88_640      # steps 0 .. 88,640 of the 70B trace: 63,998,080 records
 
 
-def _sub_desc(d, rows):
-    """The records `rows` (sorted) of d, with d's request lists: the oracle
-    then prices only those records."""
-    fam = d.family()[rows]
-    fam_off = np.zeros(gen.NFAM + 1, np.int64)
-    fam_off[1:] = np.cumsum(np.bincount(fam, minlength=gen.NFAM))
-    return gen.Desc(fam_off, d.step[rows], d.m[rows], d.n[rows], d.k[rows], d.a[rows], d.b[rows],
-                    d.req_off, d.req_q, d.req_h, d.expert_rows, d.elem_bytes)
+_sub_desc = sub_desc
 
 
 def test_max_size_batch_sampled():
