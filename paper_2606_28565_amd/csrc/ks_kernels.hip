@@ -211,7 +211,7 @@ __device__ __forceinline__ Cnt record_counts(int fam, uint32_t m32, uint32_t n32
 // The eta = 1 stream uses it when no per-record count is written: it avoids
 // the 64-bit products and 64-bit to float conversions of the exact path.
 struct CntF {
-  float F, Bt;
+  float F, Bt, M;   // M: the row count of feature x10
   uint64_t B;
 };
 
@@ -221,7 +221,7 @@ __device__ __forceinline__ CntF record_counts_f(int fam, uint32_t m32, uint32_t 
                                                 uint32_t a32, uint32_t b32, uint32_t step,
                                                 const EvalParams &p, uint32_t &bad) {
   const float dt = (float)p.elem_bytes, M = (float)m32, N = (float)n32, K = (float)k32, A = (float)a32;
-  CntF c{0.0f, 0.0f, 0};
+  CntF c{0.0f, 0.0f, M, 0};
   switch (fam) {
     case KS_GEMM:
     case KS_LM_HEAD:
@@ -242,6 +242,7 @@ __device__ __forceinline__ CntF record_counts_f(int fam, uint32_t m32, uint32_t 
         bad |= kErrExpert;
       }
       const float Ms = (float)ms;
+      c.M = Ms;
       c.F = (Ms * N) * (2.0f * K);
       c.Bt = dt * (Ms * K + (float)act * (K * N) + Ms * N);
       c.B = (uint64_t)tiles * ((n32 + 127u) >> 7);
@@ -257,6 +258,7 @@ __device__ __forceinline__ CntF record_counts_f(int fam, uint32_t m32, uint32_t 
         T = p.agg[3 * p.n_steps + step];
       }
       const float NK = N * K;   // exact: N, K < 2^12
+      c.M = u64_to_f32(Q);
       c.F = (4.0f * NK) * u64_to_f32(P);
       c.Bt = dt * (2.0f * NK * u64_to_f32(Q) + (2.0f * A * K) * u64_to_f32(KV));
       c.B = (uint64_t)n32 * T;
@@ -340,12 +342,12 @@ struct RowC {
   float Ff, Btf, Bf, rcp_b, rcp_bt1, la, x0, xs[7];  // la = log2(AI); xs = x8 .. x14
 };
 
-__device__ __forceinline__ RowC row_consts(const Cnt &c, uint32_t n, uint32_t k) {
+__device__ __forceinline__ RowC row_consts(uint64_t B, float Ff, float Btf, float Mf, uint32_t n, uint32_t k) {
   RowC r;
-  r.B = c.B;
-  r.Ff = (float)c.F;
-  r.Btf = (float)c.Bt;
-  r.Bf = (float)c.B;
+  r.B = B;
+  r.Ff = Ff;
+  r.Btf = Btf;
+  r.Bf = (float)B;
   r.rcp_b = rcpf(fmaxf(r.Bf, 1.0f));
   r.rcp_bt1 = rcpf(fmaxf(r.Btf, 1.0f));
   // log2(0) = -inf for F = 0; every use clamps it from below
@@ -353,7 +355,7 @@ __device__ __forceinline__ RowC row_consts(const Cnt &c, uint32_t n, uint32_t k)
   r.x0 = fmaxf(r.la, -10.0f) * (1.0f / 16);
   r.xs[0] = log2f_fast(1.0f + r.Ff) * (1.0f / 64);
   r.xs[1] = log2f_fast(1.0f + r.Btf) * (1.0f / 48);
-  r.xs[2] = log2f_fast(1.0f + (float)c.M) * (1.0f / 24);
+  r.xs[2] = log2f_fast(1.0f + Mf) * (1.0f / 24);
   r.xs[3] = log2f_fast(1.0f + (float)n) * (1.0f / 24);
   r.xs[4] = log2f_fast(1.0f + (float)k) * (1.0f / 24);
   r.xs[5] = log2f_fast(1.0f + r.Ff * r.rcp_b) * (1.0f / 48);
@@ -1323,13 +1325,14 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
     uint32_t bad = 0;
     if ((int64_t)fc.st >= p.n_steps) bad |= kErrStep;
     RowC rc;
-    if (!H::kMlp && !bnd && !grd && !p.o_flops && !p.o_bytes && !p.o_blocks) {
+    // F, Bt and the feature row count in fp32 as they are formed (a few
+    // roundings, within 1e-6 relative of the exact counts) when no count is
+    // written: no 64-bit products or 64-bit to float conversions.  Calls
+    // with a measured grid keep the exact path, so that a record's cell is
+    // the one the exact features give.
+    if (!GRID && !p.o_flops && !p.o_bytes && !p.o_blocks) {
       const CntF cf = record_counts_f(fam, fc.m, fc.n, fc.k, fc.a, fc.b, fc.st, p, bad);
-      rc.B = cf.B;
-      rc.Ff = cf.F;
-      rc.Btf = cf.Bt;
-      rc.Bf = (float)cf.B;
-      rc.rcp_b = rcpf(fmaxf(rc.Bf, 1.0f));
+      rc = row_consts(cf.B, cf.F, cf.Bt, cf.M, fc.n, fc.k);
     } else {
       const Cnt c = record_counts(fam, fc.m, fc.n, fc.k, fc.a, fc.b, fc.st, p, bad);
       if (valid) {
@@ -1337,7 +1340,7 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
         if (p.o_bytes) p.o_bytes[row] = c.Bt;
         if (p.o_blocks) p.o_blocks[row] = c.B;
       }
-      rc = row_consts(c, fc.n, fc.k);
+      rc = row_consts(c.B, (float)c.F, (float)c.Bt, (float)c.M, fc.n, fc.k);
     }
     if (valid && bad) atomicOr(p.err, bad);
     const bool live = valid && !(bad & kErrStep);
@@ -1406,8 +1409,11 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
         }
         float zp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
         float tr_prev = 0.0f, t0_prev = 0.0f;
-        for (int s = 0; s < S; ++s) {
-          const SpecC sn = spec_at(p.spec_c, s + 1 < S ? s + 1 : s);
+        // one spec's groups; NEXT: whether a next spec exists (the last
+        // spec's groups are a second copy without the next spec's work)
+        auto spec_iter = [&](int s, auto next_c) {
+          constexpr bool NEXT = decltype(next_c)::value;
+          const SpecC sn = spec_at(p.spec_c, NEXT ? s + 1 : s);
           Roof on;
           u32x4 XBn[2][1];
           float xn[IN];
@@ -1429,16 +1435,16 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
                 spec_tail<MULT>(p, s - 1, tr_prev, eta_prev, fmaxf(tr_prev * eta_prev, t0_prev), valid, live, row,
                                 tfac, fac, dst);
             }
-            if constexpr (I == 20) on = small ? roofline<true>(rc, sn) : roofline<false>(rc, sn);
-            if constexpr (I == 22) {
+            if constexpr (NEXT && I == 20) on = small ? roofline<true>(rc, sn) : roofline<false>(rc, sn);
+            if constexpr (NEXT && I == 22) {
 #pragma unroll
               for (int i = 1; i < 4; ++i) xn[i] = feature<H::kRaw>(i, rc, sn, on);
             }
-            if constexpr (I == 24) {
+            if constexpr (NEXT && I == 24) {
 #pragma unroll
               for (int i = 4; i < 8; ++i) xn[i] = feature<H::kRaw>(i, rc, sn, on);
             }
-            if constexpr (I == 28) {
+            if constexpr (NEXT && I == 28) {
               xn[0] = feature<H::kRaw>(0, rc, sn, on);
 #pragma unroll
               for (int i = 8; i < 16; ++i) xn[i] = feature<H::kRaw>(i, rc, sn, on);
@@ -1448,11 +1454,15 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
           H::run_groups(st, lds, hook);
           tr_prev = tr_cur;
           t0_prev = t0_cur;
-          o = on;
-          sc = sn;
-          XB[0][0] = XBn[0][0];
-          XB[1][0] = XBn[1][0];
-        }
+          if constexpr (NEXT) {
+            o = on;
+            sc = sn;
+            XB[0][0] = XBn[0][0];
+            XB[1][0] = XBn[1][0];
+          }
+        };
+        for (int s = 0; s + 1 < S; ++s) spec_iter(s, std::true_type{});
+        spec_iter(S - 1, std::false_type{});
         // the last spec's epilogue and tail
         float zl[4];
 #pragma unroll

@@ -43,7 +43,15 @@ def _sampled_check(wl, seed):
     gpu = {k: ko_t[k][:, rows_t].cpu().numpy() for k in ("t_roof", "eta", "t_kernel")}
     cnt = {k: ko_t[k][rows_t].cpu().numpy().view(np.uint64) for k in ("flops", "bytes", "blocks")}
     step_out = {k: so_t[k].cpu().numpy()[:, steps] for k in ("t_body", "t_gpu", "t_step")}
-    del ko_t, so_t, di
+    del ko_t
+    # the benchmark's launch: step outputs only (no per-pair or count
+    # outputs, so F, Bt and the row-count feature are formed in fp32)
+    abi.ks_eval_steps(di.desc, di.steps, di.specs_ptr, di.n_specs, di.heads, di.host, so, None,
+                      di.ws_ptr, di.ws_bytes, abi.current_stream())
+    torch.cuda.synchronize()
+    abi.ks_device_status(di.ws_ptr, di.ws_bytes, abi.current_stream())
+    bench_out = {k: so_t[k].cpu().numpy()[:, steps] for k in ("t_body", "t_gpu", "t_step")}
+    del so_t, di
     torch.cuda.empty_cache()
 
     sd = sub_desc(d, rows)
@@ -68,6 +76,8 @@ def _sampled_check(wl, seed):
     for k in ("t_body", "t_gpu", "t_step"):
         assert g.rel_err(step_out[k], ge[k][:, steps]).max() <= REL, k
         assert g.rel_err(step_out[k], e2e[k][:, steps]).max() <= REL_BF16, k
+        assert g.rel_err(bench_out[k], e2e[k][:, steps]).max() <= REL_BF16, k
+        assert g.rel_err(bench_out[k], step_out[k]).max() <= REL_BF16, k
 
 
 @pytest.mark.parametrize("shape_idx", range(6))

@@ -143,10 +143,13 @@ def test_c1_deterministic():
 
 
 # ------------------------------------------------------------ bf16 heads ----
-def _bf16_case(wl, n_specs=None):
+def _bf16_case(wl, n_specs=None, counts=True):
+    """counts=False: no per-record counts written, so the kernel forms F, Bt
+    and the row-count feature in fp32 (the path of calls without count
+    outputs, e.g. the benchmark's)."""
     n_specs = n_specs or wl.n_specs
     ref = o.eval_kernels(wl.desc, wl.specs, wl.heads, spec_ids=range(n_specs))
-    gpu = g.eval_steps(wl, n_specs=n_specs)
+    gpu = g.eval_steps(wl, n_specs=n_specs, counts=counts)
     _check_kernels(wl, gpu, ref, bf16=True)
     rs = o.eval_steps(wl.desc, wl.steps, wl.specs, wl.host, wl.heads, spec_ids=range(n_specs), kern=ref)
     _check_steps(wl, gpu, rs, bf16=True, n_specs=n_specs)
@@ -175,17 +178,20 @@ def test_spec_loop_counts_for_the_16_128_head(n_specs):
             np.testing.assert_array_equal(gpu[k][:n_specs - 1], fewer[k], err_msg=k)
 
 
-def test_c3_moe_subset():
-    _bf16_case(gen.config3(0, 30))
+@pytest.mark.parametrize("counts", [True, False])
+def test_c3_moe_subset(counts):
+    _bf16_case(gen.config3(0, 30), counts=counts)
 
 
-def test_c5_subset_bf16_32_256():
-    _bf16_case(gen.config5(0, 24))
+@pytest.mark.parametrize("counts", [True, False])
+def test_c5_subset_bf16_32_256(counts):
+    _bf16_case(gen.config5(0, 24), counts=counts)
 
 
 @pytest.mark.parametrize("shape_idx", range(6))
-def test_c2_shape_subsets_with_tp(shape_idx):
-    _bf16_case(gen.config2(shape_idx, 0, 12))
+@pytest.mark.parametrize("counts", [True, False])
+def test_c2_shape_subsets_with_tp(shape_idx, counts):
+    _bf16_case(gen.config2(shape_idx, 0, 12), counts=counts)
 
 
 def test_c4_full_size_sampled():
@@ -219,11 +225,14 @@ KINDS = [("f32", 16, 64), ("f32", 16, 128), ("f32", 32, 64), ("f32", 32, 128),
 
 
 @pytest.mark.parametrize("precision,in_dim,hidden", KINDS)
-def test_every_head_kind(precision, in_dim, hidden):
+@pytest.mark.parametrize("counts", [True, False])
+def test_every_head_kind(precision, in_dim, hidden, counts):
+    """counts=False: the fp32 count path (no per-record count output)."""
     wl = gen.config1(0, 6).with_heads(gen.make_heads(in_dim, hidden, precision))
     ref = o.eval_kernels(wl.desc, wl.specs, wl.heads)
-    gpu = g.eval_kernels(wl)
+    gpu = g.eval_kernels(wl, counts=counts)
     _check_kernels(wl, gpu, ref, bf16=precision == "bf16")
+    assert ("flops" in gpu) == counts
 
 
 @pytest.mark.parametrize("precision,in_dim,hidden", KINDS)
