@@ -1533,7 +1533,28 @@ static_assert(kTileRows == 16 * kStreamR, "a 64-record tile is one 16-lane row")
 
 // what a launch of the stream computes: step sums, per-pair outputs, and
 // whether records carry multiplicities (step sums only)
-enum : int { kStrSums = 1, kStrPair = 2, kStrMult = 4 };
+enum : int { kStrSums = 1, kStrPair = 2, kStrMult = 4, kStrBnd = 8 };
+
+// The bounded analytical head in the stream (families with their bounded
+// bit; the others keep eta = 1).  Its two logits g . x and a . x are split
+// into the spec-independent features (x0, x8 .. x15: one partial sum per
+// record and logit, formed once per tile) and the spec-dependent ones (x1 ..
+// x7, per spec); the parameters are read through the scalar cache.
+struct SBnd {
+  float zg[kStreamR], za[kStreamR];   // g . x and a . x over x0, x8 .. x15
+  float la[kStreamR];                 // log2(F / max(Bt, 1))
+  float bf[kStreamR];                 // B
+  float rbt[kStreamR];                // 1 / max(Bt, 1)
+};
+
+__device__ __forceinline__ float bnd_param(const float *base, int i) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  typedef const __attribute__((address_space(4))) float *CPtr;
+  return ((CPtr)base)[i];
+#else
+  return base[i];
+#endif
+}
 
 // fields a family's counts read besides step and n
 constexpr bool uses_m(int fam) {
@@ -1659,17 +1680,18 @@ __device__ __forceinline__ void store_quad(float *base, int lane, int nvalid, co
 // 32-bit byte offsets r.off (the launcher takes this kernel for step sums
 // only when the partial and carry regions span less than 4 GiB), so a spec
 // costs no per-lane address arithmetic.
-template <int VAR, class BH>
+template <int VAR, bool BND, class BH>
 __device__ __forceinline__ void stream_specs(const EvalParams &p, const STile &tc, int lane, const SRec &r,
                                              const BH (&bh)[kStreamR], const float (&frb)[kStreamR],
-                                             const float (&btf)[kStreamR], double *part, bool any_tail) {
+                                             const float (&btf)[kStreamR], double *part, bool any_tail,
+                                             const SBnd &q, const float *prm) {
   constexpr bool SUMS = (VAR & kStrSums) != 0, PAIR = (VAR & kStrPair) != 0, MULT = (VAR & kStrMult) != 0;
   const size_t S = (size_t)p.n_specs;
   const size_t n_rows = (size_t)p.fam_off[KS_NFAM];
   for (int s = 0; s < p.n_specs; ++s) {
     const SpecC sc = spec_at(p.spec_c, s);
     const float np = sc.n_f * sc.rcp_p;
-    float t[kStreamR], tr[kStreamR];
+    float t[kStreamR], tr[kStreamR], eta[kStreamR];
 #pragma unroll
     for (int j = 0; j < kStreamR; ++j) {
       float W;
@@ -1677,16 +1699,41 @@ __device__ __forceinline__ void stream_specs(const EvalParams &p, const STile &t
         W = ceilf(bh[j] * sc.rcp_n);
       else
         W = (float)ceil(bh[j] * sc.rcp_nd);
-      tr[j] = fmaxf(W * (frb[j] * np), btf[j] * sc.rcp_bw);
-      t[j] = fmaxf(tr[j], sc.t0);
+      const float tc_ = W * (frb[j] * np), tm = btf[j] * sc.rcp_bw;
+      tr[j] = fmaxf(tc_, tm);
+      if constexpr (BND) {
+        // x1 .. x7 of this spec (Sec. 5.3 feature list; u = W N / B, and
+        // a record without blocks has u = 1), then the bounded head
+#pragma clang fp contract(off)
+        const float u = q.bf[j] > 0.0f ? W * sc.n_f * rcpf(q.bf[j]) : 1.0f;
+        float x[8];
+        x[1] = fmaxf(q.la[j] + sc.lr, -20.0f) * (1.0f / 16);
+        x[2] = log2f_fast(fmaf(q.bf[j], sc.rcp_n, 1.0f)) * (1.0f / 16);
+        x[3] = rcpf(u);
+        x[4] = log2f_fast(1.0f + W) * (1.0f / 16);
+        x[5] = fminf(1.0f, sc.l2 * q.rbt[j]);
+        x[6] = log2f_fast(fmaxf(tr[j] * sc.rcp_t0, 0x1p-20f)) * (1.0f / 16);
+        const float den = tc_ + tm;
+        x[7] = den > 0.0f ? tc_ * rcpf(den) : 0.0f;
+        float zg = q.zg[j], za = q.za[j];
+#pragma unroll
+        for (int i = 1; i < 8; ++i) {
+          zg = fmaf(bnd_param(prm, i), x[i], zg);
+          za = fmaf(bnd_param(prm, 16 + i), x[i], za);
+        }
+        const float w = fmaxf(W, 1.0f);
+        const float eg = __expf(-zg), ea = __expf(-za);
+        eta[j] = (1.0f + eg) * (w * (1.0f + ea)) * rcpf((w - 1.0f) + w * ea);
+        t[j] = fmaxf(tr[j] * eta[j], sc.t0);
+      } else {
+        eta[j] = 1.0f;
+        t[j] = fmaxf(tr[j], sc.t0);
+      }
     }
     if constexpr (PAIR) {
       const size_t i0 = (size_t)s * n_rows + (size_t)tc.row0;
       if (p.o_troof) store_quad(p.o_troof + i0, lane, tc.nvalid, tr);
-      if (p.o_eta) {
-        const float one[kStreamR] = {1.0f, 1.0f, 1.0f, 1.0f};
-        store_quad(p.o_eta + i0, lane, tc.nvalid, one);
-      }
+      if (p.o_eta) store_quad(p.o_eta + i0, lane, tc.nvalid, eta);
       if (p.o_t) store_quad(p.o_t + i0, lane, tc.nvalid, t);
     }
     if constexpr (SUMS) {
@@ -1755,7 +1802,7 @@ __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc
   bool live[kStreamR];
   bool big = false;
   uint64_t B[kStreamR];
-  float Ff[kStreamR], Btf[kStreamR];
+  float Ff[kStreamR], Btf[kStreamR], Mf[kStreamR];
   // a step at or past n_steps (none can be when n_steps >= 2^32)
   const bool lim = p.n_steps <= (int64_t)UINT32_MAX;
   const uint32_t n_steps32 = (uint32_t)p.n_steps;
@@ -1776,11 +1823,13 @@ __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc
       B[j] = c.B;
       Ff[j] = (float)c.F;
       Btf[j] = (float)c.Bt;
+      Mf[j] = (float)c.M;
     } else {
       const CntF cf = record_counts_f(FAM, v[1][j], v[2][j], v[3][j], v[4][j], v[5][j], v[0][j], p, b);
       B[j] = cf.B;
       Ff[j] = cf.F;
       Btf[j] = cf.Bt;
+      Mf[j] = cf.M;
     }
     if (valid) bad |= b;
     live[j] = valid && !(b & kErrStep);
@@ -1840,6 +1889,44 @@ __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc
     r.g[2] = dpp_key<0x114, 0xf, 0xe>(kl) == kl ? 1.0f : 0.0f;
     r.g[3] = dpp_key<0x118, 0xf, 0xc>(kl) == kl ? 1.0f : 0.0f;
   }
+  // the bounded head's spec-independent part (families with their bit set)
+  SBnd q;
+  const float *prm = nullptr;
+  const bool bnd = (VAR & kStrBnd) != 0 && ((p.bounded_mask >> FAM) & 1u);   // wave-uniform
+  if constexpr ((VAR & kStrBnd) != 0) {
+    if (bnd) {
+      prm = p.bounded + FAM * 32;
+#pragma unroll
+      for (int j = 0; j < kStreamR; ++j) {
+#pragma clang fp contract(off)
+        const float bf = (float)B[j];
+        const float rb = rcpf(fmaxf(bf, 1.0f));
+        q.bf[j] = bf;
+        q.rbt[j] = rcpf(fmaxf(Btf[j], 1.0f));
+        // log2(0) = -inf for F = 0; the clamps of x0 and x1 take it
+        q.la[j] = log2f_fast(Ff[j] * q.rbt[j]);
+        float xi[9];
+        xi[0] = fmaxf(q.la[j], -10.0f) * (1.0f / 16);
+        xi[1] = log2f_fast(1.0f + Ff[j]) * (1.0f / 64);
+        xi[2] = log2f_fast(1.0f + Btf[j]) * (1.0f / 48);
+        xi[3] = log2f_fast(1.0f + Mf[j]) * (1.0f / 24);
+        xi[4] = log2f_fast(1.0f + (float)v[2][j]) * (1.0f / 24);
+        xi[5] = log2f_fast(1.0f + (float)v[3][j]) * (1.0f / 24);   // 0 for the families without K
+        xi[6] = log2f_fast(1.0f + Ff[j] * rb) * (1.0f / 48);
+        xi[7] = log2f_fast(1.0f + Btf[j] * rb) * (1.0f / 40);
+        xi[8] = 1.0f;
+        // x0, x8 .. x15 of the feature list: parameter indices 0, 8 .. 15
+        float zg = bnd_param(prm, 0) * xi[0], za = bnd_param(prm, 16) * xi[0];
+#pragma unroll
+        for (int i = 1; i < 9; ++i) {
+          zg = fmaf(bnd_param(prm, 7 + i), xi[i], zg);
+          za = fmaf(bnd_param(prm, 23 + i), xi[i], za);
+        }
+        q.zg[j] = zg;
+        q.za[j] = za;
+      }
+    }
+  }
   float frb[kStreamR];
   if (small) {
     float bh[kStreamR];
@@ -1849,7 +1936,10 @@ __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc
       bh[j] = Bf - 0.5f;
       frb[j] = Ff[j] * rcpf(fmaxf(Bf, 1.0f));
     }
-    stream_specs<VAR>(p, tc, lane, r, bh, frb, Btf, part, any_tail);
+    if (bnd)
+      stream_specs<VAR, (VAR & kStrBnd) != 0>(p, tc, lane, r, bh, frb, Btf, part, any_tail, q, prm);
+    else
+      stream_specs<VAR, false>(p, tc, lane, r, bh, frb, Btf, part, any_tail, q, prm);
   } else {
     double bh[kStreamR];
 #pragma unroll
@@ -1857,7 +1947,10 @@ __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc
       bh[j] = (double)B[j] - 0.5;
       frb[j] = Ff[j] * rcpf(fmaxf((float)B[j], 1.0f));
     }
-    stream_specs<VAR>(p, tc, lane, r, bh, frb, Btf, part, any_tail);
+    if (bnd)
+      stream_specs<VAR, (VAR & kStrBnd) != 0>(p, tc, lane, r, bh, frb, Btf, part, any_tail, q, prm);
+    else
+      stream_specs<VAR, false>(p, tc, lane, r, bh, frb, Btf, part, any_tail, q, prm);
   }
 }
 
@@ -1866,7 +1959,8 @@ __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc
 // (asking for seven with per-pair latencies alone spills and measured
 // slower).
 template <int VAR> struct StreamOcc {
-  static constexpr int value = VAR == kStrSums ? 6 : 4;
+  static constexpr int value =
+      VAR == kStrSums ? 6 : ((VAR & kStrBnd) && (VAR & kStrSums) && (VAR & kStrPair) ? 3 : 4);
 };
 
 template <int VAR>
@@ -2101,7 +2195,7 @@ static hipError_t launch_grid(const EvalParams &p, hipStream_t s) {
 // with or without multiplicities); grid-stride over workgroup tiles, one
 // per wave.  As many workgroups as are resident, cached per device and
 // variant.
-constexpr int kNumStreamVars = 8;
+constexpr int kNumStreamVars = 16;
 static std::atomic<int> g_stream_resident[kMaxDevices][kNumStreamVars];
 
 template <int VAR>
@@ -2152,6 +2246,26 @@ static hipError_t launch_eta_one(const EvalParams &p, hipStream_t s) {
   return pair ? launch_stream<kStrSums | kStrPair>(p, s) : launch_stream<kStrSums>(p, s);
 }
 
+// no MLP family and no grid: the bounded families and eta = 1 for the rest,
+// on the stream (same 4 GiB condition for the sum slots)
+static hipError_t launch_bounded_stream(const EvalParams &p, hipStream_t s) {
+  if (p.partial) {
+    const bool after = p.carry > p.partial;
+    const uint64_t span = after ? (uint64_t)((const char *)p.carry - (const char *)p.partial) +
+                                      (uint64_t)p.n_tiles * (uint64_t)p.n_specs * sizeof(double)
+                                : ~0ull;
+    if (span >= (1ull << 32)) return launch_kind<kBoundedOnly>(p, s);
+  }
+  const bool sums = p.partial && p.range;
+  const bool pair = p.o_flops || p.o_bytes || p.o_blocks || p.o_troof || p.o_eta || p.o_t;
+  const bool mult = sums && p.mult;
+  constexpr int B = kStrBnd;
+  if (!sums) return launch_stream<B | kStrPair>(p, s);
+  if (mult)
+    return pair ? launch_stream<B | kStrSums | kStrPair | kStrMult>(p, s) : launch_stream<B | kStrSums | kStrMult>(p, s);
+  return pair ? launch_stream<B | kStrSums | kStrPair>(p, s) : launch_stream<B | kStrSums>(p, s);
+}
+
 template <int KIND>
 static hipError_t launch_kind(const EvalParams &p, hipStream_t s) {
   // multiplicities matter only for the step sums
@@ -2165,7 +2279,7 @@ hipError_t launch_eval(int kind, const EvalParams &p, hipStream_t s) {
   if (p.wgt_off[KS_NFAM] == 0) return hipSuccess;
   switch (kind) {
     case kEtaOne: return launch_eta_one(p, s);
-    case kBoundedOnly: return launch_kind<kBoundedOnly>(p, s);
+    case kBoundedOnly: return p.grid_mask ? launch_kind<kBoundedOnly>(p, s) : launch_bounded_stream(p, s);
     case kF32_16_64: return launch_kind<kF32_16_64>(p, s);
     case kF32_16_128: return launch_kind<kF32_16_128>(p, s);
     case kF32_32_64: return launch_kind<kF32_32_64>(p, s);

@@ -421,6 +421,37 @@ def _block_count_workload(heads=None):
     return _wl(d, 1, specs=_multi_spec(n_cus), heads=heads)
 
 
+def _stream_block_count_workload():
+    """SiLU block counts k N - 1, k N and k N + 1 just below 2^22 for every
+    CU count, all in the first 256-record tile (so the stream's fp32 wave
+    count, exact below 2^22, takes them), then a tile with counts from
+    2^22 - 1 up (its fp64 path)."""
+    n_cus = [148, 132, 256, 97, 1, 65535]
+    near = []
+    for n in n_cus:
+        k = ((1 << 22) - 2) // n
+        near += [v for v in (k * n - 1, k * n, k * n + 1) if v < (1 << 22)]
+    rows = [(gen.SILU_MUL, 0, v, 1024, 0, 0, 0) for v in near]
+    rows += [(gen.SILU_MUL, 0, 1000 + i, 1024, 0, 0, 0) for i in range(256 - len(rows))]
+    rows += [(gen.SILU_MUL, 0, v, 1024, 0, 0, 0)
+             for v in ((1 << 22) - 1, 1 << 22, (1 << 22) + 1, (1 << 23) + 1, (1 << 24) - 1)]
+    d = make_desc(rows, [[(1, 1)]])
+    return _wl(d, 1, specs=_multi_spec(n_cus))
+
+
+@pytest.mark.parametrize("bounded", [False, True])
+def test_stream_wave_count_just_below_2_22(bounded):
+    wl = _stream_block_count_workload()
+    bd = gen.make_bounded(gen.BOUNDED_ALL) if bounded else None
+    ref = o.eval_kernels(wl.desc, wl.specs, None, eta_one=True, bounded=bd)
+    rs = o.eval_steps(wl.desc, wl.steps, wl.specs, wl.host, eta_one=True, kern=ref)
+    steps_only = g.eval_steps(wl, eta_one=True, per_pair=False, bounded=bd)
+    _check_steps(wl, steps_only, rs, bf16=False, n_specs=wl.n_specs)
+    gpu = g.eval_steps(wl, eta_one=True, counts=False, bounded=bd)
+    for k, r in (("t_roof", "t_roof"), ("eta", "eta"), ("t_kernel", "t")):
+        assert g.rel_err(gpu[k], ref[r]).max() <= REL, k
+
+
 def test_block_counts_around_the_fp32_wave_path():
     wl = _block_count_workload()
     b = o.kernel_counts(wl.desc)["B"]
@@ -562,15 +593,17 @@ def test_unused_k_fields_are_ignored(precision, in_dim, hidden):
 
 
 # -------------------------------------------------- bounded analytical head --
-def _bounded_case(wl, bd, eta_one=False, n_specs=None, null_mlp=False):
+def _bounded_case(wl, bd, eta_one=False, n_specs=None, null_mlp=False, counts=True):
     """Families in bd.mask: fp32 bounded head at 1e-5; the others keep the
-    MLP bar of their precision (or eta = 1 exactly)."""
+    MLP bar of their precision (or eta = 1 exactly).  counts=False: no
+    per-record count outputs (F and Bt formed in fp32)."""
     n_specs = n_specs or wl.n_specs
     heads = None if eta_one else wl.heads
     ref = o.eval_kernels(wl.desc, wl.specs, heads, eta_one=eta_one, spec_ids=range(n_specs), bounded=bd)
-    gpu = g.eval_steps(wl, eta_one=eta_one, n_specs=n_specs, bounded=bd, null_mlp=null_mlp)
+    gpu = g.eval_steps(wl, eta_one=eta_one, n_specs=n_specs, bounded=bd, null_mlp=null_mlp, counts=counts)
     c = ref["counts"]
-    np.testing.assert_array_equal(gpu["flops"], c["F"])
+    if counts:
+        np.testing.assert_array_equal(gpu["flops"], c["F"])
     assert g.rel_err(gpu["t_roof"], ref["t_roof"]).max() <= REL
     on = ((bd.mask >> wl.desc.family()) & 1).astype(bool)
     assert g.rel_err(gpu["eta"][:, on], ref["eta"][:, on]).max() <= REL
@@ -603,8 +636,31 @@ def test_bounded_only():
     bd = gen.make_bounded(gen.BOUNDED_ALL)
     _bounded_case(wl, bd, eta_one=True)
     _bounded_case(wl, bd, null_mlp=True)
+    _bounded_case(wl, bd, eta_one=True, counts=False)
     # some families bounded, the rest at eta = 1
     _bounded_case(wl, gen.make_bounded(gen.BOUNDED_MIXED), eta_one=True)
+    _bounded_case(wl, gen.make_bounded(gen.BOUNDED_MIXED), eta_one=True, counts=False)
+
+
+@pytest.mark.parametrize("seed,n_steps,max_run,n_specs", [(1, 40, 9, 1), (3, 30, 300, 5), (4, 400, 200, 2)])
+@pytest.mark.parametrize("mask", [gen.BOUNDED_ALL, gen.BOUNDED_MIXED])
+def test_bounded_stream_step_sums_runs_at_every_offset(seed, n_steps, max_run, n_specs, mask):
+    """Calls without an MLP family take the stream (four records per lane)
+    with the bounded head on its families: step sums alone, and with
+    per-pair outputs, against the oracle over runs ending at every lane,
+    row and tile offset."""
+    wl = _run_workload(seed, n_steps, max_run, n_specs)
+    bd = gen.make_bounded(mask)
+    ref = o.eval_kernels(wl.desc, wl.specs, None, eta_one=True, bounded=bd)
+    rs = o.eval_steps(wl.desc, wl.steps, wl.specs, wl.host, eta_one=True, kern=ref)
+    steps_only = g.eval_steps(wl, eta_one=True, per_pair=False, bounded=bd)
+    _check_steps(wl, steps_only, rs, bf16=False, n_specs=wl.n_specs)
+    per_pair = g.eval_steps(wl, eta_one=True, counts=False, bounded=bd)
+    assert g.rel_err(per_pair["eta"], ref["eta"]).max() <= REL
+    assert g.rel_err(per_pair["t_kernel"], ref["t"]).max() <= REL
+    assert g.rel_err(per_pair["t_roof"], ref["t_roof"]).max() <= REL
+    for key in ("t_body", "t_gpu", "t_step"):
+        assert g.rel_err(steps_only[key], per_pair[key]).max() <= 2 * REL
 
 
 def test_bounded_with_block_counts_around_2_23():
