@@ -90,6 +90,25 @@ def recorded_traffic(key: str):
     return rec["hbm_bytes_per_launch"]
 
 
+def traffic_key(args) -> str:
+    """The traffic.json entry of a benchmark configuration (the flags that
+    change the evaluation kernel or its inputs)."""
+    k = args.workload
+    if getattr(args, "eta_one", False):
+        k += "-eta1"
+    if getattr(args, "kernels", False):
+        k += "-kernels"
+    elif getattr(args, "per_pair", False):
+        k += "-pair"
+    if getattr(args, "bounded", "none") != "none":
+        k += "-bounded-" + args.bounded
+    if getattr(args, "grid", "none") != "none":
+        k += "-grid-" + args.grid
+    if getattr(args, "expand", "none") != "none":
+        k += "-expand-" + args.expand
+    return k
+
+
 def copy_calibration(nbytes: int, reps: int) -> None:
     """A plain device-to-device copy of nbytes, reps times: the reference
     whose FETCH_SIZE / WRITE_SIZE counters scale the evaluation kernel's."""
@@ -516,10 +535,11 @@ def _bench_sweep(args) -> int:
                              else "kernel records")},
         "step_evals_per_s": n_steps_total * n_specs / (ms * 1e-3),
         "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
-                     "traffic": None, "kernel_ms": k_ms,
+                     "traffic": recorded_traffic(traffic_key(args)), "kernel_ms": k_ms,
                      "note": "achieved = algorithmic work of the sweep's evaluation-kernel launches (head "
                              "FLOPs over the records evaluated, or the bytes the model reads and writes) / "
-                             "the sum of those kernels' mean durations from HIP events around each launch"},
+                             "the sum of those kernels' mean durations from HIP events around each launch; "
+                             "traffic = HBM bytes of those launches per sweep (counters)"},
         "calls": [{"name": pt["name"], "records": pt["rows"], "kernel_ms": pt["kernel_ms"],
                    **({"expand_ms": pt["expand_ms"]} if "expand_ms" in pt else {}),
                    **({"tp": pt["tp"]} if "tp" in pt else {})} for pt in parts],
@@ -842,9 +862,7 @@ def main() -> int:
         "step_evals_per_s": step_evals,
         "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
                      "frac": achieved / peak if achieved is not None else None,
-                     "traffic": (recorded_traffic(f"{args.workload}{'-eta1' if args.eta_one else ''}"
-                                                  f"{'-kernels' if args.kernels else ('-pair' if args.per_pair else '')}")
-                                 if not bmask and db is None and grid is None else None),
+                     "traffic": recorded_traffic(traffic_key(args)),
                      "kernel_ms": k_ms, "evaluated_records": n_eval,
                      "note": "achieved = algorithmic work of one evaluation-kernel launch (FLOPs of the "
                              "head over the records it evaluates, or the bytes the model reads and "
