@@ -213,6 +213,8 @@ void fill_eval(ks::EvalParams &p, const ks_desc *d, const ks_spec *specs, int32_
     p.wgt_off[f] = t.wgt_off[f];
   }
   p.n_tiles = t.tile_off[KS_NFAM];
+  p.spec_chunk = n_specs;
+  p.n_chunks = 1;
   p.bounded_mask = h->bounded_mask;
   p.bounded = h->bounded_mask ? h->bounded : nullptr;
   p.grid_mask = h->grid_mask;

@@ -61,6 +61,10 @@ struct EvalParams {
   int32_t tile_off[KS_NFAM + 1];   // wave-tile offsets per family
   int32_t wgt_off[KS_NFAM + 1];    // workgroup-tile offsets per family
   int32_t n_tiles;
+  // work items: every workgroup tile once per spec range of spec_chunk
+  // specs (n_chunks ranges; one range of all specs unless the record tiles
+  // alone would not fill the GPU)
+  int32_t spec_chunk, n_chunks;
   // heads
   const void *w1, *w2, *b2, *w3, *b3;
   uint32_t bounded_mask;       // families that take the bounded analytical head

@@ -1278,24 +1278,28 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
   __shared__ float bnd_lds[32];   // the bounded head of the staged family: g then a
   __shared__ float grid_lds[KS_GRID_MAX_NODES];   // the staged family's measured grid
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int n_wgt = p.wgt_off[KS_NFAM];
+  // work item w: workgroup tile w / n_chunks, specs [s0, s1) of range w % n_chunks
+  const int n_chunks = p.n_chunks;
+  const int n_work = p.wgt_off[KS_NFAM] * n_chunks;
   int staged = -1;
   // the next tile's fields are loaded while the current one is evaluated
   Tile tn = {};
   Fields fn = {0, 0, 0, 0, 0, 0, kNoKey, kNoKey, kNoKey, 1.0f};
   // tiles without a head take their neighbour steps by a vector load
   constexpr bool VEC = !H::kMlp;
-  if ((int)blockIdx.x < n_wgt) {
-    tn = locate(p, blockIdx.x, wave, 0);
+  if ((int)blockIdx.x < n_work) {
+    tn = locate(p, (int)blockIdx.x / n_chunks, wave, 0);
     fn = load_fields<MULT, VEC>(p, tn, lane);
   }
-  for (int wt = blockIdx.x; wt < n_wgt; wt += gridDim.x) {
+  for (int w = blockIdx.x; w < n_work; w += gridDim.x) {
     const Tile tc = tn;
     const Fields fc = fn;
-    if (wt + (int)gridDim.x < n_wgt) {
-      tn = locate(p, wt + gridDim.x, wave, tc.fam);
+    if (w + (int)gridDim.x < n_work) {
+      tn = locate(p, (w + (int)gridDim.x) / n_chunks, wave, tc.fam);
       fn = load_fields<MULT, VEC>(p, tn, lane);
     }
+    const int s_lo = (w % n_chunks) * p.spec_chunk;
+    const int s_hi = min(s_lo + p.spec_chunk, p.n_specs);
     const int fam = tc.fam;
     // this family takes the bounded head (the plain eta = 1 stream has none)
     const bool bnd = KIND != kEtaOne && ((p.bounded_mask >> fam) & 1u);
@@ -1398,8 +1402,9 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
         using S4 = typename H::S4;
         S4 st;
         H::init_state(st);
-        const int S = p.n_specs;
-        SpecC sc = spec_at(p.spec_c, 0);
+        // specs s_lo + s, s = 0 .. S - 1
+        const int S = s_hi - s_lo;
+        SpecC sc = spec_at(p.spec_c, s_lo);
         Roof o = small ? roofline<true>(rc, sc) : roofline<false>(rc, sc);
         u32x4 XB[2][1];
         {
@@ -1413,7 +1418,7 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
         // spec's groups are a second copy without the next spec's work)
         auto spec_iter = [&](int s, auto next_c) {
           constexpr bool NEXT = decltype(next_c)::value;
-          const SpecC sn = spec_at(p.spec_c, NEXT ? s + 1 : s);
+          const SpecC sn = spec_at(p.spec_c, s_lo + (NEXT ? s + 1 : s));
           Roof on;
           u32x4 XBn[2][1];
           float xn[IN];
@@ -1432,8 +1437,8 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
             if constexpr (I == 12) eta_prev = 1.0f + __expf(-H::tail_reduce(zp, lds));
             if constexpr (I == 14) {
               if (s > 0)
-                spec_tail<MULT>(p, s - 1, tr_prev, eta_prev, fmaxf(tr_prev * eta_prev, t0_prev), valid, live, row,
-                                tfac, fac, dst);
+                spec_tail<MULT>(p, s_lo + s - 1, tr_prev, eta_prev, fmaxf(tr_prev * eta_prev, t0_prev), valid, live,
+                                row, tfac, fac, dst);
             }
             if constexpr (NEXT && I == 20) on = small ? roofline<true>(rc, sn) : roofline<false>(rc, sn);
             if constexpr (NEXT && I == 22) {
@@ -1470,11 +1475,12 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
         H::tail_pairs(st, zl, 0, 4);
         H::tail_pairs(st, zl, 4, 8);
         const float eta = 1.0f + __expf(-H::tail_reduce(zl, lds));
-        spec_tail<MULT>(p, S - 1, tr_prev, eta, fmaxf(tr_prev * eta, t0_prev), valid, live, row, tfac, fac, dst);
+        spec_tail<MULT>(p, s_lo + S - 1, tr_prev, eta, fmaxf(tr_prev * eta, t0_prev), valid, live, row, tfac, fac,
+                        dst);
         continue;
       }
     }
-    for (int s = 0; s < p.n_specs; ++s) {
+    for (int s = s_lo; s < s_hi; ++s) {
       const SpecC sc = spec_at(p.spec_c, s);
       const Roof o = small ? roofline<true>(rc, sc) : roofline<false>(rc, sc);
       float eta = 1.0f;
@@ -2186,8 +2192,23 @@ static hipError_t launch_grid(const EvalParams &p, hipStream_t s) {
   const hipError_t e = resident_wgs<KIND, VAR>(&cap);
   if (e != hipSuccess) return e;
   const int n_wgt = p.wgt_off[KS_NFAM];
-  const int grid = n_wgt < cap ? n_wgt : cap;
-  hipLaunchKernelGGL((k_eval<KIND, VAR>), dim3(grid), dim3(kWgThreads), 0, s, p);
+  // Too few record tiles to fill the GPU (e.g. one serving round of many
+  // spec vectors): split the spec loop into ranges, each a work item of its
+  // own, so that ranges of the same tile run on different CUs.  The sums
+  // and outputs of different specs are disjoint; the record ranges are
+  // written alike by every range.
+  EvalParams q = p;
+  q.spec_chunk = p.n_specs;
+  q.n_chunks = 1;
+  if (n_wgt < cap && p.n_specs > 1) {
+    const int want = (cap + n_wgt - 1) / n_wgt;
+    const int chunks = want < p.n_specs ? want : p.n_specs;
+    q.spec_chunk = (p.n_specs + chunks - 1) / chunks;
+    q.n_chunks = (p.n_specs + q.spec_chunk - 1) / q.spec_chunk;
+  }
+  const int64_t work = (int64_t)n_wgt * q.n_chunks;
+  const int grid = work < cap ? (int)work : cap;
+  hipLaunchKernelGGL((k_eval<KIND, VAR>), dim3(grid), dim3(kWgThreads), 0, s, q);
   return hipGetLastError();
 }
 
