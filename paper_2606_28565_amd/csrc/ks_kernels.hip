@@ -10,9 +10,9 @@
 //                on MFMA (Sec. 5.3), t = max(t_roof eta, t0) (Eq. 2), a
 //                wavefront segmented sum of t by step, and each (family,
 //                step) record range
-//   k_stream     instead of k_eval for the eta = 1 step sums without
-//                per-pair outputs: the same per 256 records and wave, four
-//                consecutive records per lane
+//   k_stream     instead of k_eval for every call with no MLP family and
+//                no measured grid (eta = 1, the bounded head): the same per
+//                256 records and wave, four consecutive records per lane
 //   k_finish     per (spec, step): body sum, all-reduce (Eq. 3), assembly (Eq. 4)
 #include <hip/hip_runtime.h>
 
@@ -1519,14 +1519,16 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
 }
 
 // ------------------------------------------------------------ eta = 1 stream
-// The pure roofline (eta = 1, Eq. 2) of every (spec, record) pair: its
-// per-pair outputs and/or the step sums (Sec. 5.7).  A wave takes a
-// workgroup tile on its own (256 consecutive records of one family: four
-// 64-record tiles) and each lane four consecutive records of it, so that
-// each 16-lane DPP row holds exactly one 64-record tile.  A lane loads its
-// four records of a field with one 16-byte load, so the wave's load of a
-// field covers the tile's 1 KB contiguously.  Per spec a lane writes its four records' per-pair outputs as one vector
-// store each, and sums their t in runs of equal step (one FMA each); one
+// The pure roofline (eta = 1, Eq. 2), or the bounded head on its families,
+// for every (spec, record) pair: its per-pair outputs and/or the step sums
+// (Sec. 5.7).  A wave takes a workgroup tile on its own (256 consecutive
+// records of one family: four 64-record tiles) and each lane four
+// consecutive records of it, so that each 16-lane DPP row holds exactly one
+// 64-record tile.  A lane loads its four records of a field with one
+// 16-byte load, so the wave's load of a field covers the tile's 1 KB
+// contiguously.  Per spec a lane writes its four records' per-pair outputs
+// as one vector store each, and sums their t in runs of equal step (one FMA
+// each); one
 // segmented scan per row then joins the lanes' last runs, and each run's
 // tail record adds the carry-in of the lanes before it.  The cross-lane
 // work is thus per four records instead of per record.  Runs are split at
