@@ -1584,10 +1584,9 @@ struct STile {
   bool hp, hn;   // a record of the family exists just before / after it
 };
 
-__device__ __forceinline__ STile stream_locate(const EvalParams &p, int wt, int fam0) {
+// workgroup tile wt, one of family fam's
+__device__ __forceinline__ STile stream_locate(const EvalParams &p, int wt, int fam) {
   STile t;
-  int fam = fam0;
-  while (wt >= p.wgt_off[fam + 1]) ++fam;
   const int in_fam = wt - p.wgt_off[fam];
   const int64_t lo = p.fam_off[fam], hi = p.fam_off[fam + 1];
   t.fam = fam;
@@ -1769,40 +1768,52 @@ __device__ __forceinline__ void stream_specs(const EvalParams &p, const STile &t
   }
 }
 
-// One workgroup tile of family FAM; rng and part: the family's range table
-// and partials (formed before the family is dispatched on, so that each
-// family's code does not hold its own copy of them).
+// A tile's loads: the lane's four records of each field its family uses
+// (16 bytes per lane and field, so the wave's load of a field covers the
+// tile contiguously; zero for the unused fields), the multiplicities, and
+// the steps just before and after the tile (lane 0 and lane 1 of one load;
+// each address inside the family: the tile's first row where a neighbour
+// does not exist).
+struct SLoad {
+  u32x4 f[6];
+  u32x4 mult;
+  uint32_t pn;
+};
+
+template <int FAM, int VAR>
+__device__ __forceinline__ void stream_load(const EvalParams &p, const STile &t, int lane, SLoad &o) {
+  const uint32_t *src[6] = {p.step, p.m, p.n, p.k, p.a, p.b};
+#pragma unroll
+  for (int f = 0; f < 6; ++f) {
+    o.f[f] = u32x4{0, 0, 0, 0};
+    if (uses_field(FAM, f)) o.f[f] = load_quad(src[f] + t.row0, lane, t.nvalid);
+  }
+  if constexpr ((VAR & kStrMult) != 0) o.mult = load_quad(p.mult + t.row0, lane, t.nvalid);
+  o.pn = 0;
+  if constexpr ((VAR & kStrSums) != 0) {
+    const int pn_off = lane == 0 ? (t.hp ? -1 : 0) : (t.hn ? kWgRows : 0);
+    o.pn = (p.step + t.row0)[pn_off];
+  }
+}
+
+// One workgroup tile of family FAM, its loads in `in`; rng and part: the
+// family's range table and partials.
 template <int FAM, int VAR>
 __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc, int lane, uint32_t *rng,
-                                            double *part) {
+                                            double *part, const SLoad &in) {
   constexpr bool SUMS = (VAR & kStrSums) != 0, PAIR = (VAR & kStrPair) != 0, MULT = (VAR & kStrMult) != 0;
-  // the lane's four records of each field the family uses, 16 bytes per
-  // lane and field (the wave's loads of a field cover the tile contiguously)
   uint32_t v[6][kStreamR];
-  {
-    const uint32_t *src[6] = {p.step, p.m, p.n, p.k, p.a, p.b};
 #pragma unroll
-    for (int f = 0; f < 6; ++f) {
-      u32x4 q = {0, 0, 0, 0};
-      if (uses_field(FAM, f)) q = load_quad(src[f] + tc.row0, lane, tc.nvalid);
+  for (int f = 0; f < 6; ++f) {
 #pragma unroll
-      for (int j = 0; j < kStreamR; ++j) v[f][j] = q[j];
-    }
+    for (int j = 0; j < kStreamR; ++j) v[f][j] = uses_field(FAM, f) ? in.f[f][j] : 0u;
   }
   SRec r;
   if constexpr (MULT) {
-    const u32x4 q = load_quad(p.mult + tc.row0, lane, tc.nvalid);
 #pragma unroll
-    for (int j = 0; j < kStreamR; ++j) r.mf[j] = (float)q[j];   // exact below 2^24
+    for (int j = 0; j < kStreamR; ++j) r.mf[j] = (float)in.mult[j];   // exact below 2^24
   }
-  // the steps just before and after the tile: lane 0 and lane 1 of one load
-  // (each address inside the family: the tile's first row where a
-  // neighbour does not exist)
-  uint32_t pn = 0;
-  if constexpr (SUMS) {
-    const int pn_off = lane == 0 ? (tc.hp ? -1 : 0) : (tc.hn ? kWgRows : 0);
-    pn = (p.step + tc.row0)[pn_off];
-  }
+  const uint32_t pn = in.pn;
 
   // per record: counts and the spec-independent roofline operands; exact
   // (u64) when the per-record counts are written, else in fp32
@@ -1904,6 +1915,9 @@ __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc
   if constexpr ((VAR & kStrBnd) != 0) {
     if (bnd) {
       prm = p.bounded + FAM * 32;
+      // read the parameters again in each tile rather than hold them in
+      // scalar registers across the family's tiles
+      asm volatile("" : "+s"(prm));
 #pragma unroll
       for (int j = 0; j < kStreamR; ++j) {
 #pragma clang fp contract(off)
@@ -1962,44 +1976,54 @@ __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc
   }
 }
 
-// Waves per SIMD the register allocator must fit: six for the plain step
-// sums (80 registers); the other variants take what their registers allow
-// (asking for seven with per-pair latencies alone spills and measured
-// slower).
+// Waves per SIMD the register allocator must fit, at least: six for the
+// plain step sums (seven spills and measured slower); the other variants
+// take what their registers allow.
 template <int VAR> struct StreamOcc {
   static constexpr int value =
       VAR == kStrSums ? 6 : ((VAR & kStrBnd) && (VAR & kStrSums) && (VAR & kStrPair) ? 3 : 4);
 };
 
+// The wave's tiles of family FAM, from tile wt on in steps of stride (wt
+// advances past them).  Looping over one family at a time keeps the
+// family's constants and code out of the other families' loops (fewer live
+// registers than dispatching on the family per tile); issuing a tile's
+// loads a tile ahead measured no faster.
+template <int FAM, int VAR>
+__device__ __forceinline__ void stream_family(const EvalParams &p, int &wt, int stride, int lane) {
+  const int end = p.wgt_off[FAM + 1];
+  if (wt >= end) return;
+  uint32_t *rng = nullptr;
+  double *part = nullptr;
+  if constexpr ((VAR & kStrSums) != 0) {
+    rng = p.range + 2 * (size_t)FAM * (size_t)p.n_steps;
+    part = p.partial + (size_t)FAM * (size_t)p.n_steps * (size_t)p.n_specs;
+  }
+  for (; wt < end; wt += stride) {
+    const STile t = stream_locate(p, wt, FAM);
+    SLoad in;
+    stream_load<FAM, VAR>(p, t, lane, in);
+    stream_tile<FAM, VAR>(p, t, lane, rng, part, in);
+  }
+}
+
 template <int VAR>
 __global__ __launch_bounds__(kWgThreads) __attribute__((amdgpu_waves_per_eu(StreamOcc<VAR>::value)))
 void k_stream(EvalParams p) {
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int n_wgt = p.wgt_off[KS_NFAM];
   const int stride = (int)gridDim.x * kWgWaves;
-  int fam = 0;
-  for (int wt = (int)blockIdx.x * kWgWaves + wave; wt < n_wgt; wt += stride) {
-    const STile tc = stream_locate(p, wt, fam);
-    fam = tc.fam;
-    uint32_t *rng = nullptr;
-    double *part = nullptr;
-    if constexpr ((VAR & kStrSums) != 0) {
-      rng = p.range + 2 * (size_t)fam * (size_t)p.n_steps;
-      part = p.partial + (size_t)fam * (size_t)p.n_steps * (size_t)p.n_specs;
-    }
-    switch (fam) {
-      case KS_GEMM: stream_tile<KS_GEMM, VAR>(p, tc, lane, rng, part); break;
-      case KS_LM_HEAD: stream_tile<KS_LM_HEAD, VAR>(p, tc, lane, rng, part); break;
-      case KS_GROUPED_GEMM: stream_tile<KS_GROUPED_GEMM, VAR>(p, tc, lane, rng, part); break;
-      case KS_ATTN_PREFILL: stream_tile<KS_ATTN_PREFILL, VAR>(p, tc, lane, rng, part); break;
-      case KS_ATTN_DECODE: stream_tile<KS_ATTN_DECODE, VAR>(p, tc, lane, rng, part); break;
-      case KS_RMSNORM: stream_tile<KS_RMSNORM, VAR>(p, tc, lane, rng, part); break;
-      case KS_ROPE: stream_tile<KS_ROPE, VAR>(p, tc, lane, rng, part); break;
-      case KS_SILU_MUL: stream_tile<KS_SILU_MUL, VAR>(p, tc, lane, rng, part); break;
-      case KS_KV_WRITE: stream_tile<KS_KV_WRITE, VAR>(p, tc, lane, rng, part); break;
-      default: stream_tile<KS_EMBED, VAR>(p, tc, lane, rng, part); break;
-    }
-  }
+  int wt = (int)blockIdx.x * kWgWaves + wave;
+  stream_family<KS_GEMM, VAR>(p, wt, stride, lane);
+  stream_family<KS_LM_HEAD, VAR>(p, wt, stride, lane);
+  stream_family<KS_GROUPED_GEMM, VAR>(p, wt, stride, lane);
+  stream_family<KS_ATTN_PREFILL, VAR>(p, wt, stride, lane);
+  stream_family<KS_ATTN_DECODE, VAR>(p, wt, stride, lane);
+  stream_family<KS_RMSNORM, VAR>(p, wt, stride, lane);
+  stream_family<KS_ROPE, VAR>(p, wt, stride, lane);
+  stream_family<KS_SILU_MUL, VAR>(p, wt, stride, lane);
+  stream_family<KS_KV_WRITE, VAR>(p, wt, stride, lane);
+  stream_family<KS_EMBED, VAR>(p, wt, stride, lane);
+  static_assert(KS_EMBED == KS_NFAM - 1, "every family has its loop");
 }
 
 // ------------------------------------------------------------ eta source
@@ -2219,6 +2243,12 @@ static hipError_t launch_grid(const EvalParams &p, hipStream_t s) {
 // per wave.  As many workgroups as are resident, cached per device and
 // variant.
 constexpr int kNumStreamVars = 16;
+// Workgroups per CU of a variant, at most (0: as many as are resident):
+// the per-pair outputs alone fit seven waves per SIMD in registers and
+// measured faster at five.
+template <int VAR> struct StreamWgCap {
+  static constexpr int value = VAR == kStrPair ? 5 : 0;
+};
 static std::atomic<int> g_stream_resident[kMaxDevices][kNumStreamVars];
 
 template <int VAR>
@@ -2234,6 +2264,7 @@ static hipError_t launch_stream(const EvalParams &p, hipStream_t s) {
     if (e != hipSuccess) return e;
     e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
+    if (StreamWgCap<VAR>::value > 0 && per_cu > StreamWgCap<VAR>::value) per_cu = StreamWgCap<VAR>::value;
     cap = (per_cu < 1 ? 1 : per_cu) * (n_cu < 1 ? 1 : n_cu);
     if (slot) slot->store(cap, std::memory_order_relaxed);
   }
