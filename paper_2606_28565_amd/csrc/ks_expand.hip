@@ -171,13 +171,14 @@ __global__ __launch_bounds__(256) void k_expand_records(ExpandParams p) {
       const uint32_t r0 = p.req_off[j], r1 = p.req_off[j + 1];
       m = r1 >= r0 ? r1 - r0 : 0u;
     }
-    p.o_step[dst] = j;
-    p.o_m[dst] = m;
-    p.o_n[dst] = tn;
-    p.o_k[dst] = tk;
-    p.o_a[dst] = ta;
-    p.o_b[dst] = tg ? (j * p.L + layer) * p.E : 0u;
-    if (p.o_mult) p.o_mult[dst] = p.mult[f];
+    // written once and read by a later kernel: stream past the caches
+    __builtin_nontemporal_store(j, p.o_step + dst);
+    __builtin_nontemporal_store(m, p.o_m + dst);
+    __builtin_nontemporal_store(tn, p.o_n + dst);
+    __builtin_nontemporal_store(tk, p.o_k + dst);
+    __builtin_nontemporal_store(ta, p.o_a + dst);
+    __builtin_nontemporal_store(tg ? (j * p.L + layer) * p.E : 0u, p.o_b + dst);
+    if (p.o_mult) __builtin_nontemporal_store(p.mult[f], p.o_mult + dst);
   }
   if (bad) atomicOr(p.err, bad);
 }

@@ -1645,12 +1645,13 @@ struct SRec {
 // a lane's four consecutive records (4 lane .. 4 lane + 3 of the tile) of
 // one field array, base: the tile's first record: one 16-byte load when the
 // four are valid and the address is 16-byte aligned, else one load per
-// record with its index clamped to the tile's valid rows (nvalid >= 1)
+// record with its index clamped to the tile's valid rows (nvalid >= 1).
+// The 16-byte loads are non-temporal: every record is read once per call.
 __device__ __forceinline__ u32x4 load_quad(const uint32_t *base, int lane, int nvalid) {
   const uint32_t *q = reinterpret_cast<const uint32_t *>(reinterpret_cast<const char *>(base) +
                                                          (uint32_t)(16 * lane));
   if (kStreamR * lane + kStreamR - 1 < nvalid && (reinterpret_cast<uintptr_t>(q) & 15) == 0)
-    return *reinterpret_cast<const u32x4 *>(q);
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(q));
   u32x4 r;
 #pragma unroll
   for (int j = 0; j < kStreamR; ++j) {
@@ -1663,13 +1664,13 @@ __device__ __forceinline__ u32x4 load_quad(const uint32_t *base, int lane, int n
 // four consecutive per-pair values of a lane (records 4 lane .. 4 lane + 3
 // of the tile) at base + 4 lane (base: the tile's first record, the same
 // for the whole wave, so the lane's part is a 32-bit offset): one 16-byte
-// store when all four are valid and the address is 16-byte aligned, else
-// one store per valid record
+// store (non-temporal: nothing here reads it back) when all four are valid
+// and the address is 16-byte aligned, else one store per valid record
 __device__ __forceinline__ void store_quad(float *base, int lane, int nvalid, const float (&v)[kStreamR]) {
   typedef float f32x4 __attribute__((ext_vector_type(4)));
   float *q = reinterpret_cast<float *>(reinterpret_cast<char *>(base) + (uint32_t)(16 * lane));
   if (kStreamR * lane + kStreamR - 1 < nvalid && (reinterpret_cast<uintptr_t>(q) & 15) == 0) {
-    *reinterpret_cast<f32x4 *>(q) = f32x4{v[0], v[1], v[2], v[3]};
+    __builtin_nontemporal_store(f32x4{v[0], v[1], v[2], v[3]}, reinterpret_cast<f32x4 *>(q));
   } else {
 #pragma unroll
     for (int j = 0; j < kStreamR; ++j)
