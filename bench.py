@@ -68,11 +68,19 @@ def expand_bytes(n_records: int, n_steps: int, with_mult: bool) -> float:
 
 
 def kernel_source_hash() -> str:
+    """SHA-256 of the GPU kernels' sources with comments and blank lines
+    taken out, so that the recorded counters follow the code, not its
+    commentary."""
     import hashlib
+    import re
     h = hashlib.sha256()
-    for f in ("ks_kernels.hip", "ks_expand.hip", "ks_internal.h"):
-        with open(os.path.join(ROOT, "paper_2606_28565_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+    for f in ("ks_kernels.hip", "ks_expand.hip", "ks_internal.h", "ks_sched.inc"):
+        with open(os.path.join(ROOT, "paper_2606_28565_amd", "csrc", f)) as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", "", text)
+        code = [line.rstrip() for line in text.splitlines() if line.strip()]
+        h.update(("\n".join(code) + "\n").encode())
     return h.hexdigest()
 
 
