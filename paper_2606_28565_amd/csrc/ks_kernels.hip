@@ -749,8 +749,94 @@ struct HeadBF16 {
   // ---- the pieces of one spec's head (mlp4 runs them in order; the
   // software-pipelined spec loop of k_eval spreads the last block's
   // epilogue over the next spec's groups).  kPipe: the heads whose group
-  // schedule that loop knows.
-  static constexpr bool kPipe = MB == 4 && KC1 == 1;
+  // schedule that loop knows; kHooks: the groups after which it places the
+  // previous spec's last-block epilogue (four slices), its eta and its tail,
+  // and the next spec's roofline, features and packing.  The epilogue
+  // slices come before the first group that overwrites the last block's
+  // accumulators; the other hooks sit mostly in groups with no VALU work of
+  // their own.
+  // What the pipelined loop does after group I: the previous spec's
+  // last-block epilogue pairs [tp0, tp1), its eta, its tail; the next spec's
+  // roofline, the features in the mask feat, the squares [sq0, sq1) of a
+  // 32-input head, and the packing of layer-1 K chunks [pk0, pk1).
+  struct Hook {
+    int tp0, tp1;
+    bool eta, tail, roof;
+    uint32_t feat;
+    int sq0, sq1, pk0, pk1;
+  };
+  static constexpr bool kPipe = (MB == 4 && KC1 == 1) || (MB == 8 && KC1 == 2);
+  // the first group that overwrites the last block's accumulators (p0, p1)
+  __device__ static constexpr int first_p_write() {
+    for (int i = 0; i < kNG; ++i)
+      if (sched(i).mk == 2 && sched(i).kc == 0 && sched(i).mb > 0) return i;
+    return kNG;
+  }
+  __device__ static constexpr Hook hook_at(int I) {
+    Hook h{0, 0, false, false, false, 0u, 0, 0, 0, 0};
+    if constexpr (MB == 4) {
+      // two waves per SIMD: the other wave's MFMAs cover larger slices
+      if (I == 0) h.tp0 = 0, h.tp1 = 2;
+      if (I == 5) h.tp0 = 2, h.tp1 = 4;
+      if (I == 6) h.tp0 = 4, h.tp1 = 6;
+      if (I == 11) h.tp0 = 6, h.tp1 = 8;
+      if (I == 12) h.eta = true;
+      if (I == 14) h.tail = true;
+      if (I == 20) h.roof = true;
+      if (I == 22) h.feat = 0xeu;
+      if (I == 24) h.feat = 0xf0u;
+      if (I == 28) h.feat = 0xff01u, h.pk0 = 0, h.pk1 = KC1;
+    } else {
+      // one wave per SIMD: slices small enough to issue in the shadow of
+      // one group's MFMA pair, in groups without VALU work of their own
+      constexpr int tp[8] = {0, 1, 4, 5, 8, 9, 12, 13};
+      for (int j = 0; j < 8; ++j)
+        if (I == tp[j]) h.tp0 = j, h.tp1 = j + 1;
+      if (I == 16) h.eta = true;
+      if (I == 20) h.tail = true;
+      if (I == 35) h.roof = true;
+      constexpr int ft[8] = {37, 39, 41, 43, 45, 47, 51, 53};   // features 1 .. 7, then 0 and 8 .. 15
+      for (int f = 1; f < 8; ++f)
+        if (I == ft[f - 1]) h.feat = 1u << f;
+      if (I == ft[7]) h.feat = 0xff01u;
+      if (I == 55) h.pk0 = 0, h.pk1 = 1;
+      if (I == 57) h.sq0 = 0, h.sq1 = 8;
+      if (I == 59) h.sq0 = 8, h.sq1 = 16;
+      if (I == 61) h.pk0 = 1, h.pk1 = 2;
+    }
+    return h;
+  }
+  // every epilogue pair once, before the accumulators are overwritten;
+  // every feature, square and chunk once, in order
+  __device__ static constexpr bool hooks_ok() {
+    int pairs = 0, last_tp = -1, eta = -1, tail = -1, roof = -1, pk = 0, sq = 0;
+    uint32_t feats = 0;
+    for (int i = 0; i < kNG; ++i) {
+      const Hook h = hook_at(i);
+      if (h.tp1 > h.tp0) {
+        if (h.tp0 != pairs || i >= first_p_write()) return false;
+        pairs = h.tp1, last_tp = i;
+      }
+      if (h.eta) eta = i;
+      if (h.tail) tail = i;
+      if (h.roof) roof = i;
+      if (h.feat && (roof < 0 || (feats & h.feat))) return false;
+      feats |= h.feat;
+      if (h.sq1 > h.sq0) {
+        if (h.sq0 != sq || feats != 0xffffu) return false;
+        sq = h.sq1;
+      }
+      if (h.pk1 > h.pk0) {
+        if (h.pk0 != pk) return false;
+        for (int kc = h.pk0; kc < h.pk1; ++kc)
+          if (kc == 0 ? feats != 0xffffu : sq < 16) return false;
+        pk = h.pk1;
+      }
+    }
+    return pairs == 8 && last_tp < eta && eta < tail && tail < roof && feats == 0xffffu && pk == KC1 &&
+           (KC1 == 1 || sq == 16);
+  }
+  static_assert(!kPipe || hooks_ok(), "every hook once, in order, the epilogue before its accumulators go");
   __device__ static __forceinline__ void init_state(S4 &st) {
     st.lane = threadIdx.x & 63;
     st.g = st.lane >> 5;
@@ -813,12 +899,13 @@ struct HeadBF16 {
 
   // x -> bf16 pairs; the swap turns "own record" into the B layout of the
   // two 32-record column blocks
-  __device__ static __forceinline__ void pack_x(const float (&x)[IN], u32x4 (&XB)[2][KC1]) {
+  __device__ static __forceinline__ void pack_x(const float (&x)[IN], u32x4 (&XB)[2][KC1], int kc0 = 0,
+                                                int kc1 = KC1) {
     uint32_t P[IN / 2];
 #pragma unroll
-    for (int c = 0; c < IN / 2; ++c) P[c] = pack_bf16(x[2 * c], x[2 * c + 1]);
+    for (int c = 8 * kc0; c < 8 * kc1; ++c) P[c] = pack_bf16(x[2 * c], x[2 * c + 1]);
 #pragma unroll
-    for (int kc = 0; kc < KC1; ++kc) {
+    for (int kc = kc0; kc < kc1; ++kc) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         uint32_t lo = P[8 * kc + q], hi = P[8 * kc + 4 + q];
@@ -1406,7 +1493,8 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
         const int S = s_hi - s_lo;
         SpecC sc = spec_at(p.spec_c, s_lo);
         Roof o = small ? roofline<true>(rc, sc) : roofline<false>(rc, sc);
-        u32x4 XB[2][1];
+        constexpr int KC1 = H::KC1;
+        u32x4 XB[2][KC1];
         {
           float x[IN];
           features<IN, H::kRaw>(rc, sc, o, x);
@@ -1420,41 +1508,34 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
           constexpr bool NEXT = decltype(next_c)::value;
           const SpecC sn = spec_at(p.spec_c, s_lo + (NEXT ? s + 1 : s));
           Roof on;
-          u32x4 XBn[2][1];
+          u32x4 XBn[2][KC1];
           float xn[IN];
           float eta_prev = 1.0f;
           const float tr_cur = o.t_roof, t0_cur = sc.t0;
           H::begin_spec(st, XB, lds, zp);
-          // group indices of the 36-group schedule of the 16-128 head: 0, 5,
-          // 6 and 11 carry no VALU work of their own, nor do 20 and 28; the
-          // next spec's features are spread over three groups
+          // after each group, its share of the neighbouring specs' work
+          // (hook_at)
           auto hook = [&](auto ic) {
             constexpr int I = decltype(ic)::value;
-            if constexpr (I == 0) H::tail_pairs(st, zp, 0, 2);
-            if constexpr (I == 5) H::tail_pairs(st, zp, 2, 4);
-            if constexpr (I == 6) H::tail_pairs(st, zp, 4, 6);
-            if constexpr (I == 11) H::tail_pairs(st, zp, 6, 8);
-            if constexpr (I == 12) eta_prev = 1.0f + __expf(-H::tail_reduce(zp, lds));
-            if constexpr (I == 14) {
+            constexpr typename H::Hook a = H::hook_at(I);
+            if constexpr (a.tp1 > a.tp0) H::tail_pairs(st, zp, a.tp0, a.tp1);
+            if constexpr (a.eta) eta_prev = 1.0f + __expf(-H::tail_reduce(zp, lds));
+            if constexpr (a.tail) {
               if (s > 0)
                 spec_tail<MULT>(p, s_lo + s - 1, tr_prev, eta_prev, fmaxf(tr_prev * eta_prev, t0_prev), valid, live,
                                 row, tfac, fac, dst);
             }
-            if constexpr (NEXT && I == 20) on = small ? roofline<true>(rc, sn) : roofline<false>(rc, sn);
-            if constexpr (NEXT && I == 22) {
+            if constexpr (NEXT && a.roof) on = small ? roofline<true>(rc, sn) : roofline<false>(rc, sn);
+            if constexpr (NEXT && a.feat != 0u) {
 #pragma unroll
-              for (int i = 1; i < 4; ++i) xn[i] = feature<H::kRaw>(i, rc, sn, on);
+              for (int i = 0; i < 16; ++i)
+                if ((a.feat >> i) & 1u) xn[i] = feature<H::kRaw>(i, rc, sn, on);
             }
-            if constexpr (NEXT && I == 24) {
+            if constexpr (NEXT && a.sq1 > a.sq0) {
 #pragma unroll
-              for (int i = 4; i < 8; ++i) xn[i] = feature<H::kRaw>(i, rc, sn, on);
+              for (int i = a.sq0; i < a.sq1; ++i) xn[16 + i] = xn[i] * xn[i];
             }
-            if constexpr (NEXT && I == 28) {
-              xn[0] = feature<H::kRaw>(0, rc, sn, on);
-#pragma unroll
-              for (int i = 8; i < 16; ++i) xn[i] = feature<H::kRaw>(i, rc, sn, on);
-              H::pack_x(xn, XBn);
-            }
+            if constexpr (NEXT && a.pk1 > a.pk0) H::pack_x(xn, XBn, a.pk0, a.pk1);
           };
           H::run_groups(st, lds, hook);
           tr_prev = tr_cur;
@@ -1462,8 +1543,11 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
           if constexpr (NEXT) {
             o = on;
             sc = sn;
-            XB[0][0] = XBn[0][0];
-            XB[1][0] = XBn[1][0];
+#pragma unroll
+            for (int kc = 0; kc < KC1; ++kc) {
+              XB[0][kc] = XBn[0][kc];
+              XB[1][kc] = XBn[1][kc];
+            }
           }
         };
         for (int s = 0; s + 1 < S; ++s) spec_iter(s, std::true_type{});
