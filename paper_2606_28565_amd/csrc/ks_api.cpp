@@ -248,12 +248,10 @@ void fill_eval(ks::EvalParams &p, const ks_desc *d, const ks_spec *specs, int32_
 
 ks_status prologue(const ks_desc *d, const ks_spec *specs, int32_t n_specs, char *ws, const Layout &L,
                    bool with_range, hipStream_t s) {
-  hipError_t e = ks::launch_clear(reinterpret_cast<uint32_t *>(ws), reinterpret_cast<uint32_t *>(ws + L.range),
-                                  with_range ? 2 * (int64_t)KS_NFAM * d->n_steps : 0, s);
-  if (e != hipSuccess) return hip_fail(e, "clear launch");
-  e = ks::launch_spec_prep(specs, n_specs, reinterpret_cast<ks::SpecC *>(ws + L.specc),
-                           reinterpret_cast<uint32_t *>(ws), s);
-  if (e != hipSuccess) return hip_fail(e, "spec constants launch");
+  hipError_t e = ks::launch_clear_prep(reinterpret_cast<uint32_t *>(ws), reinterpret_cast<uint32_t *>(ws + L.range),
+                                       with_range ? 2 * (int64_t)KS_NFAM * d->n_steps : 0, specs, n_specs,
+                                       reinterpret_cast<ks::SpecC *>(ws + L.specc), s);
+  if (e != hipSuccess) return hip_fail(e, "clear and spec constants launch");
   e = ks::launch_attn_agg(d->req_off, d->req_q, d->req_h, d->n_steps, d->n_req,
                           reinterpret_cast<uint64_t *>(ws + L.agg), reinterpret_cast<uint32_t *>(ws), s);
   if (e != hipSuccess) return hip_fail(e, "attention aggregate launch");

@@ -174,6 +174,10 @@ ks_status set_error(ks_status st, const char *fmt, ...);
 
 hipError_t launch_clear(uint32_t *err, uint32_t *range, int64_t n_range, hipStream_t s);
 hipError_t launch_spec_prep(const ks_spec *specs, int32_t n_specs, SpecC *out, uint32_t *err, hipStream_t s);
+// launch_clear, then the spec constants of launch_spec_prep (in the same
+// launch for a few specs)
+hipError_t launch_clear_prep(uint32_t *err, uint32_t *range, int64_t n_range, const ks_spec *specs,
+                             int32_t n_specs, SpecC *out, hipStream_t s);
 hipError_t launch_attn_agg(const uint32_t *req_off, const uint32_t *q, const uint32_t *h,
                            int64_t n_steps, int64_t n_req, uint64_t *agg, uint32_t *err,
                            hipStream_t s);

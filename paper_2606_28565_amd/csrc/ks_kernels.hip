@@ -79,9 +79,20 @@ __device__ __forceinline__ void swap32(uint32_t &lo, uint32_t &hi) {
 // ------------------------------------------------------------ clear / agg
 // Reset the flag word and, when step sums are wanted, the per-(family,
 // step) range table (an empty range marks a family without that step).
-__global__ void k_clear(uint32_t *err, uint32_t *range, int64_t n_range) {
+__device__ void spec_prep_one(const ks_spec *__restrict__ specs, int s, SpecC *__restrict__ out, uint32_t *err);
+
+// With specs (n_specs > 0), the first workgroup also forms their constants
+// once the flag word is reset (a bad spec then flags the fresh word).
+__global__ void k_clear(uint32_t *err, uint32_t *range, int64_t n_range, const ks_spec *specs, int32_t n_specs,
+                        SpecC *specc) {
   const int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i0 == 0) err[0] = 0;
+  if (blockIdx.x == 0) {
+    if (threadIdx.x == 0) err[0] = 0;
+    if (n_specs > 0) {
+      __syncthreads();
+      for (int s = threadIdx.x; s < n_specs; s += blockDim.x) spec_prep_one(specs, s, specc, err);
+    }
+  }
   for (int64_t i = i0; i < n_range; i += (int64_t)gridDim.x * blockDim.x) range[i] = 0;
 }
 
@@ -294,10 +305,7 @@ __device__ __forceinline__ CntF record_counts_f(int fam, uint32_t m32, uint32_t 
 }
 
 // ------------------------------------------------------------ spec constants
-__global__ void k_spec_prep(const ks_spec *__restrict__ specs, int32_t n_specs, SpecC *__restrict__ out,
-                            uint32_t *err) {
-  const int s = blockIdx.x * blockDim.x + threadIdx.x;
-  if (s >= n_specs) return;
+__device__ void spec_prep_one(const ks_spec *__restrict__ specs, int s, SpecC *__restrict__ out, uint32_t *err) {
   const ks_spec sp = specs[s];
   SpecC c = {};
   const double P = sp.peak_flops, BW = sp.hbm_bw;
@@ -320,6 +328,12 @@ __global__ void k_spec_prep(const ks_spec *__restrict__ specs, int32_t n_specs, 
   c.rcp_n = (float)(1.0 / (double)n);
   c.rcp_nd = 1.0 / (double)n;
   out[s] = c;
+}
+
+__global__ void k_spec_prep(const ks_spec *__restrict__ specs, int32_t n_specs, SpecC *__restrict__ out,
+                            uint32_t *err) {
+  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s < n_specs) spec_prep_one(specs, s, out, err);
 }
 
 // Spec constants through the scalar cache: they are read-only during the
@@ -2152,21 +2166,41 @@ __global__ __launch_bounds__(kFinThreads) void k_finish(FinishParams p, int spec
       const int64_t j = j0 + jj;
       if (s < p.n_specs && j < p.n_steps) {
         const size_t S = (size_t)p.n_specs;
-        double body = 0.0;
+        // every family's range, then its partial and first carry, are
+        // loaded before any is summed (independent loads in flight together
+        // instead of a chain of ten); the sum keeps family order: partial,
+        // then the carries of its later tiles
+        uint32_t r0[KS_NFAM], r1[KS_NFAM];
+#pragma unroll
+        for (int f = 0; f < KS_NFAM; ++f) {
+          r0[f] = p.range[2 * (f * p.n_steps + j)];
+          r1[f] = p.range[2 * (f * p.n_steps + j) + 1];
+        }
+        bool any[KS_NFAM];
+        int t_first[KS_NFAM], t_last[KS_NFAM];
+        double part[KS_NFAM], car1[KS_NFAM];
+#pragma unroll
         for (int f = 0; f < KS_NFAM; ++f) {
           // clamped to the family's rows: a range left half-written by
           // unsorted input (reported by ks_validate) still indexes only this
           // family's tiles
           const int64_t base = p.fam_off[f], top = p.fam_off[f + 1];
-          int64_t r0 = p.range[2 * (f * p.n_steps + j)];
-          int64_t r1 = p.range[2 * (f * p.n_steps + j) + 1];
-          r0 = r0 < base ? base : (r0 > top ? top : r0);
-          r1 = r1 < base ? base : (r1 > top ? top : r1);
-          if (r0 >= r1) continue;
-          body += p.partial[((size_t)f * (size_t)p.n_steps + (size_t)j) * S + s];
-          const int t_first = p.tile_off[f] + (int)((r0 - base) / kTileRows);
-          const int t_last = p.tile_off[f] + (int)((r1 - 1 - base) / kTileRows);
-          for (int t = t_first + 1; t <= t_last; ++t) body += p.carry[(size_t)t * S + s];
+          int64_t a = r0[f], b = r1[f];
+          a = a < base ? base : (a > top ? top : a);
+          b = b < base ? base : (b > top ? top : b);
+          any[f] = a < b;
+          t_first[f] = any[f] ? p.tile_off[f] + (int)((a - base) / kTileRows) : 0;
+          t_last[f] = any[f] ? p.tile_off[f] + (int)((b - 1 - base) / kTileRows) : 0;
+          part[f] = any[f] ? p.partial[((size_t)f * (size_t)p.n_steps + (size_t)j) * S + s] : 0.0;
+          car1[f] = t_last[f] > t_first[f] ? p.carry[(size_t)(t_first[f] + 1) * S + s] : 0.0;
+        }
+        double body = 0.0;
+#pragma unroll
+        for (int f = 0; f < KS_NFAM; ++f) {
+          if (!any[f]) continue;
+          body += part[f];
+          if (t_last[f] > t_first[f]) body += car1[f];
+          for (int t = t_first[f] + 2; t <= t_last[f]; ++t) body += p.carry[(size_t)t * S + s];
         }
         const ks_spec sp = p.specs[s];
         const double P = (double)p.tp[j];
@@ -2253,7 +2287,8 @@ static int grid_for(int64_t n, int block, int cap) {
 }
 
 hipError_t launch_clear(uint32_t *err, uint32_t *range, int64_t n_range, hipStream_t s) {
-  hipLaunchKernelGGL(k_clear, dim3(grid_for(n_range, 256, 2048)), dim3(256), 0, s, err, range, n_range);
+  hipLaunchKernelGGL(k_clear, dim3(grid_for(n_range, 256, 2048)), dim3(256), 0, s, err, range, n_range,
+                     (const ks_spec *)nullptr, 0, (SpecC *)nullptr);
   return hipGetLastError();
 }
 
@@ -2268,6 +2303,20 @@ hipError_t launch_attn_agg(const uint32_t *req_off, const uint32_t *q, const uin
 hipError_t launch_spec_prep(const ks_spec *specs, int32_t n_specs, SpecC *out, uint32_t *err, hipStream_t s) {
   hipLaunchKernelGGL(k_spec_prep, dim3(grid_for(n_specs, 256, 4096)), dim3(256), 0, s, specs, n_specs, out, err);
   return hipGetLastError();
+}
+
+// up to this many specs the clear kernel's first workgroup forms the spec
+// constants (one launch less); more take their own grid
+constexpr int32_t kFusedSpecs = 1024;
+
+hipError_t launch_clear_prep(uint32_t *err, uint32_t *range, int64_t n_range, const ks_spec *specs,
+                             int32_t n_specs, SpecC *out, hipStream_t s) {
+  const bool fused = n_specs <= kFusedSpecs;
+  hipLaunchKernelGGL(k_clear, dim3(grid_for(n_range, 256, 2048)), dim3(256), 0, s, err, range, n_range, specs,
+                     fused ? n_specs : 0, out);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || fused) return e;
+  return launch_spec_prep(specs, n_specs, out, err, s);
 }
 
 // The persistent grid: as many workgroups as are resident at once (the

@@ -42,6 +42,12 @@ hipError_t launch_clear(uint32_t *err, uint32_t *range, int64_t n_range, hipStre
 
 hipError_t launch_spec_prep(const ks_spec *, int32_t, SpecC *, uint32_t *, hipStream_t) { return hipSuccess; }
 
+hipError_t launch_clear_prep(uint32_t *err, uint32_t *range, int64_t n_range, const ks_spec *specs, int32_t n_specs,
+                             SpecC *out, hipStream_t st) {
+  launch_clear(err, range, n_range, st);
+  return launch_spec_prep(specs, n_specs, out, err, st);
+}
+
 hipError_t launch_attn_agg(const uint32_t *req_off, const uint32_t *q, const uint32_t *h, int64_t n_steps,
                            int64_t n_req, uint64_t *agg, uint32_t *err, hipStream_t) {
   for (int64_t j = 0; j < n_steps; ++j) {

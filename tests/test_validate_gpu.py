@@ -117,3 +117,39 @@ def test_bad_spec_flagged():
     sp["n_cu"][:] = 0
     st, msg = _validate(_wl(GOOD_ROWS[:1], GOOD_REQS[:1], specs=sp))
     assert st == abi.KS_ERANGE and "spec" in msg
+
+
+@pytest.mark.parametrize("n_specs", [3, 1100])
+def test_bad_spec_flagged_by_evaluation(n_specs):
+    """A spec vector whose n_cu lies outside 1 .. 65535 is flagged by the
+    evaluation call itself: with few specs their constants are formed in the
+    clear kernel right after the flag word is reset, with many (1100) by a
+    grid of their own.  The next call with good specs reports clean."""
+    sp = {k: np.repeat(v, n_specs) for k, v in spec(P=1e15, BW=4e12, n_cu=132, t0=2e-6).items()}
+    for bad in (0, 70000):
+        sp["n_cu"][n_specs - 1] = bad
+        st, msg, _ = _eval_status(_wl(GOOD_ROWS, GOOD_REQS, experts=[3, 0], specs=sp))
+        assert st == abi.KS_ERANGE and "spec" in msg, (bad, msg)
+    sp["n_cu"][n_specs - 1] = 132
+    st, msg, _ = _eval_status(_wl(GOOD_ROWS, GOOD_REQS, experts=[3, 0], specs=sp))
+    assert st == abi.KS_OK, msg
+
+
+def test_many_specs_match_single_spec_calls():
+    """1100 distinct spec vectors in one call (spec constants formed by their
+    own grid) give, spec by spec, the step latencies of a one-spec call (spec
+    constants formed in the clear kernel), bit for bit."""
+    n = 1100
+    base = spec(P=1e15, BW=4e12, n_cu=132, t0=2e-6)
+    sp = {k: np.repeat(v, n) for k, v in base.items()}
+    sp["peak_flops"] = 1e15 * (1.0 + np.arange(n) / n)
+    sp["hbm_bw"] = 4e12 * (1.0 + 0.5 * np.cos(np.arange(n)))
+    sp["n_cu"] = (64 + np.arange(n) % 200).astype(np.int64)
+    st, msg, many = _eval_status(_wl(GOOD_ROWS, GOOD_REQS, experts=[3, 0], specs=sp))
+    assert st == abi.KS_OK, msg
+    for i in (0, 1, 1023, 1024, n - 1):
+        one = {k: v[i:i + 1].copy() for k, v in sp.items()}
+        st, msg, out = _eval_status(_wl(GOOD_ROWS, GOOD_REQS, experts=[3, 0], specs=one))
+        assert st == abi.KS_OK, msg
+        for k in ("t_body", "t_gpu", "t_step"):
+            np.testing.assert_array_equal(many[k].reshape(n, -1)[i], out[k].reshape(1, -1)[0], err_msg=f"{k} {i}")
