@@ -2,7 +2,9 @@
 // (CDNA4: wave64, MFMA, 160 KB LDS per CU).
 //
 // Data flow of one evaluation (all on the caller's stream):
-//   k_clear      reset the workspace's bad-data flag and step-range table
+//   k_clear      reset the workspace's bad-data flag and step-range table,
+//                then form the per-spec constants (k_spec_prep instead for
+//                more than 1024 specs)
 //   k_attn_agg   per step: Q, KV, PAIRS, TILES of its request list (Sec. 5.8)
 //   k_eval<K>    per wave: 64 records of one family x every spec vector:
 //                exact counts (Eq. 1-2 operands), waves and u (Sec. 2.2),
