@@ -1371,6 +1371,9 @@ __device__ __forceinline__ void spec_tail(const EvalParams &p, int s, float t_ro
   }
 }
 
+// work items per workgroup below which the heads take contiguous ranges
+constexpr int kBlockedItems = 32;
+
 template <int KIND, int VAR>
 __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalParams p) {
   constexpr bool GRID = (VAR & kVarGrid) != 0;
@@ -1390,15 +1393,28 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
   Fields fn = {0, 0, 0, 0, 0, 0, kNoKey, kNoKey, kNoKey, 1.0f};
   // tiles without a head take their neighbour steps by a vector load
   constexpr bool VEC = !H::kMlp;
-  if ((int)blockIdx.x < n_work) {
-    tn = locate(p, (int)blockIdx.x / n_chunks, wave, 0);
+  // With few work items per workgroup the heads take a contiguous range of
+  // them, so that a workgroup meets one or two families and stages their
+  // weights into LDS once or twice (striding over the grid it restaged them
+  // at nearly every item); with many, striding balances the families'
+  // different per-tile costs better, and the HBM-bound kinds always stride,
+  // which keeps the chip's loads in one window.  (The bounds are
+  // wave-uniform: readfirstlane keeps them in scalar registers.)
+  const int G = (int)gridDim.x, b = (int)blockIdx.x;
+  const bool blocked = H::kMlp && n_work < kBlockedItems * G;
+  const int w_begin = blocked ? __builtin_amdgcn_readfirstlane(b * (n_work / G) + min(b, n_work % G)) : b;
+  const int w_end =
+      blocked ? __builtin_amdgcn_readfirstlane(w_begin + n_work / G + (b < n_work % G ? 1 : 0)) : n_work;
+  const int w_step = blocked ? 1 : G;
+  if (w_begin < w_end) {
+    tn = locate(p, w_begin / n_chunks, wave, 0);
     fn = load_fields<MULT, VEC>(p, tn, lane);
   }
-  for (int w = blockIdx.x; w < n_work; w += gridDim.x) {
+  for (int w = w_begin; w < w_end; w += w_step) {
     const Tile tc = tn;
     const Fields fc = fn;
-    if (w + (int)gridDim.x < n_work) {
-      tn = locate(p, (w + (int)gridDim.x) / n_chunks, wave, tc.fam);
+    if (w + w_step < w_end) {
+      tn = locate(p, (w + w_step) / n_chunks, wave, tc.fam);
       fn = load_fields<MULT, VEC>(p, tn, lane);
     }
     const int s_lo = (w % n_chunks) * p.spec_chunk;
