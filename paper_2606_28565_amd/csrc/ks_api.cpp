@@ -432,9 +432,10 @@ ks_status ks_eval_kernels(const ks_desc *desc, const ks_spec *specs, int32_t n_s
   return KS_OK;
 }
 
-ks_status ks_eval_steps(const ks_desc *desc, const ks_steps *steps, const ks_spec *specs, int32_t n_specs,
-                        const ks_heads *heads, const ks_host *host, const ks_step_out *out,
-                        const ks_kernel_out *kout, void *ws, size_t ws_bytes, hipStream_t stream) {
+static ks_status eval_steps_impl(const ks_desc *desc, const ks_steps *steps, const ks_spec *specs,
+                                 int32_t n_specs, const ks_heads *heads, const ks_host *host,
+                                 const ks_step_out *out, const ks_kernel_out *kout, void *ws, size_t ws_bytes,
+                                 const uint32_t *own, double *lat, hipStream_t stream) {
   Layout L;
   ks_status st = check_common(desc, specs, n_specs, ws, ws_bytes, &L);
   if (st != KS_OK) return st;
@@ -484,9 +485,18 @@ ks_status ks_eval_steps(const ks_desc *desc, const ks_steps *steps, const ks_spe
   f.t_body = out->t_body;
   f.t_gpu = out->t_gpu;
   f.t_step = out->t_step;
+  f.own = own;
+  f.lat = lat;
   e = ks::launch_finish(f, stream);
   if (e != hipSuccess) return hip_fail(e, "step finish launch");
   return KS_OK;
+}
+
+ks_status ks_eval_steps(const ks_desc *desc, const ks_steps *steps, const ks_spec *specs, int32_t n_specs,
+                        const ks_heads *heads, const ks_host *host, const ks_step_out *out,
+                        const ks_kernel_out *kout, void *ws, size_t ws_bytes, hipStream_t stream) {
+  return eval_steps_impl(desc, steps, specs, n_specs, heads, host, out, kout, ws, ws_bytes, nullptr, nullptr,
+                         stream);
 }
 
 ks_status ks_validate(const ks_desc *desc, const ks_steps *steps, const ks_spec *specs, int32_t n_specs, void *ws,
@@ -629,9 +639,7 @@ ks_status ks_expand(const ks_model *model, const ks_batch *batch, int32_t mode, 
   p.o_hidden = out->hidden;
   p.o_tp = out->tp;
   p.o_nlaunch = out->n_launch;
-  hipError_t e = ks::launch_clear(p.err, nullptr, 0, stream);
-  if (e != hipSuccess) return hip_fail(e, "clear launch");
-  e = ks::launch_expand(p, stream, g_ev_before, g_ev_after);
+  hipError_t e = ks::launch_expand(p, stream, g_ev_before, g_ev_after);
   if (e != hipSuccess) return hip_fail(e, "expansion launch");
   return KS_OK;
 }
@@ -648,3 +656,10 @@ const char *ks_last_error(void) { return g_err.c_str(); }
 const char *ks_version(void) { return "ks 0.1.0 (gfx950)"; }
 
 }  // extern "C"
+
+ks_status ks::eval_steps_own(const ks_desc *desc, const ks_steps *steps, const ks_spec *specs, int32_t n_specs,
+                             const ks_heads *heads, const ks_host *host, const ks_step_out *out, void *ws,
+                             size_t ws_bytes, const uint32_t *own, double *lat, hipStream_t stream) {
+  if (!own || !lat) return fail(KS_EINVAL, "own or lat is NULL");
+  return eval_steps_impl(desc, steps, specs, n_specs, heads, host, out, nullptr, ws, ws_bytes, own, lat, stream);
+}

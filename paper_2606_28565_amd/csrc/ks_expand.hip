@@ -14,6 +14,9 @@
 //   k_expand_records  one thread per record: step and slot from the item
 //                     index, fields from the family's templates, stores to
 //                     the record arrays (HBM write stream)
+//   k_expand_small    all of the above (and the flag reset) in one
+//                     workgroup, for batches of at most 1024 steps and 16k
+//                     records (a serving round): one launch instead of five
 #include <hip/hip_runtime.h>
 
 #include "ks_internal.h"
@@ -22,11 +25,10 @@ namespace ks {
 
 constexpr int kTokLanes = 16;
 
-__global__ __launch_bounds__(256) void k_expand_steps(ExpandParams p) {
-  const int sub = threadIdx.x & (kTokLanes - 1);
-  const int64_t groups = ((int64_t)gridDim.x * blockDim.x) / kTokLanes;
+// steps g0, g0 + groups, ... (one group of kTokLanes lanes, lane sub)
+__device__ __forceinline__ void expand_steps(const ExpandParams &p, int64_t g0, int64_t groups, int sub) {
   uint32_t bad = 0;
-  for (int64_t j = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kTokLanes; j < p.n_steps; j += groups) {
+  for (int64_t j = g0; j < p.n_steps; j += groups) {
     uint32_t r0 = p.req_off[j], r1 = p.req_off[j + 1];
     if (r0 > r1 || (int64_t)r1 > p.n_req || (j == 0 && r0 != 0)) {
       bad |= kErrReq;
@@ -51,12 +53,17 @@ __global__ __launch_bounds__(256) void k_expand_steps(ExpandParams p) {
   if (bad) atomicOr(p.err, bad);
 }
 
+__global__ __launch_bounds__(256) void k_expand_steps(ExpandParams p) {
+  expand_steps(p, ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kTokLanes,
+               ((int64_t)gridDim.x * blockDim.x) / kTokLanes, threadIdx.x & (kTokLanes - 1));
+}
+
 // In-block exclusive prefix of the prefill flags: thread t of block b owns
 // steps b 1024 + 4 t .. + 3.
-__global__ __launch_bounds__(256) void k_expand_rank(ExpandParams p) {
+__device__ __forceinline__ void expand_rank(const ExpandParams &p, int64_t blk) {
   __shared__ uint32_t wsum[4];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int64_t j0 = (int64_t)blockIdx.x * kExpandBlk + 4 * tid;
+  const int64_t j0 = blk * kExpandBlk + 4 * tid;
   uint32_t fl[4], cnt = 0;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -79,12 +86,14 @@ __global__ __launch_bounds__(256) void k_expand_rank(ExpandParams p) {
     if (j0 + i < p.n_steps) p.rank[j0 + i] = excl;
     excl += fl[i];
   }
-  if (tid == 255) p.blk[blockIdx.x] = excl;
+  if (tid == 255) p.blk[blk] = excl;
 }
+
+__global__ __launch_bounds__(256) void k_expand_rank(ExpandParams p) { expand_rank(p, blockIdx.x); }
 
 // Exclusive prefix of the block totals in place, 256 at a time; the grand
 // total must equal the batch's n_prefill.
-__global__ __launch_bounds__(256) void k_expand_scan(ExpandParams p) {
+__device__ __forceinline__ void expand_scan(const ExpandParams &p) {
   __shared__ uint32_t wsum[4];
   __shared__ uint64_t carry_s;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -111,6 +120,8 @@ __global__ __launch_bounds__(256) void k_expand_scan(ExpandParams p) {
   if (tid == 0 && (int64_t)carry != p.n_prefill) atomicOr(p.err, kErrPrefill);
 }
 
+__global__ __launch_bounds__(256) void k_expand_scan(ExpandParams p) { expand_scan(p); }
+
 // One record per item.  Attention items are the (step, layer) pairs of all
 // steps: a prefill step's go to ATTN_PREFILL at its rank among prefill
 // steps, the others to ATTN_DECODE at their rank among the rest (an item
@@ -123,12 +134,12 @@ __global__ __launch_bounds__(256) void k_expand_scan(ExpandParams p) {
 // the 2^-20 lift keeps whole quotients whole), the layer from one fp32 FMA
 // (slot / n_tpl with slot < 2^16), the template from selects among the
 // family's at most four, and the record index is 32-bit.
-__global__ __launch_bounds__(256) void k_expand_records(ExpandParams p) {
+__device__ __forceinline__ void expand_records(const ExpandParams &p, int64_t c0, int64_t cstep) {
   const int64_t n_chunks = p.chunk_off[KS_NFAM];
   const int64_t n_pre = p.n_prefill, n_dec = p.n_steps - p.n_prefill;
   uint32_t bad = 0;
   int f = 0;
-  for (int64_t c = blockIdx.x; c < n_chunks; c += gridDim.x) {
+  for (int64_t c = c0; c < n_chunks; c += cstep) {
     while (c >= p.chunk_off[f + 1]) ++f;
     const int64_t i64 = (c - p.chunk_off[f]) * 256 + threadIdx.x;
     if (i64 >= p.item_off[f + 1] - p.item_off[f]) continue;
@@ -183,6 +194,26 @@ __global__ __launch_bounds__(256) void k_expand_records(ExpandParams p) {
   if (bad) atomicOr(p.err, bad);
 }
 
+__global__ __launch_bounds__(256) void k_expand_records(ExpandParams p) { expand_records(p, blockIdx.x, gridDim.x); }
+
+// One workgroup: the flag reset, then each stage in turn, separated by
+// barriers (the per-step T, ranks and block prefix reach the later stages
+// through global memory within the workgroup).
+__global__ __launch_bounds__(256) void k_expand_small(ExpandParams p) {
+  if (threadIdx.x == 0) p.err[0] = 0;
+  __syncthreads();
+  expand_steps(p, threadIdx.x / kTokLanes, 256 / kTokLanes, threadIdx.x & (kTokLanes - 1));
+  __syncthreads();
+  expand_rank(p, 0);
+  __syncthreads();
+  expand_scan(p);
+  __syncthreads();
+  expand_records(p, 0, 1);
+}
+
+// batches the one-workgroup path takes: one rank block, at most 64 chunks
+constexpr int64_t kSmallChunks = 64;
+
 static int grid_cap(int64_t n, int block, int cap) {
   int64_t g = (n + block - 1) / block;
   if (g < 1) g = 1;
@@ -190,9 +221,20 @@ static int grid_cap(int64_t n, int block, int cap) {
 }
 
 hipError_t launch_expand(const ExpandParams &p, hipStream_t s, hipEvent_t before, hipEvent_t after) {
-  if (p.n_steps == 0) return hipSuccess;
+  if (p.n_steps > 0 && p.n_blk == 1 && p.chunk_off[KS_NFAM] <= kSmallChunks) {
+    if (before && after) {
+      const hipError_t e = hipEventRecord(before, s);
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(k_expand_small, dim3(1), dim3(256), 0, s, p);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return before && after ? hipEventRecord(after, s) : hipSuccess;
+  }
+  hipError_t e = launch_clear(p.err, nullptr, 0, s);
+  if (e != hipSuccess || p.n_steps == 0) return e;
   hipLaunchKernelGGL(k_expand_steps, dim3(grid_cap(p.n_steps * kTokLanes, 256, 16384)), dim3(256), 0, s, p);
-  hipError_t e = hipGetLastError();
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_expand_rank, dim3((unsigned)p.n_blk), dim3(256), 0, s, p);
   e = hipGetLastError();
@@ -210,21 +252,6 @@ hipError_t launch_expand(const ExpandParams &p, hipStream_t s, hipEvent_t before
     if (e != hipSuccess) return e;
   }
   return before && after ? hipEventRecord(after, s) : hipSuccess;
-}
-
-// lat[i] = t_step[own[i]][i]: step i's latency under its own spec vector
-// (t_step is [n_specs][n_steps]; the host bounds own[i] below n_specs)
-__global__ void k_gather_own(const double *t_step, int64_t n_steps, const uint32_t *own, double *lat) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n_steps) lat[i] = t_step[(int64_t)own[i] * n_steps + i];
-}
-
-hipError_t launch_gather_own(const double *t_step, int64_t n_steps, const uint32_t *own, double *lat,
-                             hipStream_t s) {
-  if (n_steps <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_gather_own, dim3((unsigned)((n_steps + 255) / 256)), dim3(256), 0, s, t_step, n_steps, own,
-                     lat);
-  return hipGetLastError();
 }
 
 }  // namespace ks

@@ -98,6 +98,9 @@ struct FinishParams {
   const uint32_t *range;               // [KS_NFAM][n_steps][2]
   ks_host host;
   double *t_body, *t_gpu, *t_step;
+  // optional: lat[j] = t_step of step j under spec own[j] (both or neither)
+  const uint32_t *own;
+  double *lat;
 };
 
 struct ValidateParams {
@@ -158,12 +161,16 @@ struct ExpandParams {
   uint32_t *o_layers, *o_hidden, *o_tp, *o_nlaunch;
 };
 
-// events recorded around the record-writing kernel (both null: none)
+// the flag reset and the expansion; events recorded around the
+// record-writing kernel (both null: none)
 hipError_t launch_expand(const ExpandParams &p, hipStream_t s, hipEvent_t before, hipEvent_t after);
 
-// lat[i] = t_step[own[i] * n_steps + i] for i < n_steps (device arrays)
-hipError_t launch_gather_own(const double *t_step, int64_t n_steps, const uint32_t *own, double *lat,
-                             hipStream_t s);
+// ks_eval_steps, and in the same launches lat[j] = t_step of step j under
+// spec own[j] (device arrays of n_steps; own[j] < n_specs, the caller's
+// guarantee): the serving simulation's per-step latencies
+ks_status eval_steps_own(const ks_desc *desc, const ks_steps *steps, const ks_spec *specs, int32_t n_specs,
+                         const ks_heads *heads, const ks_host *host, const ks_step_out *out, void *ws,
+                         size_t ws_bytes, const uint32_t *own, double *lat, hipStream_t stream);
 
 // workspace bytes of one evaluation call for a record layout (family
 // offsets), step count and spec count, without the descriptor's pointers

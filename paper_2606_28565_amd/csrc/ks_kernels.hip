@@ -2246,6 +2246,7 @@ __global__ __launch_bounds__(kFinThreads) void k_finish(FinishParams p, int spec
         p.t_body[o] = res[0][ss * tst + jj];
         p.t_gpu[o] = res[1][ss * tst + jj];
         p.t_step[o] = res[2][ss * tst + jj];
+        if (p.own && p.own[j] == (uint32_t)s) p.lat[j] = res[2][ss * tst + jj];
       }
     }
     __syncthreads();

@@ -393,9 +393,24 @@ ks_status ks_simulate(const ks_model *model, const ks_spec *specs, int32_t n_spe
   std::vector<std::vector<Sched>> batch((size_t)S);
   std::vector<uint8_t> pre((size_t)S), live((size_t)S, 1);
   std::vector<int64_t> who;             // the simulation of each step of the round
-  std::vector<uint32_t> h_off, h_q, h_h, h_spec, h_stage;
+  std::vector<uint32_t> h_off, h_q, h_h, h_spec;
   std::vector<uint8_t> h_pre;
-  std::vector<double> lat((size_t)S);
+  // the round's packed batch and its latencies cross PCIe through pinned
+  // host buffers (asynchronous DMA rather than a staged pageable copy),
+  // sized like the workspace's stage region; each round's synchronization
+  // ends its copies before the buffers are reused
+  struct Pinned {
+    void *p = nullptr;
+    ~Pinned() {
+      if (p) (void)hipHostFree(p);
+    }
+  } pin_stage, pin_lat;
+  const size_t stage_words = (size_t)(S + 1 + 2 * S * L.Q + S + (S + 3) / 4);
+  hipError_t e = hipHostMalloc(&pin_stage.p, stage_words * sizeof(uint32_t), 0);
+  if (e == hipSuccess) e = hipHostMalloc(&pin_lat.p, (size_t)S * sizeof(double), 0);
+  if (e != hipSuccess) return ks::set_error(KS_EHIP, "pinned staging buffers: %s", hipGetErrorString(e));
+  uint32_t *h_stage = static_cast<uint32_t *>(pin_stage.p);
+  double *lat = static_cast<double *>(pin_lat.p);
   while (true) {
     // every unfinished simulation forms its next step
     who.clear();
@@ -443,16 +458,16 @@ ks_status ks_simulate(const ks_model *model, const ks_spec *specs, int32_t n_spe
     uint32_t *d_req_off = d_stage, *d_req_q = d_req_off + (A + 1), *d_req_h = d_req_q + nq;
     uint32_t *d_own = d_req_h + nq;
     uint8_t *d_prefill = reinterpret_cast<uint8_t *>(d_own + A);
-    h_stage.clear();
-    h_stage.insert(h_stage.end(), h_off.begin(), h_off.end());
-    h_stage.insert(h_stage.end(), h_q.begin(), h_q.end());
-    h_stage.insert(h_stage.end(), h_h.begin(), h_h.end());
-    h_stage.insert(h_stage.end(), h_spec.begin(), h_spec.end());
-    const size_t words = h_stage.size();
-    h_stage.resize(words + (size_t)(A + 3) / 4, 0u);
-    std::memcpy(h_stage.data() + words, h_pre.data(), (size_t)A);
-    hipError_t e = hipMemcpyAsync(d_stage, h_stage.data(), h_stage.size() * sizeof(uint32_t),
-                                  hipMemcpyHostToDevice, stream);
+    size_t words = 0;
+    for (const std::vector<uint32_t> *v : {&h_off, &h_q, &h_h, &h_spec}) {
+      std::memcpy(h_stage + words, v->data(), v->size() * sizeof(uint32_t));
+      words += v->size();
+    }
+    const size_t pre_words = (size_t)(A + 3) / 4;
+    std::memset(h_stage + words, 0, pre_words * sizeof(uint32_t));
+    std::memcpy(h_stage + words, h_pre.data(), (size_t)A);
+    words += pre_words;
+    e = hipMemcpyAsync(d_stage, h_stage, words * sizeof(uint32_t), hipMemcpyHostToDevice, stream);
     if (e != hipSuccess) return ks::set_error(KS_EHIP, "batch copy: %s", hipGetErrorString(e));
     ks_batch bt = {A, d_req_off, d_req_q, nq, d_prefill, n_pre};
     int64_t fo[KS_NFAM + 1];
@@ -480,15 +495,17 @@ ks_status ks_simulate(const ks_model *model, const ks_spec *specs, int32_t n_spe
     ks_steps stp = {A, rec.layers, rec.hidden, rec.tp, rec.n_launch};
     ks_step_out so = {d_out, d_out + S * A, d_out + 2 * S * A};
     // every step against every spec (all pairs); each simulation keeps its own
-    st = ks_eval_steps(&d, &stp, specs, n_specs, heads, host, &so, nullptr, w + L.eval, L.eval_bytes, stream);
+    // (and each step's latency under its own simulation's spec, in the same
+    // launches)
+    st = ks::eval_steps_own(&d, &stp, specs, n_specs, heads, host, &so, w + L.eval, L.eval_bytes, d_own, d_lat,
+                            stream);
     if (st != KS_OK) return st;
-    e = ks::launch_gather_own(so.t_step, A, d_own, d_lat, stream);
-    if (e == hipSuccess) e = hipMemcpyAsync(lat.data(), d_lat, A * sizeof(double), hipMemcpyDeviceToHost, stream);
+    e = hipMemcpyAsync(lat, d_lat, A * sizeof(double), hipMemcpyDeviceToHost, stream);
     if (e == hipSuccess) e = hipStreamSynchronize(stream);
     if (e != hipSuccess) return ks::set_error(KS_EHIP, "step latency readback: %s", hipGetErrorString(e));
     for (int64_t i = 0; i < A; ++i) {
       const int64_t s = who[(size_t)i];
-      sims[(size_t)s].advance(batch[(size_t)s], lat[(size_t)i], pre[(size_t)s] != 0, &outs[s]);
+      sims[(size_t)s].advance(batch[(size_t)s], lat[i], pre[(size_t)s] != 0, &outs[s]);
     }
   }
   for (int64_t s = 0; s < S; ++s) sims[(size_t)s].finish(&outs[s]);

@@ -12,17 +12,26 @@
 //   launch_finish     a stand-in step latency,
 //                     t_step = 1e-3 + 2e-7 Q + 1e-4 s + 5e-4 [n_launch > 0]
 //                     (s: the spec index), and t_body = t_gpu = t_step
-//   launch_gather_own each step's latency under its own spec
+//                     and, with own, each step's latency under its own spec
 // and the others do nothing.  The stand-in latency is not the model: the
 // driver prices schedules with it so that the oracle's scheduler, given the
 // same function, must form the same batches.
 #include <hip/hip_runtime_api.h>
 
+#include <cstdlib>
 #include <cstring>
 
 #include "ks_internal.h"
 
 extern "C" {
+hipError_t hipHostMalloc(void **ptr, size_t size, unsigned int) {
+  *ptr = std::malloc(size);
+  return *ptr ? hipSuccess : hipErrorOutOfMemory;
+}
+hipError_t hipHostFree(void *ptr) {
+  std::free(ptr);
+  return hipSuccess;
+}
 hipError_t hipMemcpyAsync(void *dst, const void *src, size_t n, hipMemcpyKind, hipStream_t) {
   if (n) std::memcpy(dst, src, n);
   return hipSuccess;
@@ -44,8 +53,8 @@ hipError_t launch_spec_prep(const ks_spec *, int32_t, SpecC *, uint32_t *, hipSt
 
 hipError_t launch_clear_prep(uint32_t *err, uint32_t *range, int64_t n_range, const ks_spec *specs, int32_t n_specs,
                              SpecC *out, hipStream_t st) {
-  launch_clear(err, range, n_range, st);
-  return launch_spec_prep(specs, n_specs, out, err, st);
+  const hipError_t e = launch_clear(err, range, n_range, st);
+  return e != hipSuccess ? e : launch_spec_prep(specs, n_specs, out, err, st);
 }
 
 hipError_t launch_attn_agg(const uint32_t *req_off, const uint32_t *q, const uint32_t *h, int64_t n_steps,
@@ -84,6 +93,7 @@ hipError_t launch_finish(const FinishParams &p, hipStream_t) {
       p.t_body[i] = t;
       p.t_gpu[i] = t;
       p.t_step[i] = t;
+      if (p.own && p.own[j] == (uint32_t)s) p.lat[j] = t;
     }
   return hipSuccess;
 }
@@ -92,18 +102,13 @@ hipError_t launch_fill_source(const EvalParams &, hipStream_t) { return hipSucce
 hipError_t launch_validate(const ValidateParams &, hipStream_t) { return hipSuccess; }
 
 hipError_t launch_expand(const ExpandParams &p, hipStream_t, hipEvent_t, hipEvent_t) {
+  p.err[0] = 0;
   for (int64_t j = 0; j < p.n_steps; ++j) {
     p.o_layers[j] = p.L;
     p.o_hidden[j] = p.D;
     p.o_tp[j] = p.P;
     p.o_nlaunch[j] = p.prefill[j] ? p.L : 0;
   }
-  return hipSuccess;
-}
-
-hipError_t launch_gather_own(const double *t_step, int64_t n_steps, const uint32_t *own, double *lat,
-                             hipStream_t) {
-  for (int64_t i = 0; i < n_steps; ++i) lat[i] = t_step[(size_t)own[i] * (size_t)n_steps + (size_t)i];
   return hipSuccess;
 }
 
