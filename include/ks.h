@@ -371,8 +371,9 @@ size_t ks_simulate_workspace_bytes(const ks_model* model, const ks_sched* sched,
 /* Runs n_specs simulations (1 .. 256) to completion (synchronous: it waits
  * for each round's latencies on `stream`).  The one entry point that
  * allocates: two pinned HOST buffers for the rounds' copies (the round's
- * batch, at most 4 (1 + n_specs (2 + 2 max_num_seqs)) bytes, and its
- * latencies), freed before it returns.  specs: DEVICE array of n_specs
+ * packed batch, 8 max_num_seqs + 9 bytes per simulation plus 4, and its
+ * latencies, 8 bytes per simulation), freed before it returns.  specs:
+ * DEVICE array of n_specs
  * ks_spec; heads and host as for ks_eval_steps; out: HOST array of n_specs
  * results, out[s] for specs[s] (the same request arrays are read by all).
  * A simulation's results do not depend on the others run beside it, up to
