@@ -765,16 +765,13 @@ struct HeadBF16 {
   // ---- the pieces of one spec's head (mlp4 runs them in order; the
   // software-pipelined spec loop of k_eval spreads the last block's
   // epilogue over the next spec's groups).  kPipe: the heads whose group
-  // schedule that loop knows; kHooks: the groups after which it places the
-  // previous spec's last-block epilogue (four slices), its eta and its tail,
-  // and the next spec's roofline, features and packing.  The epilogue
-  // slices come before the first group that overwrites the last block's
-  // accumulators; the other hooks sit mostly in groups with no VALU work of
-  // their own.
-  // What the pipelined loop does after group I: the previous spec's
-  // last-block epilogue pairs [tp0, tp1), its eta, its tail; the next spec's
-  // roofline, the features in the mask feat, the squares [sq0, sq1) of a
-  // 32-input head, and the packing of layer-1 K chunks [pk0, pk1).
+  // schedule that loop knows.  hook_at(I): what the loop does after group
+  // I: the previous spec's last-block epilogue pairs [tp0, tp1), its eta,
+  // its tail; the next spec's roofline, the features in the mask feat, the
+  // squares [sq0, sq1) of a 32-input head, and the packing of layer-1 K
+  // chunks [pk0, pk1).  The epilogue pairs come before the first group that
+  // overwrites the last block's accumulators; the other pieces sit mostly
+  // in groups with no VALU work of their own.
   struct Hook {
     int tp0, tp1;
     bool eta, tail, roof;
