@@ -144,6 +144,27 @@ struct Cnt {
   uint64_t F, Bt, B, M;
 };
 
+// Expert row counts a0 .. a0 + n - 1 of a grouped GEMM (in bounds: the
+// caller checks), eight loads issued before any is used, so a record's
+// experts cost one memory round trip per eight instead of one each: their
+// sum, the experts with rows, and the 128-row tiles, accumulated in T.
+template <typename T>
+__device__ __forceinline__ void expert_sums(const uint32_t *rows, uint32_t a0, uint32_t n, T &ms, T &act,
+                                            T &tiles) {
+  ms = act = tiles = 0;
+  for (uint32_t e0 = 0; e0 < n; e0 += 8) {
+    uint32_t me[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) me[u] = e0 + u < n ? rows[a0 + e0 + u] : 0u;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      ms += (T)me[u];
+      act += me[u] > 0 ? 1 : 0;
+      tiles += ((T)me[u] + 127) >> 7;
+    }
+  }
+}
+
 // FLOPs F, bytes Bt, thread blocks B and feature row count M of one record.
 __device__ __forceinline__ Cnt record_counts(int fam, uint32_t m32, uint32_t n32, uint32_t k32,
                                              uint32_t a32, uint32_t b32, uint32_t step,
@@ -160,12 +181,7 @@ __device__ __forceinline__ Cnt record_counts(int fam, uint32_t m32, uint32_t n32
     case KS_GROUPED_GEMM: {
       uint64_t ms = 0, act = 0, tiles = 0;
       if ((uint64_t)b32 + A <= (uint64_t)p.n_expert_rows && A <= 1024) {
-        for (uint32_t e = 0; e < a32; ++e) {
-          const uint64_t me = p.expert_rows[b32 + e];
-          ms += me;
-          act += me > 0;
-          tiles += (me + 127) >> 7;
-        }
+        expert_sums(p.expert_rows, b32, a32, ms, act, tiles);
       } else {
         bad |= kErrExpert;
       }
@@ -245,12 +261,7 @@ __device__ __forceinline__ CntF record_counts_f(int fam, uint32_t m32, uint32_t 
     case KS_GROUPED_GEMM: {
       uint32_t ms = 0, act = 0, tiles = 0;
       if ((uint64_t)b32 + a32 <= (uint64_t)p.n_expert_rows && a32 <= 1024) {
-        for (uint32_t e = 0; e < a32; ++e) {
-          const uint32_t me = p.expert_rows[b32 + e];
-          ms += me;
-          act += me > 0;
-          tiles += (me + 127u) >> 7;
-        }
+        expert_sums(p.expert_rows, b32, a32, ms, act, tiles);
       } else {
         bad |= kErrExpert;
       }
