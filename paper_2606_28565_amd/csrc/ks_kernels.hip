@@ -2281,8 +2281,8 @@ __global__ void k_validate(ValidateParams p) {
       if (a > 1024u || (uint64_t)b + a > (uint64_t)p.n_expert_rows) {
         bad |= kErrExpert;
       } else {
-        uint64_t ms = 0;
-        for (uint32_t e = 0; e < a; ++e) ms += p.expert_rows[b + e];
+        uint64_t ms, act, tiles;
+        expert_sums(p.expert_rows, b, a, ms, act, tiles);
         if (ms >= (1ull << 24)) bad |= kErrRange;
       }
     }
