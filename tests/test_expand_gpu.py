@@ -117,6 +117,20 @@ def test_expand_all_or_no_prefill_and_block_edges(prefill):
     check_against_oracle(_Tr(shape, reqs, prefill), False)
 
 
+# A batch of at most 1024 steps (one block of the prefill rank scan) and at
+# most 64 chunks of 256 items takes the one-workgroup expansion: 1024 steps
+# of a one-layer model (about 45 chunks) sit on its edge; 1025 steps, or the
+# same steps of a two-layer model (about 80 chunks), take the multi-kernel
+# path.
+@pytest.mark.parametrize("layers,n_steps", [(1, 1024), (1, 1025), (2, 1024)])
+def test_expand_one_workgroup_path_edges(layers, n_steps):
+    shape = gen.ModelShape("edge", 256, layers, 4, 2, 64, 512)
+    prefill = [(j % 7) == 3 for j in range(n_steps)]
+    reqs = [[(1 + (j % 5), 10 + j)] * (1 + j % 3) for j in range(n_steps)]
+    check_against_oracle(_Tr(shape, reqs, prefill), False)
+    check_against_oracle(_Tr(shape, reqs, prefill), True)
+
+
 def test_expand_empty_steps_and_empty_batch():
     shape = gen.ModelShape("s", 256, 2, 4, 2, 64, 512)
     # steps without requests still dispatch their kernels over 0 tokens
