@@ -1405,11 +1405,13 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
   // them, so that a workgroup meets one or two families and stages their
   // weights into LDS once or twice (striding over the grid it restaged them
   // at nearly every item); with many, striding balances the families'
-  // different per-tile costs better, and the HBM-bound kinds always stride,
-  // which keeps the chip's loads in one window.  (The bounds are
-  // wave-uniform: readfirstlane keeps them in scalar registers.)
+  // different per-tile costs better, and so it does for calls where some
+  // families take the bounded head or a grid (far cheaper tiles than the
+  // MLP's); the HBM-bound kinds always stride, which keeps the chip's loads
+  // in one window.  (The bounds are wave-uniform: readfirstlane keeps them
+  // in scalar registers.)
   const int G = (int)gridDim.x, b = (int)blockIdx.x;
-  const bool blocked = H::kMlp && n_work < kBlockedItems * G;
+  const bool blocked = H::kMlp && !GRID && p.bounded_mask == 0u && n_work < kBlockedItems * G;
   const int w_begin = blocked ? __builtin_amdgcn_readfirstlane(b * (n_work / G) + min(b, n_work % G)) : b;
   const int w_end =
       blocked ? __builtin_amdgcn_readfirstlane(w_begin + n_work / G + (b < n_work % G ? 1 : 0)) : n_work;
