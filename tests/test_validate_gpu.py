@@ -119,7 +119,7 @@ def test_bad_spec_flagged():
     assert st == abi.KS_ERANGE and "spec" in msg
 
 
-@pytest.mark.parametrize("n_specs", [3, 1100])
+@pytest.mark.parametrize("n_specs", [3, 1024, 1025, 1100])
 def test_bad_spec_flagged_by_evaluation(n_specs):
     """A spec vector whose n_cu lies outside 1 .. 65535 is flagged by the
     evaluation call itself: with few specs their constants are formed in the
@@ -135,11 +135,11 @@ def test_bad_spec_flagged_by_evaluation(n_specs):
     assert st == abi.KS_OK, msg
 
 
-def test_many_specs_match_single_spec_calls():
-    """1100 distinct spec vectors in one call (spec constants formed by their
-    own grid) give, spec by spec, the step latencies of a one-spec call (spec
-    constants formed in the clear kernel), bit for bit."""
-    n = 1100
+@pytest.mark.parametrize("n", [1024, 1025, 1100])
+def test_many_specs_match_single_spec_calls(n):
+    """n distinct spec vectors in one call (spec constants formed in the
+    clear kernel up to 1024 specs, by a grid of their own beyond) give, spec
+    by spec, the step latencies of a one-spec call, bit for bit."""
     base = spec(P=1e15, BW=4e12, n_cu=132, t0=2e-6)
     sp = {k: np.repeat(v, n) for k, v in base.items()}
     sp["peak_flops"] = 1e15 * (1.0 + np.arange(n) / n)
@@ -147,7 +147,7 @@ def test_many_specs_match_single_spec_calls():
     sp["n_cu"] = (64 + np.arange(n) % 200).astype(np.int64)
     st, msg, many = _eval_status(_wl(GOOD_ROWS, GOOD_REQS, experts=[3, 0], specs=sp))
     assert st == abi.KS_OK, msg
-    for i in (0, 1, 1023, 1024, n - 1):
+    for i in sorted({0, 1, 1023, min(1024, n - 1), n - 1}):
         one = {k: v[i:i + 1].copy() for k, v in sp.items()}
         st, msg, out = _eval_status(_wl(GOOD_ROWS, GOOD_REQS, experts=[3, 0], specs=one))
         assert st == abi.KS_OK, msg
