@@ -1813,16 +1813,20 @@ __device__ __forceinline__ void store_quad(float *base, int lane, int nvalid, co
 // The sum slots are addressed as the spec's uniform base plus the records'
 // 32-bit byte offsets r.off (the launcher takes this kernel for step sums
 // only when the partial and carry regions span less than 4 GiB), so a spec
-// costs no per-lane address arithmetic.
-template <int VAR, bool BND, class BH>
+// costs no per-lane address arithmetic.  With one or two specs (BUF) a
+// tail's sums are stored after the loop, both specs' in one 16-byte store
+// (its slots are adjacent and 16-byte aligned); with more, each spec's as
+// it is formed.
+template <int VAR, bool BND, bool BUF, class BH>
 __device__ __forceinline__ void stream_specs(const EvalParams &p, const STile &tc, int lane, const SRec &r,
                                              const BH (&bh)[kStreamR], const float (&frb)[kStreamR],
                                              const float (&btf)[kStreamR], double *part, bool any_tail,
                                              const SBnd &q, const float *prm) {
   constexpr bool SUMS = (VAR & kStrSums) != 0, PAIR = (VAR & kStrPair) != 0, MULT = (VAR & kStrMult) != 0;
-  const size_t S = (size_t)p.n_specs;
   const size_t n_rows = (size_t)p.fam_off[KS_NFAM];
-  for (int s = 0; s < p.n_specs; ++s) {
+  // spec s: per-pair outputs, and (SUMS) each record's run sum so far in
+  // v: a tail record's v is its stored sum
+  auto spec = [&](int s, float (&v)[kStreamR]) {
     const SpecC sc = spec_at(p.spec_c, s);
     const float np = sc.n_f * sc.rcp_p;
     float t[kStreamR], tr[kStreamR], eta[kStreamR];
@@ -1874,24 +1878,69 @@ __device__ __forceinline__ void stream_specs(const EvalParams &p, const STile &t
       float acc[kStreamR];
 #pragma unroll
       for (int j = 0; j < kStreamR; ++j) {
-        const float v = MULT ? t[j] * r.mf[j] : t[j];
-        acc[j] = j == 0 ? v : fmaf(r.fj[j], acc[j - 1], v);
+        const float x = MULT ? t[j] * r.mf[j] : t[j];
+        acc[j] = j == 0 ? x : fmaf(r.fj[j], acc[j - 1], x);
       }
       // the run ending at this lane's last record, over the row's lanes so far
       const float x = row_scan(acc[kStreamR - 1], r.g);
       // what the lanes before add to this lane's first run (0 at a row start)
       const float cin = r.fc * __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
                                                            0, __builtin_bit_cast(int, x), 0x111, 0xf, 0xf, true));
-      if (any_tail) {
 #pragma unroll
-        for (int j = 0; j < kStreamR; ++j) {
-          if ((r.ptail >> j) & 1u) {
-            const double v = (double)(((r.first >> j) & 1u) ? acc[j] + cin : acc[j]);
-            *reinterpret_cast<double *>(reinterpret_cast<char *>(part + s) + r.off[j]) = v;
-          }
+      for (int j = 0; j < kStreamR; ++j) v[j] = ((r.first >> j) & 1u) ? acc[j] + cin : acc[j];
+    }
+  };
+  if constexpr (BUF && SUMS) {
+    float v0[kStreamR], v1[kStreamR];
+    spec(0, v0);
+    const bool two = p.n_specs == 2;
+    if (two) spec(1, v1);
+    if (any_tail) {
+      if (two) {
+        typedef double f64x2 __attribute__((ext_vector_type(2)));
+#pragma unroll
+        for (int j = 0; j < kStreamR; ++j)
+          if ((r.ptail >> j) & 1u)
+            *reinterpret_cast<f64x2 *>(reinterpret_cast<char *>(part) + r.off[j]) = f64x2{(double)v0[j], (double)v1[j]};
+      } else {
+#pragma unroll
+        for (int j = 0; j < kStreamR; ++j)
+          if ((r.ptail >> j) & 1u) *reinterpret_cast<double *>(reinterpret_cast<char *>(part) + r.off[j]) = (double)v0[j];
+      }
+    }
+  } else {
+    for (int s = 0; s < p.n_specs; ++s) {
+      float v[kStreamR];
+      spec(s, v);
+      if constexpr (SUMS) {
+        if (any_tail) {
+#pragma unroll
+          for (int j = 0; j < kStreamR; ++j)
+            if ((r.ptail >> j) & 1u) *reinterpret_cast<double *>(reinterpret_cast<char *>(part + s) + r.off[j]) = (double)v[j];
         }
       }
     }
+  }
+}
+
+// the spec loop's instance: bounded head or not, one or two specs (whose
+// sums are stored after the loop) or more
+template <int VAR, class BH>
+__device__ __forceinline__ void stream_dispatch(const EvalParams &p, const STile &tc, int lane, const SRec &r,
+                                                const BH (&bh)[kStreamR], const float (&frb)[kStreamR],
+                                                const float (&btf)[kStreamR], double *part, bool any_tail,
+                                                const SBnd &q, const float *prm, bool bnd) {
+  constexpr bool B = (VAR & kStrBnd) != 0;
+  if (p.n_specs <= 2) {
+    if (bnd)
+      stream_specs<VAR, B, true>(p, tc, lane, r, bh, frb, btf, part, any_tail, q, prm);
+    else
+      stream_specs<VAR, false, true>(p, tc, lane, r, bh, frb, btf, part, any_tail, q, prm);
+  } else {
+    if (bnd)
+      stream_specs<VAR, B, false>(p, tc, lane, r, bh, frb, btf, part, any_tail, q, prm);
+    else
+      stream_specs<VAR, false, false>(p, tc, lane, r, bh, frb, btf, part, any_tail, q, prm);
   }
 }
 
@@ -2001,22 +2050,28 @@ __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc
     const uint32_t rk0 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)r.key[0], 0x150, 0xf, 0xf, false);
     const uint32_t rkp = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)kp, 0x150, 0xf, 0xf, false);
     r.ptail = r.to_carry = r.first = 0;
+    uint32_t heads = 0, ends = 0;   // bit j: record j starts / ends its (family, step) range
 #pragma unroll
     for (int j = 0; j < kStreamR; ++j) {
       const uint32_t key = r.key[j];
       const uint32_t before = j == 0 ? kp : r.key[j - 1];
       const uint32_t after = j == kStreamR - 1 ? kn : r.key[j + 1];
       r.fj[j] = j > 0 && key == before ? 1.0f : 0.0f;
-      // the (family, step) record range, written where its global first and
-      // last records are
-      const uint32_t row = (uint32_t)(tc.row0 + kStreamR * lane + j);
-      if (live[j] && before != key) rng[2 * (size_t)key] = row;
-      if (live[j] && after != key) rng[2 * (size_t)key + 1] = row + 1;
+      heads |= (live[j] && before != key ? 1u : 0u) << j;
+      ends |= (live[j] && after != key ? 1u : 0u) << j;
       // a run's last record within its 64-record tile
       const bool pt = live[j] && (after != key || (j == kStreamR - 1 && row_lane == 15));
       r.ptail |= (pt ? 1u : 0u) << j;
       r.to_carry |= (key == rk0 && rkp == rk0 ? 1u : 0u) << j;
       r.first |= (key == r.key[0] ? 1u : 0u) << j;
+    }
+    // the (family, step) record range, written where its global first and
+    // last records are
+    const uint32_t row_l = (uint32_t)tc.row0 + (uint32_t)(kStreamR * lane);
+#pragma unroll
+    for (int j = 0; j < kStreamR; ++j) {
+      if ((heads >> j) & 1u) rng[2 * (size_t)r.key[j]] = row_l + j;
+      if ((ends >> j) & 1u) rng[2 * (size_t)r.key[j] + 1] = row_l + j + 1;
     }
     any_tail = __ballot(r.ptail != 0) != 0;
     {
@@ -2085,10 +2140,7 @@ __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc
       bh[j] = Bf - 0.5f;
       frb[j] = Ff[j] * rcpf(fmaxf(Bf, 1.0f));
     }
-    if (bnd)
-      stream_specs<VAR, (VAR & kStrBnd) != 0>(p, tc, lane, r, bh, frb, Btf, part, any_tail, q, prm);
-    else
-      stream_specs<VAR, false>(p, tc, lane, r, bh, frb, Btf, part, any_tail, q, prm);
+    stream_dispatch<VAR>(p, tc, lane, r, bh, frb, Btf, part, any_tail, q, prm, bnd);
   } else {
     double bh[kStreamR];
 #pragma unroll
@@ -2096,10 +2148,7 @@ __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc
       bh[j] = (double)B[j] - 0.5;
       frb[j] = Ff[j] * rcpf(fmaxf((float)B[j], 1.0f));
     }
-    if (bnd)
-      stream_specs<VAR, (VAR & kStrBnd) != 0>(p, tc, lane, r, bh, frb, Btf, part, any_tail, q, prm);
-    else
-      stream_specs<VAR, false>(p, tc, lane, r, bh, frb, Btf, part, any_tail, q, prm);
+    stream_dispatch<VAR>(p, tc, lane, r, bh, frb, Btf, part, any_tail, q, prm, bnd);
   }
 }
 
@@ -2139,7 +2188,15 @@ __global__ __launch_bounds__(kWgThreads) __attribute__((amdgpu_waves_per_eu(Stre
 void k_stream(EvalParams p) {
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int stride = (int)gridDim.x * kWgWaves;
-  int wt = (int)blockIdx.x * kWgWaves + wave;
+  // Workgroups go to the eight XCDs round-robin (workgroup b to XCD b mod
+  // 8).  With step sums they are renumbered so that each XCD takes one
+  // contiguous eighth of the tiles of every pass over the grid: the partial
+  // sums and record ranges of consecutive steps (several to a cache line)
+  // are then written from one XCD's L2 instead of up to eight, each holding
+  // a partial line (per-pair outputs alone measured faster without it).
+  int b = (int)blockIdx.x;
+  if ((VAR & kStrSums) != 0 && (gridDim.x & 7u) == 0u) b = (b & 7) * (int)(gridDim.x >> 3) + (b >> 3);
+  int wt = b * kWgWaves + wave;
   stream_family<KS_GEMM, VAR>(p, wt, stride, lane);
   stream_family<KS_LM_HEAD, VAR>(p, wt, stride, lane);
   stream_family<KS_GROUPED_GEMM, VAR>(p, wt, stride, lane);
