@@ -1367,7 +1367,9 @@ template <class H> struct PipeOK<H, std::enable_if_t<H::kPipe>> : std::true_type
 template <bool MULT>
 __device__ __forceinline__ void spec_tail(const EvalParams &p, int s, float t_roof, float eta, float t, bool valid,
                                           bool live, int64_t row, float tfac, const float (&fac)[6], double *dst) {
-  if (valid) {
+  // (the per-pair test first: a call without per-pair outputs forms no
+  // address)
+  if ((p.o_troof || p.o_eta || p.o_t) && valid) {
     const size_t i = (size_t)s * (size_t)p.fam_off[KS_NFAM] + (size_t)row;
     if (p.o_troof) p.o_troof[i] = t_roof;
     if (p.o_eta) p.o_eta[i] = eta;
