@@ -1401,8 +1401,12 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
   // the next tile's fields are loaded while the current one is evaluated
   Tile tn = {};
   Fields fn = {0, 0, 0, 0, 0, 0, kNoKey, kNoKey, kNoKey, 1.0f};
-  // tiles without a head take their neighbour steps by a vector load
-  constexpr bool VEC = !H::kMlp;
+  // tiles without a head, and the heads that run one wave per SIMD, take
+  // their neighbour steps by a vector load (the scalar loads' round trip is
+  // waited for by the next scalar or LDS wait, which one wave per SIMD
+  // cannot cover; with two waves per SIMD the vector load measured no
+  // better overall)
+  constexpr bool VEC = !H::kMlp || MinWg<KIND>::value == 1;
   // With few work items per workgroup the heads take a contiguous range of
   // them, so that a workgroup meets one or two families and stages their
   // weights into LDS once or twice (striding over the grid it restaged them
