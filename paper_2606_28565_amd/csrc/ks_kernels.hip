@@ -1684,6 +1684,7 @@ struct SBnd {
   float zg[kStreamR], za[kStreamR];   // g . x and a . x over x0, x8 .. x15
   float la[kStreamR];                 // log2(F / max(Bt, 1))
   float bf[kStreamR];                 // B
+  float rb[kStreamR];                 // 1 / max(B, 1)
   float rbt[kStreamR];                // 1 / max(Bt, 1)
 };
 
@@ -1849,7 +1850,7 @@ __device__ __forceinline__ void stream_specs(const EvalParams &p, const STile &t
         // x1 .. x7 of this spec (Sec. 5.3 feature list; u = W N / B, and
         // a record without blocks has u = 1), then the bounded head
 #pragma clang fp contract(off)
-        const float u = q.bf[j] > 0.0f ? W * sc.n_f * rcpf(q.bf[j]) : 1.0f;
+        const float u = q.bf[j] > 0.0f ? W * sc.n_f * q.rb[j] : 1.0f;   // (1 / B for B >= 1)
         float x[8];
         x[1] = fmaxf(q.la[j] + sc.lr, -20.0f) * (1.0f / 16);
         x[2] = log2f_fast(fmaf(q.bf[j], sc.rcp_n, 1.0f)) * (1.0f / 16);
@@ -2112,6 +2113,7 @@ __device__ __forceinline__ void stream_tile(const EvalParams &p, const STile &tc
         const float bf = (float)B[j];
         const float rb = rcpf(fmaxf(bf, 1.0f));
         q.bf[j] = bf;
+        q.rb[j] = rb;
         q.rbt[j] = rcpf(fmaxf(Btf[j], 1.0f));
         // log2(0) = -inf for F = 0; the clamps of x0 and x1 take it
         q.la[j] = log2f_fast(Ff[j] * q.rbt[j]);
