@@ -1384,6 +1384,17 @@ __device__ __forceinline__ void spec_tail(const EvalParams &p, int s, float t_ro
 // work items per workgroup below which the heads take contiguous ranges
 constexpr int kBlockedItems = 32;
 
+// the workgroup tile and the spec range of work item w: w / n and w % n,
+// with no integer division in the usual case of one range of all specs
+__device__ __forceinline__ int item_tile(int w, int n) {
+  if (n == 1) return w;
+  return w / n;
+}
+__device__ __forceinline__ int item_range(int w, int n) {
+  if (n == 1) return 0;
+  return w % n;
+}
+
 template <int KIND, int VAR>
 __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalParams p) {
   constexpr bool GRID = (VAR & kVarGrid) != 0;
@@ -1423,17 +1434,17 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
       blocked ? __builtin_amdgcn_readfirstlane(w_begin + n_work / G + (b < n_work % G ? 1 : 0)) : n_work;
   const int w_step = blocked ? 1 : G;
   if (w_begin < w_end) {
-    tn = locate(p, w_begin / n_chunks, wave, 0);
+    tn = locate(p, item_tile(w_begin, n_chunks), wave, 0);
     fn = load_fields<MULT, VEC>(p, tn, lane);
   }
   for (int w = w_begin; w < w_end; w += w_step) {
     const Tile tc = tn;
     const Fields fc = fn;
     if (w + w_step < w_end) {
-      tn = locate(p, (w + w_step) / n_chunks, wave, tc.fam);
+      tn = locate(p, item_tile(w + w_step, n_chunks), wave, tc.fam);
       fn = load_fields<MULT, VEC>(p, tn, lane);
     }
-    const int s_lo = (w % n_chunks) * p.spec_chunk;
+    const int s_lo = item_range(w, n_chunks) * p.spec_chunk;
     const int s_hi = min(s_lo + p.spec_chunk, p.n_specs);
     const int fam = tc.fam;
     // this family takes the bounded head (the plain eta = 1 stream has none)
