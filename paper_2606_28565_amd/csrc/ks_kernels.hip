@@ -595,13 +595,31 @@ struct HeadBF16 {
       const int k0 = kc * 16 + (lane >> 5) * 8 + 2 * q;
       lds[d] = raw_scaled(w1[row * IN + k0], k0) | (raw_scaled(w1[row * IN + k0 + 1], k0 + 1) << 16);
     }
-    for (int d = threadIdx.x; d < W2_DW; d += kWgThreads) {
-      const int q = d & 3, lane = (d >> 2) & 63, frag = d >> 8;
-      const int kc = frag % KC2, mb = frag / KC2;
-      const int row = mb * 32 + (lane & 31);
-      const int s0 = (lane >> 5) * 8 + 2 * q;
-      lds[OFF_W2 + d] = (uint32_t)w2[row * HID + hid_of(kc, s0)] |
-                        ((uint32_t)w2[row * HID + hid_of(kc, s0 + 1)] << 16);
+    if ((reinterpret_cast<uintptr_t>(w2) & 15) == 0) {
+      // W2 by 16-byte row chunks: hidden units 8 c8 .. 8 c8 + 7 of a row are,
+      // by hid_of, slots 0-3 of lane (row mod 32) and of lane (row mod 32) +
+      // 32 of one K chunk's fragment, at dwords 0-1 (first 8 of the chunk's
+      // 16 units) or 2-3 (last 8): each load feeds two 8-byte LDS writes
+      // (one 2-byte load per unit, scattered, took several times longer)
+      for (int c = threadIdx.x; c < HID * HID / 8; c += kWgThreads) {
+        const int row = c / (HID / 8), col = (c % (HID / 8)) * 8;
+        const u32x4 v = *reinterpret_cast<const u32x4 *>(w2 + (size_t)row * HID + col);
+        const int kc = 2 * (col >> 5) + ((col >> 4) & 1);
+        const int frag = (row >> 5) * KC2 + kc;
+        const int d0 = (frag * 64 + (row & 31)) * 4 + ((col & 8) ? 2 : 0);
+        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+        *reinterpret_cast<u32x2 *>(lds + OFF_W2 + d0) = u32x2{v[0], v[1]};
+        *reinterpret_cast<u32x2 *>(lds + OFF_W2 + d0 + 32 * 4) = u32x2{v[2], v[3]};
+      }
+    } else {
+      for (int d = threadIdx.x; d < W2_DW; d += kWgThreads) {
+        const int q = d & 3, lane = (d >> 2) & 63, frag = d >> 8;
+        const int kc = frag % KC2, mb = frag / KC2;
+        const int row = mb * 32 + (lane & 31);
+        const int s0 = (lane >> 5) * 8 + 2 * q;
+        lds[OFF_W2 + d] = (uint32_t)w2[row * HID + hid_of(kc, s0)] |
+                          ((uint32_t)w2[row * HID + hid_of(kc, s0 + 1)] << 16);
+      }
     }
     for (int d = threadIdx.x; d < B2_DW; d += kWgThreads) {
       const int r = d & 15, g = (d >> 4) & 1, mb = d >> 5;
