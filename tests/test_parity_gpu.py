@@ -259,6 +259,41 @@ def test_every_head_kind_stress(precision, in_dim, hidden):
     assert g.rel_err(gpu["eta"], ref["eta"]).max() <= REL_BF16
 
 
+@pytest.mark.parametrize("in_dim,hidden", [(16, 128), (32, 256), (16, 64)])
+def test_bf16_weights_at_unaligned_addresses(in_dim, hidden):
+    """The bf16 heads stage W2 into LDS by 16-byte row chunks when its
+    address allows, else element by element: W1 and W2 passed two bytes past
+    a 16-byte boundary give outputs bit-identical to the aligned call."""
+    import torch
+    wl = gen.config1(0, 4).with_heads(gen.make_heads(in_dim, hidden, "bf16"))
+    di = abi.DeviceInputs(wl)
+
+    def run(heads):
+        so_t, so = abi.step_outputs(wl.desc.n_steps, di.n_specs)
+        ko_t, ko = abi.kernel_outputs(wl.desc.n_rows, di.n_specs, counts=False)
+        abi.ks_eval_steps(di.desc, di.steps, di.specs_ptr, di.n_specs, heads, di.host, so, ko,
+                          di.ws_ptr, di.ws_bytes, abi.current_stream())
+        torch.cuda.synchronize()
+        abi.ks_device_status(di.ws_ptr, di.ws_bytes, abi.current_stream())
+        return {k: v.cpu().numpy() for k, v in list(so_t.items()) + list(ko_t.items())}
+
+    aligned = run(di.make_heads("bf16", in_dim, hidden, abi.KS_ETA_MLP))
+    heads = di.make_heads("bf16", in_dim, hidden, abi.KS_ETA_MLP)
+    keep = []
+    for name in ("w1", "w2"):
+        t = di.heads_t[name]
+        buf = torch.zeros(t.numel() + 16, dtype=t.dtype, device=t.device)
+        base = (-buf.data_ptr() % 16) // t.element_size() + 1   # one element past a 16-byte boundary
+        buf[base:base + t.numel()] = t
+        keep.append(buf)
+        ptr = buf.data_ptr() + base * t.element_size()
+        assert ptr % 16 == 2
+        setattr(heads, name, ptr)
+    unaligned = run(heads)
+    for k in aligned:
+        np.testing.assert_array_equal(unaligned[k], aligned[k], err_msg=k)
+
+
 # ------------------------------------------------------------- edge cases --
 def _wl(desc, n_steps, heads=None, tp=1, layers=1, specs=None):
     return gen.Workload("edge", desc, steprec(n_steps, layers=layers, hidden=64, tp=tp, n_launch=1),
