@@ -583,12 +583,20 @@ struct HeadBF16 {
     return __builtin_bit_cast(uint32_t, f) >> 16;
   }
   __device__ static void stage(uint32_t *lds, int fam, const EvalParams &p) {
+    // The two-wave heads (hidden 64 and 128, 256 registers) take the thread
+    // index through an opaque copy, so that the per-thread addresses of
+    // these loops are formed here, when a family is staged, rather than
+    // hoisted out of the work loop and kept live across it (the 16-128 head
+    // spilled them to scratch); the one-wave heads keep the hoisted form
+    // (the opaque copy there made their scalar spills to VGPR lanes grow).
+    int tid = (int)threadIdx.x;
+    if constexpr (HID <= 128) asm volatile("" : "+v"(tid));
     const uint16_t *w1 = (const uint16_t *)p.w1 + (size_t)fam * HID * IN;
     const uint16_t *w2 = (const uint16_t *)p.w2 + (size_t)fam * HID * HID;
     const uint16_t *b2 = (const uint16_t *)p.b2 + (size_t)fam * HID;
     const uint16_t *w3 = (const uint16_t *)p.w3 + (size_t)fam * HID;
     const uint16_t *b3 = (const uint16_t *)p.b3 + fam;
-    for (int d = threadIdx.x; d < W1_DW; d += kWgThreads) {
+    for (int d = tid; d < W1_DW; d += kWgThreads) {
       const int q = d & 3, lane = (d >> 2) & 63, frag = d >> 8;
       const int kc = frag % KC1, mb = frag / KC1;
       const int row = mb * 32 + (lane & 31);
@@ -601,7 +609,7 @@ struct HeadBF16 {
       // 32 of one K chunk's fragment, at dwords 0-1 (first 8 of the chunk's
       // 16 units) or 2-3 (last 8): each load feeds two 8-byte LDS writes
       // (one 2-byte load per unit, scattered, took several times longer)
-      for (int c = threadIdx.x; c < HID * HID / 8; c += kWgThreads) {
+      for (int c = tid; c < HID * HID / 8; c += kWgThreads) {
         const int row = c / (HID / 8), col = (c % (HID / 8)) * 8;
         const u32x4 v = *reinterpret_cast<const u32x4 *>(w2 + (size_t)row * HID + col);
         const int kc = 2 * (col >> 5) + ((col >> 4) & 1);
@@ -612,7 +620,7 @@ struct HeadBF16 {
         *reinterpret_cast<u32x2 *>(lds + OFF_W2 + d0 + 32 * 4) = u32x2{v[2], v[3]};
       }
     } else {
-      for (int d = threadIdx.x; d < W2_DW; d += kWgThreads) {
+      for (int d = tid; d < W2_DW; d += kWgThreads) {
         const int q = d & 3, lane = (d >> 2) & 63, frag = d >> 8;
         const int kc = frag % KC2, mb = frag / KC2;
         const int row = mb * 32 + (lane & 31);
@@ -621,15 +629,15 @@ struct HeadBF16 {
                           ((uint32_t)w2[row * HID + hid_of(kc, s0 + 1)] << 16);
       }
     }
-    for (int d = threadIdx.x; d < B2_DW; d += kWgThreads) {
+    for (int d = tid; d < B2_DW; d += kWgThreads) {
       const int r = d & 15, g = (d >> 4) & 1, mb = d >> 5;
       lds[OFF_B2 + d] = __builtin_bit_cast(uint32_t, bf16_to_f32(b2[out_of(mb, g, r)]));
     }
-    for (int d = threadIdx.x; d < W3_DW; d += kWgThreads) {
+    for (int d = tid; d < W3_DW; d += kWgThreads) {
       const int r = d & 15, g = (d >> 4) & 1, mb = d >> 5;
       lds[OFF_W3 + d] = __builtin_bit_cast(uint32_t, bf16_to_f32(w3[out_of(mb, g, r)]));
     }
-    if (threadIdx.x == 0) lds[OFF_B3] = __builtin_bit_cast(uint32_t, bf16_to_f32(b3[0]));
+    if (tid == 0) lds[OFF_B3] = __builtin_bit_cast(uint32_t, bf16_to_f32(b3[0]));
   }
 
   // layer 3 over one 32-unit block of layer 2, in fp32: z += w3 . relu(h2)
@@ -1419,7 +1427,7 @@ __global__ __launch_bounds__(kWgThreads, MinWg<KIND>::value) void k_eval(EvalPar
   constexpr bool MULT = (VAR & kVarMult) != 0;
   using H = typename KindOf<KIND>::H;
   constexpr int IN = KindOf<KIND>::IN;
-  __shared__ uint32_t lds[H::LDS_DW];
+  __shared__ __align__(16) uint32_t lds[H::LDS_DW];   // 16-byte fragment reads, 8-byte staging writes
   __shared__ float bnd_lds[32];   // the bounded head of the staged family: g then a
   __shared__ float grid_lds[KS_GRID_MAX_NODES];   // the staged family's measured grid
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
